@@ -1,0 +1,255 @@
+"""CPU oracle for Plan7 profile-HMM database search (ctypes over hmm_oracle.c).
+
+TEST INFRASTRUCTURE.  Only the test suite, the package smoke check and the
+benchmark's CPU-baseline leg may import this package.  It shares no code
+with the GPU library (paper_2111_06340_amd); both consume the seeded inputs
+of the `synth` package and nothing else in common.
+
+Functions take numpy arrays and return Python scalars / numpy arrays.
+Score conversions to bits and the score calibration below follow the
+readings stated in hmm_oracle.c (lambda = ln 2 per bit, Gumbel law for the
+MSV and Viterbi filter scores, exponential tail for Forward).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "hmm_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+S8 = 3.0 / math.log(2.0)
+S16 = 500.0 / math.log(2.0)
+BASE8 = 190
+LN2 = math.log(2.0)
+
+F_MSV_PASS, F_MSV_OVF, F_VIT_RAN, F_VIT_PASS, F_VIT_OVF, F_FWD_RAN, F_FWD_PASS = (
+    0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (scalar on purpose: -O2 -fno-tree-vectorize)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fno-tree-vectorize", "-std=c11", "-D_GNU_SOURCE",
+                               "-Wall", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm", "-lpthread"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def build_variant(src_text: str, out_path: str) -> str:
+    """Compile a modified copy of the oracle source (mutation tests)."""
+    src = out_path + ".c"
+    with open(src, "w") as f:
+        f.write(src_text)
+    subprocess.check_call(["gcc", "-O1", "-std=c11", "-D_GNU_SOURCE", "-w", "-shared", "-fPIC",
+                           "-o", out_path, src, "-lm", "-lpthread"])
+    return out_path
+
+
+def source_text() -> str:
+    with open(_SRC) as f:
+        return f.read()
+
+
+def load(path: str):
+    """Load an oracle build and declare its signatures."""
+    L = C.CDLL(path)
+    vp, ip, dp = C.c_void_p, C.c_int, C.c_double
+    L.orc_profile_new.restype = vp
+    L.orc_profile_new.argtypes = [ip, vp, vp, vp, vp]
+    L.orc_profile_free.argtypes = [vp]
+    L.orc_profile_scalars.argtypes = [vp, vp]
+    L.orc_profile_tables.argtypes = [vp, vp, vp, vp, vp]
+    for f in ("orc_loop", "orc_move", "orc_null"):
+        getattr(L, f).restype = dp
+        getattr(L, f).argtypes = [ip]
+    for f in ("orc_move8", "orc_move16"):
+        getattr(L, f).restype = ip
+        getattr(L, f).argtypes = [ip]
+    L.orc_thresholds.argtypes = [vp, vp, ip, vp, vp, vp]
+    L.orc_msv.restype = ip
+    L.orc_msv.argtypes = [vp, vp, ip, vp]
+    L.orc_vit16.restype = ip
+    L.orc_vit16.argtypes = [vp, vp, ip, vp]
+    L.orc_vit32.restype = C.c_int32
+    L.orc_vit32.argtypes = [vp, vp, ip]
+    for f in ("orc_vit_f64", "orc_fwd_f64", "orc_fwd_f64_scaled"):
+        getattr(L, f).restype = dp
+        getattr(L, f).argtypes = [vp, vp, ip]
+    L.orc_search.restype = ip
+    L.orc_search.argtypes = [vp, vp, vp, C.c_int64, vp, vp, ip, ip, vp, vp, vp, vp, vp]
+    return L
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = load(_LIB)
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+class OracleProfile:
+    """Oracle-side scores and integer tables of one profile."""
+
+    def __init__(self, prof, library=None):
+        self.lib = lib() if library is None else library
+        self.M = int(prof.M)
+        self._keep = [np.ascontiguousarray(prof.bg, np.float64),
+                      np.ascontiguousarray(prof.match, np.float64),
+                      np.ascontiguousarray(prof.insert, np.float64).reshape(-1),
+                      np.ascontiguousarray(prof.trans, np.float64).reshape(-1)]
+        if self._keep[2].size == 0:
+            self._keep[2] = np.zeros(1)
+            self._keep[3] = np.zeros(1)
+        self.h = self.lib.orc_profile_new(self.M, *[_ptr(a) for a in self._keep])
+        if not self.h:
+            raise ValueError("oracle rejected the profile")
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h:
+            self.lib.orc_profile_free(h)
+            self.h = None
+
+    def scalars(self) -> dict:
+        out = np.zeros(5, np.int32)
+        self.lib.orc_profile_scalars(self.h, _ptr(out))
+        return dict(bias8=int(out[0]), entry8=int(out[1]), exit8=int(out[2]),
+                    entry16=int(out[3]), ej16=int(out[4]))
+
+    def tables(self) -> dict:
+        M = self.M
+        cost8 = np.zeros((M, 20), np.uint8)
+        msc16 = np.zeros((M, 20), np.int16)
+        isc16 = np.zeros((max(M - 1, 1), 20), np.int16)
+        t16 = np.zeros((max(M - 1, 1), 7), np.int16)
+        self.lib.orc_profile_tables(self.h, _ptr(cost8), _ptr(msc16), _ptr(isc16), _ptr(t16))
+        return dict(cost8=cost8, msc16=msc16, isc16=isc16[:M - 1], t16=t16[:M - 1])
+
+
+def _seq(x) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.uint8)
+    if x.size < 1:
+        raise ValueError("empty sequence")
+    return x
+
+
+def msv(p: OracleProfile, x) -> tuple[int, int]:
+    x = _seq(x)
+    ovf = C.c_int(0)
+    r = p.lib.orc_msv(p.h, _ptr(x), x.size, C.byref(ovf))
+    return int(r), int(ovf.value)
+
+
+def vit16(p: OracleProfile, x) -> tuple[int, int]:
+    x = _seq(x)
+    ovf = C.c_int(0)
+    r = p.lib.orc_vit16(p.h, _ptr(x), x.size, C.byref(ovf))
+    return int(r), int(ovf.value)
+
+
+def vit32(p: OracleProfile, x) -> int:
+    x = _seq(x)
+    return int(p.lib.orc_vit32(p.h, _ptr(x), x.size))
+
+
+def vit_f64(p: OracleProfile, x) -> float:
+    x = _seq(x)
+    return float(p.lib.orc_vit_f64(p.h, _ptr(x), x.size))
+
+
+def fwd_f64(p: OracleProfile, x) -> float:
+    x = _seq(x)
+    return float(p.lib.orc_fwd_f64(p.h, _ptr(x), x.size))
+
+
+def fwd_f64_scaled(p: OracleProfile, x) -> float:
+    x = _seq(x)
+    return float(p.lib.orc_fwd_f64_scaled(p.h, _ptr(x), x.size))
+
+
+def length_params(L: int, library=None) -> dict:
+    l = lib() if library is None else library
+    return dict(loop=l.orc_loop(L), move=l.orc_move(L), null=l.orc_null(L),
+                move8=l.orc_move8(L), move16=l.orc_move16(L))
+
+
+def thresholds(calib, F, L: int) -> tuple[int, int, float]:
+    c = np.asarray(calib, np.float64)
+    f = np.asarray(F, np.float64)
+    t8, t16, ft = C.c_int32(0), C.c_int32(0), C.c_double(0)
+    lib().orc_thresholds(_ptr(c), _ptr(f), L, C.byref(t8), C.byref(t16), C.byref(ft))
+    return int(t8.value), int(t16.value), float(ft.value)
+
+
+# ------------------------------------------------------------ bit scores
+
+def msv_bits(raw: int, L: int) -> float:
+    return ((raw - BASE8) / S8 - 3.0 - lib().orc_null(L)) / LN2
+
+
+def vit_bits(v: int, L: int) -> float:
+    return (v / S16 - 3.0 - lib().orc_null(L)) / LN2
+
+
+def fwd_bits(f: float, L: int) -> float:
+    return (f - lib().orc_null(L)) / LN2
+
+
+def gumbel_mu(bits: np.ndarray, lam: float = LN2) -> float:
+    """Maximum-likelihood Gumbel location with the slope fixed at lam."""
+    b = np.asarray(bits, np.float64)
+    return float(-math.log(np.mean(np.exp(-lam * b))) / lam)
+
+
+def calibrate(p: OracleProfile, nthreads: int = 8, n: int = 200) -> tuple[float, float, float]:
+    """(mu_msv, mu_vit, tau) in bits from oracle scores of i.i.d. background
+    sequences: n of length 200 for the filters, n of length 100 for Forward;
+    tau puts a tail mass of 0.04 at the 8th-largest Forward score."""
+    from synth import gen
+    db = gen.random_sequences(gen.SEED_CALIB_VIT, n, 200)
+    r = search(p, db.residues, db.offsets, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0), nthreads)
+    mu_msv = gumbel_mu([msv_bits(int(v), 200) for v in r["msv"]])
+    mu_vit = gumbel_mu([vit_bits(int(v), 200) for v in r["vit"]])
+    dbf = gen.random_sequences(gen.SEED_CALIB_FWD, n, 100)
+    rf = search(p, dbf.residues, dbf.offsets, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0), nthreads)
+    fb = np.sort([fwd_bits(float(v), 100) for v in rf["fwd"]])[::-1]
+    tail = 0.04
+    xc = fb[int(round(tail * n)) - 1]
+    tau = float(xc + math.log(tail) / LN2)
+    return mu_msv, mu_vit, tau
+
+
+def search(p: OracleProfile, residues, offsets, calib, F, nthreads: int = 8,
+           fwd_scaled: bool = False) -> dict:
+    """Filter pipeline over a whole database, caller order."""
+    res = np.ascontiguousarray(residues, np.uint8)
+    off = np.ascontiguousarray(offsets, np.int64)
+    n = off.size - 1
+    out = dict(msv=np.zeros(n, np.int16), vit=np.zeros(n, np.int32),
+               fwd=np.zeros(n, np.float64), flags=np.zeros(n, np.uint8),
+               stage_s=np.zeros(3, np.float64))
+    c = np.asarray(calib, np.float64)
+    f = np.asarray(F, np.float64)
+    rc = p.lib.orc_search(p.h, _ptr(res if res.size else np.zeros(1, np.uint8)), _ptr(off),
+                          n, _ptr(c), _ptr(f), int(nthreads), int(fwd_scaled),
+                          _ptr(out["msv"]), _ptr(out["vit"]), _ptr(out["fwd"]),
+                          _ptr(out["flags"]), _ptr(out["stage_s"]))
+    if rc != 0:
+        raise ValueError("oracle search rejected its input")
+    return out
