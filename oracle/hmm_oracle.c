@@ -139,8 +139,10 @@ orc_profile *orc_profile_new(int M, const double *bg, const double *match,
   /* Viterbi */
   for (int i = 0; i < M * KA; i++)
     p->msc16[i] = (int16_t)clampl(qround(ORC_S16 * p->msc[i]), -32768, 32767);
+  /* a zero insert probability scores -inf: the int16 floor */
   for (int i = 0; i < Mi * KA; i++)
-    p->isc16[i] = (int16_t)clampl(qround(ORC_S16 * p->isc[i]), -32768, 32767);
+    p->isc16[i] = insert[i] > 0.0 ? (int16_t)clampl(qround(ORC_S16 * p->isc[i]), -32768, 32767)
+                                  : (int16_t)ORC_NEG16;
   for (int i = 0; i < Mi * 7; i++)
     p->t16[i] = trans[i] > 0.0 ? (int16_t)clampl(qround(ORC_S16 * p->tr[i]), -32768, 32767)
                                : (int16_t)ORC_NEG16;
