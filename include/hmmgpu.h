@@ -1,0 +1,204 @@
+/*
+ * hmmgpu.h -- C ABI of the MI355X (gfx950) Plan7 profile-HMM database search.
+ *
+ * The paper (ParaFold, arXiv 2111.06340, Background section) identifies the
+ * jackhmmer searches of UniRef90 and MGnify as the CPU-bound core of
+ * AlphaFold's MSA construction; its Research Motivation and Evaluation
+ * sections show that CPU stage dominating end-to-end time.  The data-parallel
+ * core of such a search is: score one profile HMM against every sequence of
+ * a large database, through a cascade of filters.  This library runs that
+ * cascade on one GPU:
+ *
+ *   MSV      uint8 saturating, multi-segment ungapped, on every target
+ *   Viterbi  int16 saturating, gapped local, on MSV survivors
+ *            (targets that saturate int16 are rescored exactly in int32)
+ *   Forward  fp32 sum over all paths, on Viterbi survivors
+ *
+ * The model, its integer score systems and the filter cutoffs are not given
+ * in the paper; the library fixes them as follows (all logs natural):
+ *   - alphabet of 20 residues, codes 0..19 = A C D E F G H I K L M N P Q R S
+ *     T V W Y;
+ *   - match/insert scores ln(e/f), transitions ln t (t = 0 allowed);
+ *   - local multihit configuration: entry ln(2/(M(M+1))) to every match
+ *     state, free exit from every M and D state, E->C = E->J = ln 1/2,
+ *     N/C/J loops ln(L/(L+3)), moves ln(3/(L+3));
+ *   - MSV in 1/3-bit uint8 units (offset 190, per-profile bias), Viterbi in
+ *     1/500-bit int16 units, both with the N/C/J loops omitted;
+ *   - P-values with slope ln 2 per bit: Gumbel law for MSV and Viterbi
+ *     (location mu), exponential tail for Forward (location tau).
+ *
+ * Conventions for every entry point:
+ *   - return 0 (HMM_OK) on success, a negative HMM_E* code on failure;
+ *     hmm_last_error() then holds a thread-local message;
+ *   - all argument validation happens on the host before any GPU call, so a
+ *     rejected call leaves no work enqueued and writes no output;
+ *   - a stream argument is a hipStream_t (NULL = the default stream).
+ */
+#ifndef HMMGPU_H
+#define HMMGPU_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HMM_OK 0
+#define HMM_EINVAL (-1)   /* bad argument: NULL pointer, M < 1, bad probabilities, bad residue code, empty sequence, offsets not increasing */
+#define HMM_ERANGE (-2)   /* size beyond a library limit (M > HMM_MAX_M, sequence longer than HMM_MAX_LEN) */
+#define HMM_ENOMEM (-3)   /* host or device allocation failed */
+#define HMM_EDEVICE (-4)  /* a HIP runtime call failed; the message carries the HIP error string */
+
+#define HMM_K 20          /* alphabet size */
+#define HMM_MAX_M 3072    /* profile length limit: the MSV cost table must fit in LDS */
+#define HMM_MAX_LEN 100000 /* target length limit */
+
+/* Per-target flag bits written by hmm_search. */
+#define HMM_MSV_PASS 0x01 /* passed the MSV filter (always set when MSV overflowed) */
+#define HMM_MSV_OVF 0x02  /* MSV saturated uint8; msv = 255 */
+#define HMM_VIT_RAN 0x04  /* Viterbi was computed */
+#define HMM_VIT_PASS 0x08 /* passed the Viterbi filter (always set when Viterbi overflowed) */
+#define HMM_VIT_OVF 0x10  /* Viterbi saturated int16; vit holds the exact int32 rescore */
+#define HMM_FWD_RAN 0x20  /* Forward was computed */
+#define HMM_FWD_PASS 0x40 /* Forward score passed the F3 cutoff (set for every Forward target when F3 >= 1) */
+
+typedef struct hmm_profile hmm_profile; /* opaque; library-owned; immutable after upload */
+typedef struct hmm_db hmm_db;           /* opaque; library-owned; holds the packed database and search scratch */
+typedef void *hmm_stream;               /* hipStream_t */
+
+/* Probability-space profile, copied by hmm_profile_upload (fp64, row-major).
+ *   bg[20]           background residue frequencies f(a)
+ *   match[M][20]     match emissions of nodes 1..M
+ *   insert[M-1][20]  insert emissions of nodes 1..M-1 (may be NULL when M = 1)
+ *   trans[M-1][7]    MM MI MD IM II DM DD out of nodes 1..M-1 (NULL when M = 1)
+ * Each emission row and bg must sum to 1 within 1e-6 with entries >= 0;
+ * match entries and bg entries must be > 0 (a log-odds score must exist);
+ * the MM+MI+MD, IM+II and DM+DD groups must each sum to 1 within 1e-6.
+ *   mu_msv, mu_vit, tau  score-distribution locations in bits, used to turn
+ *                        P-value cutoffs into score cutoffs. */
+typedef struct {
+  int32_t M;
+  const double *bg;
+  const double *match;
+  const double *insert;
+  const double *trans;
+  double mu_msv, mu_vit, tau;
+} hmm_profile_desc;
+
+/* P-value cutoffs of the three stages; a value >= 1 passes every target. */
+typedef struct {
+  double F1, F2, F3;
+} hmm_thresholds;
+
+/* Caller-owned DEVICE buffers of n_seqs elements each, in the caller's
+ * database order.  Written asynchronously on the search stream; valid after
+ * that stream synchronises.
+ *   msv[i]    MSV raw score 0..255 (255 = overflow)
+ *   vit[i]    Viterbi score in 1/500-bit units (exact int32 rescore after an
+ *             int16 overflow); INT32_MIN when Viterbi did not run
+ *   fwd[i]    Forward score in nats, raw (before the null-model correction);
+ *             NaN when Forward did not run
+ *   flags[i]  HMM_* flag bits
+ *   counts    optional device int64[4] (may be NULL): number of MSV passes,
+ *             Viterbi overflows, Viterbi passes, Forward passes. */
+typedef struct {
+  int16_t *msv;
+  int32_t *vit;
+  float *fwd;
+  uint8_t *flags;
+  int64_t *counts;
+} hmm_results;
+
+/* Quantise a profile and upload its tables to the current device.  Profile
+ * definition: Plan7 model as above (paper, Background section: jackhmmer's
+ * profile HMM).  The descriptor's arrays are copied; they may be freed when
+ * the call returns.  Blocks until the upload on `stream` completes.
+ * Errors: HMM_EINVAL (NULL, M < 1, bad probabilities), HMM_ERANGE (M >
+ * HMM_MAX_M), HMM_ENOMEM, HMM_EDEVICE. */
+int hmm_profile_upload(const hmm_profile_desc *desc, hmm_stream stream, hmm_profile **out);
+
+/* Release a profile (NULL is a no-op).  Must not be called while a search
+ * that uses the profile is still running on the GPU. */
+int hmm_profile_free(hmm_profile *p);
+
+/* Pack and upload a sequence database (the search targets; paper,
+ * Background section: the UniRef90 / MGnify sequence databases).
+ *   residues   host uint8 codes 0..19, all sequences concatenated
+ *   offsets    host int64[n_seqs + 1], offsets[0] = 0, strictly increasing
+ *              (every sequence has length >= 1 and <= HMM_MAX_LEN)
+ *   n_seqs     >= 0 (an empty database is allowed; searches then write nothing)
+ * The library sorts targets by decreasing length (stable), aligns each to
+ * 16 bytes on the device and keeps the permutation; results are always
+ * reported in the caller's order.  Blocks until the upload completes.
+ * Errors: HMM_EINVAL (NULL, bad code, bad offsets), HMM_ERANGE (too long),
+ * HMM_ENOMEM, HMM_EDEVICE. */
+int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n_seqs,
+                  hmm_stream stream, hmm_db **out);
+
+/* Release a database (NULL is a no-op); waits for its last search. */
+int hmm_db_free(hmm_db *db);
+
+/* Search one profile against a database: MSV on every target, Viterbi on
+ * MSV survivors, int32 rescore of int16-overflowed targets, Forward on
+ * Viterbi survivors.  Enqueued on `stream` without host synchronisation
+ * (except when the cutoffs change, see below); allocates nothing.
+ * Searches on one database are serialised by the library (a search on a
+ * second stream waits for the previous one on the GPU).  Changing the
+ * cutoffs or the profile between searches on a database rebuilds a small
+ * per-length table, which waits for the database's previous search on the
+ * host.  Errors: HMM_EINVAL (NULL profile/db/thresholds/out or NULL output
+ * buffer with n_seqs > 0), HMM_EDEVICE. */
+int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t,
+               const hmm_results *out, hmm_stream stream);
+
+/* Profiling hook: record HIP events around each stage of the next searches
+ * on this database, in a ring of `capacity` searches (0 turns it off).  The
+ * events are recorded on the search stream, so they bracket exactly that
+ * stream's kernels.  Errors: HMM_EINVAL (NULL db, capacity < 0),
+ * HMM_EDEVICE. */
+int hmm_db_stage_timing(hmm_db *db, int32_t capacity);
+
+/* Stage durations (ms) of the recorded searches, oldest first:
+ * out_ms[4*i + s] for search i and stage s = MSV, Viterbi int16, int32
+ * rescore, Forward (each including its small list/counter kernels).  At
+ * most `cap` searches are returned, their number in *n.  Waits for the
+ * recorded searches to finish and clears the record.  Errors: HMM_EINVAL,
+ * HMM_EDEVICE. */
+int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n);
+
+/* Database properties: number of targets, total residues, longest target. */
+int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t *max_len);
+
+/* Human-readable text of a status code (static storage). */
+const char *hmm_strerror(int status);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *hmm_last_error(void);
+
+/* Test hook: quantise a profile descriptor on the host exactly as
+ * hmm_profile_upload does, without touching the GPU.
+ *   scalars   int32[8]: BIAS8, ENTRY8, EXIT8, ENTRY16, EJ16, M, Q8, Q32
+ *             (Q8 / Q32: vectors per lane of the 16-bit / 32-bit layouts)
+ *   cost8     uint8[M][20]   MSV costs (may be NULL)
+ *   msc16     int16[M][20]   Viterbi match scores (may be NULL)
+ *   isc16     int16[M-1][20] Viterbi insert scores (may be NULL)
+ *   t16       int16[M-1][7]  Viterbi transitions (may be NULL)
+ * Errors: as hmm_profile_upload's validation (HMM_EINVAL, HMM_ERANGE). */
+int hmm_debug_tables(const hmm_profile_desc *desc, int32_t *scalars, uint8_t *cost8,
+                     int16_t *msc16, int16_t *isc16, int16_t *t16);
+
+/* Test hook: the per-length parameters a search uses for target length L
+ * under cutoffs t (host computation, no GPU call).
+ *   i32[6]: MOVE8, THR8, MOVE16, THR16, 0, 0
+ *   f64[4]: LOOP, MOVE (nats), NULL(L) (nats), Forward cutoff (nats; -inf
+ *           when F3 >= 1)
+ * Errors: HMM_EINVAL (NULL argument, L < 1, invalid descriptor). */
+int hmm_debug_length_params(const hmm_profile_desc *desc, const hmm_thresholds *t, int32_t L,
+                            int32_t *i32, double *f64);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HMMGPU_H */

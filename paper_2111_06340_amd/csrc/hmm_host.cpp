@@ -1,0 +1,697 @@
+// Host side of the GPU library: C ABI, argument validation, profile
+// quantisation and device table layout, database packing, and the search
+// driver.  The scoring model is the one stated in include/hmmgpu.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "hmm_internal.h"
+
+using namespace hmmgpu;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int fail_hip(hipError_t e, const char *what) {
+  return fail(HMM_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                    \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return fail_hip(e_, what); \
+  } while (0)
+
+// ---------------------------------------------------------------- scores
+//
+// Quantised score systems (fp64 on the host, rounding q(x) = floor(x + 1/2)):
+//   MSV, 1/3-bit units:   sc8 = q(3/ln2 * ln(e/f)); BIAS8 = clamp(-min sc8, 0, 255);
+//                         COST8 = clamp(BIAS8 - sc8, 0, 255); ENTRY8 = q(-3/ln2 * ENTRY);
+//                         EXIT8 = q(3/ln2 * ln 2); MOVE8(L) = clamp(q(-3/ln2 * MOVE(L)), 0, 255)
+//   Viterbi, 1/500 bits:  score16 = sat16(q(500/ln2 * score)); t = 0 -> -32768
+// with ENTRY = ln(2/(M(M+1))), MOVE(L) = ln(3/(L+3)), LOOP(L) = ln(L/(L+3)).
+// The host evaluates each expression in the same fp64 order so that the
+// integer tables are reproducible.
+
+constexpr double kS8 = 3.0 / M_LN2;
+constexpr double kS16 = 500.0 / M_LN2;
+
+long q_round(double x) { return (long)std::floor(x + 0.5); }
+long clampl(long v, long lo, long hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+double ln_entry(int M) { return std::log(2.0 / ((double)M * ((double)M + 1.0))); }
+double ln_move(int L) { return std::log(3.0 / ((double)L + 3.0)); }
+double ln_loop(int L) { return std::log((double)L / ((double)L + 3.0)); }
+double null_score(int L) {
+  return (double)L * std::log((double)L / ((double)L + 1.0)) + std::log(1.0 / ((double)L + 1.0));
+}
+int move8_of(int L) { return (int)clampl(q_round(-kS8 * ln_move(L)), 0, 255); }
+int move16_of(int L) { return (int)clampl(q_round(kS16 * ln_move(L)), -32768, 32767); }
+
+int instantiated_q8(int q) {
+  static const int qs[] = {1, 2, 3, 4, 5, 6, 7, 8, 10, 12, 14, 16, 20, 24};
+  for (int v : qs)
+    if (v >= q) return v;
+  return -1;
+}
+int instantiated_q32(int q) {
+  static const int qs[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 14, 16, 20, 24, 28, 32, 40, 48};
+  for (int v : qs)
+    if (v >= q) return v;
+  return -1;
+}
+
+std::atomic<uint64_t> g_profile_serial{1};
+
+}  // namespace
+
+struct hmm_profile {
+  int M = 0;
+  uint64_t serial = 0;
+  double mu_msv = 0, mu_vit = 0, tau = 0;
+  // host copies
+  int bias8 = 0, entry8 = 0, exit8 = 0, entry16 = 0, ej16 = 0;
+  std::vector<uint8_t> cost8;
+  std::vector<int16_t> msc16, isc16, t16;
+  DevProfile dev{};
+  void *dmem = nullptr;  // one device allocation holding every table
+};
+
+struct hmm_db {
+  int64_t n = 0, n_res = 0;
+  int32_t max_len = 0;
+  void *dmem = nullptr;  // packed residues + index arrays + scratch
+  DevDb dev{};
+  LenParams *h_lp = nullptr;  // pinned staging of the per-length table
+  LenParams *d_lp = nullptr;
+  // cache key of the per-length table
+  uint64_t lp_serial = 0;
+  double lp_F[3] = {-1, -1, -1};
+  hipEvent_t done = nullptr;   // completion of the latest search
+  bool searched = false;
+  // stage timing ring (profiling hook)
+  std::vector<hipEvent_t> tev;  // capacity * 5
+  int32_t tcap = 0;
+  int64_t trec = 0;             // searches recorded since the last read
+};
+
+namespace {
+
+// ---------------------------------------------------------------- checks
+
+int check_distribution(const double *p, int n, bool strictly_positive, const char *what, int row) {
+  double s = 0.0;
+  for (int i = 0; i < n; i++) {
+    if (!(p[i] >= 0.0) || !std::isfinite(p[i]))
+      return fail(HMM_EINVAL, "%s row %d: entry %d is negative or not finite", what, row, i);
+    if (strictly_positive && !(p[i] > 0.0))
+      return fail(HMM_EINVAL, "%s row %d: entry %d must be > 0", what, row, i);
+    s += p[i];
+  }
+  if (std::fabs(s - 1.0) > 1e-6) return fail(HMM_EINVAL, "%s row %d sums to %.9f, not 1", what, row, s);
+  return HMM_OK;
+}
+
+int validate_desc(const hmm_profile_desc *d) {
+  if (!d) return fail(HMM_EINVAL, "profile descriptor is NULL");
+  if (d->M < 1) return fail(HMM_EINVAL, "M = %d; need M >= 1", d->M);
+  if (d->M > HMM_MAX_M) return fail(HMM_ERANGE, "M = %d exceeds HMM_MAX_M = %d", d->M, HMM_MAX_M);
+  if (!d->bg || !d->match) return fail(HMM_EINVAL, "bg or match is NULL");
+  if (d->M > 1 && (!d->insert || !d->trans)) return fail(HMM_EINVAL, "insert or trans is NULL with M > 1");
+  if (!std::isfinite(d->mu_msv) || !std::isfinite(d->mu_vit) || !std::isfinite(d->tau))
+    return fail(HMM_EINVAL, "calibration values must be finite");
+  int rc;
+  if ((rc = check_distribution(d->bg, kAlpha, true, "bg", 0))) return rc;
+  for (int k = 0; k < d->M; k++)
+    if ((rc = check_distribution(d->match + (size_t)k * kAlpha, kAlpha, true, "match", k))) return rc;
+  for (int k = 0; k + 1 < d->M; k++) {
+    if ((rc = check_distribution(d->insert + (size_t)k * kAlpha, kAlpha, false, "insert", k))) return rc;
+    const double *t = d->trans + (size_t)k * 7;
+    if ((rc = check_distribution(t, 3, false, "trans MM/MI/MD", k))) return rc;
+    if ((rc = check_distribution(t + 3, 2, false, "trans IM/II", k))) return rc;
+    if ((rc = check_distribution(t + 5, 2, false, "trans DM/DD", k))) return rc;
+  }
+  return HMM_OK;
+}
+
+// ---------------------------------------------------------------- layout
+
+// Packed 16-bit layout of the MSV and int16 Viterbi kernels: the 128 slots
+// of a wave are (lane l, half h) -> slot 2l+h, and slot s holds cells
+// s*Q + q in its Q vectors, so a cell's left neighbour lives in the same
+// slot one vector earlier, except for vector 0 (previous slot, vector Q-1).
+inline size_t pk_index(int q, int lane) { return (size_t)q * kWave + lane; }
+inline int pk_cell(int Q, int q, int lane, int half) { return (2 * lane + half) * Q + q; }
+
+// 32-bit layout of the rescore and Forward kernels: slot = lane, cell l*Q + q.
+inline int w_cell(int Q, int q, int lane) { return lane * Q + q; }
+
+uint32_t pack16(int lo, int hi) { return (uint32_t)(uint16_t)lo | ((uint32_t)(uint16_t)hi << 16); }
+
+// Host quantisation of a validated descriptor into p's host tables.
+void quantize(const hmm_profile_desc *d, hmm_profile *p) {
+  const int M = d->M;
+  p->M = M;
+  p->serial = g_profile_serial.fetch_add(1);
+  p->mu_msv = d->mu_msv;
+  p->mu_vit = d->mu_vit;
+  p->tau = d->tau;
+  const double entry = ln_entry(M);
+  std::vector<long> sc8((size_t)M * kAlpha);
+  long min8 = 0;
+  for (int k = 0; k < M; k++)
+    for (int a = 0; a < kAlpha; a++) {
+      long v = q_round(kS8 * std::log(d->match[(size_t)k * kAlpha + a] / d->bg[a]));
+      sc8[(size_t)k * kAlpha + a] = v;
+      if ((k == 0 && a == 0) || v < min8) min8 = v;
+    }
+  p->bias8 = (int)clampl(-min8, 0, 255);
+  p->cost8.resize((size_t)M * kAlpha);
+  for (size_t i = 0; i < sc8.size(); i++) p->cost8[i] = (uint8_t)clampl(p->bias8 - sc8[i], 0, 255);
+  p->entry8 = (int)clampl(q_round(-kS8 * entry), 0, 255);
+  p->exit8 = (int)clampl(q_round(kS8 * std::log(2.0)), 0, 255);
+  p->msc16.resize((size_t)M * kAlpha);
+  for (int k = 0; k < M; k++)
+    for (int a = 0; a < kAlpha; a++)
+      p->msc16[(size_t)k * kAlpha + a] = (int16_t)clampl(
+          q_round(kS16 * std::log(d->match[(size_t)k * kAlpha + a] / d->bg[a])), -32768, 32767);
+  p->isc16.resize((size_t)std::max(M - 1, 0) * kAlpha);
+  p->t16.resize((size_t)std::max(M - 1, 0) * 7);
+  for (int k = 0; k + 1 < M; k++) {
+    for (int a = 0; a < kAlpha; a++) {
+      double e = d->insert[(size_t)k * kAlpha + a];
+      // a zero insert probability has score -inf: saturate at the floor
+      p->isc16[(size_t)k * kAlpha + a] =
+          e > 0.0 ? (int16_t)clampl(q_round(kS16 * std::log(e / d->bg[a])), -32768, 32767) : (int16_t)kNeg16;
+    }
+    for (int t = 0; t < 7; t++) {
+      double v = d->trans[(size_t)k * 7 + t];
+      p->t16[(size_t)k * 7 + t] =
+          v > 0.0 ? (int16_t)clampl(q_round(kS16 * std::log(v)), -32768, 32767) : (int16_t)kNeg16;
+    }
+  }
+  p->entry16 = (int)clampl(q_round(kS16 * entry), -32768, 32767);
+  p->ej16 = (int)clampl(q_round(kS16 * std::log(0.5)), -32768, 32767);
+
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hmm_strerror(int status) {
+  switch (status) {
+    case HMM_OK: return "success";
+    case HMM_EINVAL: return "invalid argument";
+    case HMM_ERANGE: return "size out of range";
+    case HMM_ENOMEM: return "out of memory";
+    case HMM_EDEVICE: return "GPU runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *hmm_last_error(void) { return g_last_error.c_str(); }
+
+int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile **out) {
+  if (!out) return fail(HMM_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = validate_desc(d);
+  if (rc) return rc;
+  const int M = d->M;
+  hmm_profile *p = new (std::nothrow) hmm_profile();
+  if (!p) return fail(HMM_ENOMEM, "host allocation failed");
+  quantize(d, p);
+
+  // ---- device layouts
+  const int Q8 = instantiated_q8(q8_of(M));
+  const int Q32 = instantiated_q32(q32_of(M));
+  const size_t n_msv = (size_t)kAlpha * Q8 * kWave;            // dwords
+  const size_t n_vemit = (size_t)kAlpha * 2 * Q8 * kWave;
+  const size_t n_vtr = (size_t)TR_N * Q8 * kWave;
+  const size_t n_w32emit = (size_t)kAlpha * 2 * Q32 * kWave;
+  const size_t n_w32tr = (size_t)TR_N * Q32 * kWave;
+  const size_t n_ftr = (size_t)(TR_N + 1) * Q32 * kWave;
+  const size_t total = n_msv + n_vemit + n_vtr + n_w32emit + n_w32tr + n_w32emit + n_ftr;
+  std::vector<uint32_t> h(total, 0);
+  uint32_t *h_msv = h.data();
+  uint32_t *h_vemit = h_msv + n_msv;
+  uint32_t *h_vtr = h_vemit + n_vemit;
+  int32_t *h_w32emit = (int32_t *)(h_vtr + n_vtr);
+  int32_t *h_w32tr = h_w32emit + n_w32emit;
+  float *h_femit = (float *)(h_w32tr + n_w32tr);
+  float *h_ftr = h_femit + n_w32emit;
+
+  auto t16 = [&](int node, int which) -> int {  // node 1..M-1
+    return p->t16[(size_t)(node - 1) * 7 + which];
+  };
+  // transition of plane `tr` into/at cell c (0-based; node c+1); INT_MIN = structural
+  const int kNone = INT32_MIN;
+  auto tr_cell = [&](int tr, int c) -> int {
+    if (c >= M) return kNone;
+    switch (tr) {
+      case TR_MMIN: return c >= 1 ? t16(c, 0) : kNone;
+      case TR_IMIN: return c >= 1 ? t16(c, 3) : kNone;
+      case TR_DMIN: return c >= 1 ? t16(c, 5) : kNone;
+      case TR_MDIN: return c >= 1 ? t16(c, 2) : kNone;
+      case TR_DDIN: return c >= 1 ? t16(c, 6) : kNone;
+      case TR_MI: return c + 1 < M ? t16(c + 1, 1) : kNone;
+      case TR_II: return c + 1 < M ? t16(c + 1, 4) : kNone;
+    }
+    return kNone;
+  };
+  auto tr_prob = [&](int tr, int c) -> double {
+    if (c >= M) return 0.0;
+    auto t = [&](int node, int which) { return d->trans[(size_t)(node - 1) * 7 + which]; };
+    switch (tr) {
+      case TR_MMIN: return c >= 1 ? t(c, 0) : 0.0;
+      case TR_IMIN: return c >= 1 ? t(c, 3) : 0.0;
+      case TR_DMIN: return c >= 1 ? t(c, 5) : 0.0;
+      case TR_MDIN: return c >= 1 ? t(c, 2) : 0.0;
+      case TR_DDIN: return c >= 1 ? t(c, 6) : 0.0;
+      case TR_MI: return c + 1 < M ? t(c + 1, 1) : 0.0;
+      case TR_II: return c + 1 < M ? t(c + 1, 4) : 0.0;
+    }
+    return 0.0;
+  };
+  auto msc_cell = [&](int c, int a) -> int { return c < M ? p->msc16[(size_t)c * kAlpha + a] : kNone; };
+  auto isc_cell = [&](int c, int a) -> int { return c + 1 < M ? p->isc16[(size_t)c * kAlpha + a] : kNone; };
+  auto lo16 = [](int v) { return v == INT32_MIN ? kNeg16 : v; };
+
+  for (int a = 0; a < kAlpha; a++)
+    for (int q = 0; q < Q8; q++)
+      for (int l = 0; l < kWave; l++) {
+        int c0 = pk_cell(Q8, q, l, 0), c1 = pk_cell(Q8, q, l, 1);
+        int v0 = c0 < M ? p->cost8[(size_t)c0 * kAlpha + a] : 255;
+        int v1 = c1 < M ? p->cost8[(size_t)c1 * kAlpha + a] : 255;
+        h_msv[(size_t)a * Q8 * kWave + pk_index(q, l)] = (uint32_t)(v0 << 8) | ((uint32_t)(v1 << 8) << 16);
+        h_vemit[((size_t)a * 2 + 0) * Q8 * kWave + pk_index(q, l)] =
+            pack16(lo16(msc_cell(c0, a)), lo16(msc_cell(c1, a)));
+        h_vemit[((size_t)a * 2 + 1) * Q8 * kWave + pk_index(q, l)] =
+            pack16(lo16(isc_cell(c0, a)), lo16(isc_cell(c1, a)));
+      }
+  for (int tr = 0; tr < TR_N; tr++)
+    for (int q = 0; q < Q8; q++)
+      for (int l = 0; l < kWave; l++)
+        h_vtr[(size_t)tr * Q8 * kWave + pk_index(q, l)] =
+            pack16(lo16(tr_cell(tr, pk_cell(Q8, q, l, 0))), lo16(tr_cell(tr, pk_cell(Q8, q, l, 1))));
+  auto w32 = [&](int v) { return v == INT32_MIN ? kNeg32 : v; };
+  for (int a = 0; a < kAlpha; a++)
+    for (int q = 0; q < Q32; q++)
+      for (int l = 0; l < kWave; l++) {
+        int c = w_cell(Q32, q, l);
+        size_t im = ((size_t)a * 2 + 0) * Q32 * kWave + pk_index(q, l);
+        size_t ii = ((size_t)a * 2 + 1) * Q32 * kWave + pk_index(q, l);
+        h_w32emit[im] = w32(msc_cell(c, a));
+        h_w32emit[ii] = w32(isc_cell(c, a));
+        h_femit[im] = c < M ? (float)(d->match[(size_t)c * kAlpha + a] / d->bg[a]) : 0.0f;
+        h_femit[ii] = c + 1 < M ? (float)(d->insert[(size_t)c * kAlpha + a] / d->bg[a]) : 0.0f;
+      }
+  for (int tr = 0; tr < TR_N; tr++)
+    for (int q = 0; q < Q32; q++)
+      for (int l = 0; l < kWave; l++) {
+        int c = w_cell(Q32, q, l);
+        h_w32tr[(size_t)tr * Q32 * kWave + pk_index(q, l)] = w32(tr_cell(tr, c));
+        h_ftr[(size_t)tr * Q32 * kWave + pk_index(q, l)] = (float)tr_prob(tr, c);
+      }
+  // D-chain prefix products inside each slot: prod_{j<=q} DDin(cell l*Q+j)
+  for (int l = 0; l < kWave; l++) {
+    double acc = 1.0;
+    for (int q = 0; q < Q32; q++) {
+      acc *= tr_prob(TR_DDIN, w_cell(Q32, q, l));
+      h_ftr[(size_t)TR_N * Q32 * kWave + pk_index(q, l)] = (float)acc;
+    }
+  }
+
+  hipError_t e = hipMalloc(&p->dmem, total * sizeof(uint32_t));
+  if (e != hipSuccess) {
+    delete p;
+    return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "device allocation of %zu bytes failed", total * 4)
+                                    : fail_hip(e, "hipMalloc");
+  }
+  e = hipMemcpyAsync(p->dmem, h.data(), total * sizeof(uint32_t), hipMemcpyHostToDevice, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) {
+    (void)hipFree(p->dmem);
+    delete p;
+    return fail_hip(e, "profile upload");
+  }
+  const uint32_t *base = (const uint32_t *)p->dmem;
+  DevProfile &dv = p->dev;
+  dv.M = M;
+  dv.Q8 = Q8;
+  dv.Q32 = Q32;
+  dv.bias8 = p->bias8;
+  dv.entry8 = p->entry8;
+  dv.exit8 = p->exit8;
+  dv.entry16 = p->entry16;
+  dv.ej16 = p->ej16;
+  dv.entry_p = (float)(2.0 / ((double)M * ((double)M + 1.0)));
+  dv.msv = base;
+  dv.vit_emit = base + n_msv;
+  dv.vit_tr = dv.vit_emit + n_vemit;
+  dv.v32_emit = (const int32_t *)(dv.vit_tr + n_vtr);
+  dv.v32_tr = dv.v32_emit + n_w32emit;
+  dv.f_emit = (const float *)(dv.v32_tr + n_w32tr);
+  dv.f_tr = dv.f_emit + n_w32emit;
+  *out = p;
+  return HMM_OK;
+}
+
+int hmm_profile_free(hmm_profile *p) {
+  if (!p) return HMM_OK;
+  hipError_t e = p->dmem ? hipFree(p->dmem) : hipSuccess;
+  delete p;
+  if (e != hipSuccess) return fail_hip(e, "hipFree(profile)");
+  return HMM_OK;
+}
+
+int hmm_debug_tables(const hmm_profile_desc *d, int32_t *scalars, uint8_t *cost8, int16_t *msc16,
+                     int16_t *isc16, int16_t *t16) {
+  if (!scalars) return fail(HMM_EINVAL, "scalars is NULL");
+  int rc = validate_desc(d);
+  if (rc) return rc;
+  hmm_profile p;
+  quantize(d, &p);
+  scalars[0] = p.bias8;
+  scalars[1] = p.entry8;
+  scalars[2] = p.exit8;
+  scalars[3] = p.entry16;
+  scalars[4] = p.ej16;
+  scalars[5] = p.M;
+  scalars[6] = instantiated_q8(q8_of(p.M));
+  scalars[7] = instantiated_q32(q32_of(p.M));
+  if (cost8) memcpy(cost8, p.cost8.data(), p.cost8.size());
+  if (msc16) memcpy(msc16, p.msc16.data(), p.msc16.size() * 2);
+  if (isc16) memcpy(isc16, p.isc16.data(), p.isc16.size() * 2);
+  if (t16) memcpy(t16, p.t16.data(), p.t16.size() * 2);
+  return HMM_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Per-length parameters: the cutoffs are the smallest integer scores whose
+// bit score exceeds the P-value cutoff (slope ln 2 per bit):
+//   MSV:     Gumbel, x1 = mu_msv - ln(-ln(1 - F1)) / ln 2
+//            THR8  = floor(BASE8 + S8 * (x1 ln2 + NULL(L) + 3)) + 1, in [0, 256]
+//   Viterbi: Gumbel, x2 = mu_vit - ln(-ln(1 - F2)) / ln 2
+//            THR16 = floor(S16 * (x2 ln2 + NULL(L) + 3)) + 1
+//   Forward: exponential tail, pass when fwd > (tau - ln(F3)/ln 2) ln2 + NULL(L)
+// (the 3 nats stand for the N/C/J loop scores that the integer filters omit).
+void length_params(const hmm_profile *p, const hmm_thresholds *t, int L, LenParams *lp, double *f64) {
+  const double nul = null_score(L);
+  lp->move8 = move8_of(L);
+  lp->move16 = move16_of(L);
+  if (t->F1 >= 1.0) {
+    lp->thr8 = 0;
+  } else {
+    double x1 = p->mu_msv - std::log(-std::log(1.0 - t->F1)) / M_LN2;
+    double y = std::floor(kBase8 + kS8 * (x1 * M_LN2 + nul + 3.0)) + 1.0;
+    lp->thr8 = (int32_t)(y < 0.0 ? 0.0 : (y > 256.0 ? 256.0 : y));
+  }
+  if (t->F2 >= 1.0) {
+    lp->thr16 = INT32_MIN;
+  } else {
+    double x2 = p->mu_vit - std::log(-std::log(1.0 - t->F2)) / M_LN2;
+    double y = std::floor(kS16 * (x2 * M_LN2 + nul + 3.0)) + 1.0;
+    lp->thr16 = (int32_t)(y < -2147483647.0 ? -2147483647.0 : (y > 2147483647.0 ? 2147483647.0 : y));
+  }
+  double fthr = t->F3 >= 1.0 ? -INFINITY : (p->tau - std::log(t->F3) / M_LN2) * M_LN2 + nul;
+  lp->loop_p = (float)((double)L / ((double)L + 3.0));
+  lp->move_p = (float)(3.0 / ((double)L + 3.0));
+  lp->fthr = (float)fthr;
+  lp->pad = 0.0f;
+  if (f64) {
+    f64[0] = ln_loop(L);
+    f64[1] = ln_move(L);
+    f64[2] = nul;
+    f64[3] = fthr;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int hmm_debug_length_params(const hmm_profile_desc *d, const hmm_thresholds *t, int32_t L, int32_t *i32,
+                            double *f64) {
+  if (!d || !t || !i32 || !f64) return fail(HMM_EINVAL, "NULL argument");
+  if (L < 1) return fail(HMM_EINVAL, "L = %d; need L >= 1", L);
+  if (!std::isfinite(d->mu_msv) || !std::isfinite(d->mu_vit) || !std::isfinite(d->tau))
+    return fail(HMM_EINVAL, "calibration values must be finite");
+  hmm_profile p;
+  p.mu_msv = d->mu_msv;
+  p.mu_vit = d->mu_vit;
+  p.tau = d->tau;
+  LenParams lp;
+  length_params(&p, t, L, &lp, f64);
+  i32[0] = lp.move8;
+  i32[1] = lp.thr8;
+  i32[2] = lp.move16;
+  i32[3] = lp.thr16;
+  i32[4] = 0;
+  i32[5] = 0;
+  return HMM_OK;
+}
+
+int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hmm_stream stream,
+                  hmm_db **out) {
+  if (!out) return fail(HMM_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (n < 0) return fail(HMM_EINVAL, "n_seqs = %lld", (long long)n);
+  if (!offsets) return fail(HMM_EINVAL, "offsets is NULL");
+  if (offsets[0] != 0) return fail(HMM_EINVAL, "offsets[0] = %lld, must be 0", (long long)offsets[0]);
+  if (n > 0 && !residues) return fail(HMM_EINVAL, "residues is NULL");
+  if (n > (int64_t)INT32_MAX) return fail(HMM_ERANGE, "too many sequences");
+  int32_t max_len = 0;
+  for (int64_t i = 0; i < n; i++) {
+    int64_t L = offsets[i + 1] - offsets[i];
+    if (L < 1) return fail(HMM_EINVAL, "sequence %lld has length %lld; need >= 1", (long long)i, (long long)L);
+    if (L > HMM_MAX_LEN)
+      return fail(HMM_ERANGE, "sequence %lld has length %lld > HMM_MAX_LEN", (long long)i, (long long)L);
+    max_len = std::max<int32_t>(max_len, (int32_t)L);
+  }
+  const int64_t n_res = offsets[n];
+  for (int64_t j = 0; j < n_res; j++)
+    if (residues[j] >= kAlpha)
+      return fail(HMM_EINVAL, "residue %lld has code %d; codes are 0..19", (long long)j, residues[j]);
+
+  // stable sort by decreasing length
+  std::vector<int32_t> order((size_t)n);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return offsets[a + 1] - offsets[a] > offsets[b + 1] - offsets[b];
+  });
+  std::vector<int64_t> start((size_t)n);
+  std::vector<int32_t> len((size_t)n);
+  int64_t pos = 0;
+  for (int64_t i = 0; i < n; i++) {
+    int32_t L = (int32_t)(offsets[order[i] + 1] - offsets[order[i]]);
+    start[i] = pos;
+    len[i] = L;
+    pos += ((int64_t)L + 15) / 16 * 16;
+  }
+  const int64_t res_bytes = pos + 1024;  // residue streams read up to 768 bytes past a target
+  auto al = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t sz_res = al((size_t)res_bytes);
+  const size_t sz_start = al((size_t)n * 8 + 8), sz_i32 = al((size_t)n * 4 + 4), sz_u8 = al((size_t)n + 1);
+  const size_t sz_lp = al(sizeof(LenParams) * ((size_t)max_len + 1));
+  const size_t total = sz_res + sz_start + sz_i32 * 2 + sz_u8 + sz_i32 * 3 + al(CNT_N * 4) + sz_lp;
+
+  hmm_db *db = new (std::nothrow) hmm_db();
+  if (!db) return fail(HMM_ENOMEM, "host allocation failed");
+  db->n = n;
+  db->n_res = n_res;
+  db->max_len = max_len;
+  uint8_t *stage = nullptr;
+  hipError_t e = hipHostMalloc((void **)&stage, total, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete db;
+    return fail(HMM_ENOMEM, "pinned staging of %zu bytes failed: %s", total, hipGetErrorString(e));
+  }
+  memset(stage, 0, total);
+  size_t off = 0;
+  uint8_t *s_res = stage + off;
+  const size_t o_res = off;
+  off += sz_res;
+  const size_t o_start = off;
+  int64_t *s_start = (int64_t *)(stage + off);
+  off += sz_start;
+  const size_t o_len = off;
+  int32_t *s_len = (int32_t *)(stage + off);
+  off += sz_i32;
+  const size_t o_perm = off;
+  int32_t *s_perm = (int32_t *)(stage + off);
+  off += sz_i32;
+  const size_t o_flags = off;
+  off += sz_u8;
+  const size_t o_lv = off;
+  off += sz_i32;
+  const size_t o_lo = off;
+  off += sz_i32;
+  const size_t o_lf = off;
+  off += sz_i32;
+  const size_t o_cnt = off;
+  off += al(CNT_N * 4);
+  const size_t o_lp = off;
+  off += sz_lp;
+  for (int64_t i = 0; i < n; i++) {
+    memcpy(s_res + start[i], residues + offsets[order[i]], (size_t)len[i]);
+    s_start[i] = start[i];
+    s_len[i] = len[i];
+    s_perm[i] = order[i];
+  }
+  e = hipMalloc(&db->dmem, total);
+  if (e != hipSuccess) {
+    (void)hipHostFree(stage);
+    delete db;
+    return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "device allocation of %zu bytes failed", total)
+                                    : fail_hip(e, "hipMalloc(db)");
+  }
+  e = hipMemcpyAsync(db->dmem, stage, o_flags, hipMemcpyHostToDevice, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  (void)hipHostFree(stage);
+  if (e == hipSuccess) e = hipHostMalloc((void **)&db->h_lp, sz_lp, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->done, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipFree(db->dmem);
+    if (db->h_lp) (void)hipHostFree(db->h_lp);
+    delete db;
+    return fail_hip(e, "database upload");
+  }
+  uint8_t *b = (uint8_t *)db->dmem;
+  DevDb &dv = db->dev;
+  dv.n = n;
+  dv.max_len = max_len;
+  dv.res = b + o_res;
+  dv.start = (const int64_t *)(b + o_start);
+  dv.len = (const int32_t *)(b + o_len);
+  dv.perm = (const int32_t *)(b + o_perm);
+  dv.flags_sorted = b + o_flags;
+  dv.list_vit = (int32_t *)(b + o_lv);
+  dv.list_ovf = (int32_t *)(b + o_lo);
+  dv.list_fwd = (int32_t *)(b + o_lf);
+  dv.counters = (int32_t *)(b + o_cnt);
+  db->d_lp = (LenParams *)(b + o_lp);
+  dv.lp = db->d_lp;
+  *out = db;
+  return HMM_OK;
+}
+
+static void drop_timing(hmm_db *db) {
+  for (hipEvent_t ev : db->tev) (void)hipEventDestroy(ev);
+  db->tev.clear();
+  db->tcap = 0;
+  db->trec = 0;
+}
+
+int hmm_db_stage_timing(hmm_db *db, int32_t capacity) {
+  if (!db || capacity < 0) return fail(HMM_EINVAL, "NULL db or negative capacity");
+  if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+  drop_timing(db);
+  for (int32_t i = 0; i < capacity * 5; i++) {
+    hipEvent_t ev;
+    hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) {
+      drop_timing(db);
+      return fail_hip(e, "hipEventCreate");
+    }
+    db->tev.push_back(ev);
+  }
+  db->tcap = capacity;
+  return HMM_OK;
+}
+
+int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n) {
+  if (!db || !n || (cap > 0 && !out_ms)) return fail(HMM_EINVAL, "NULL argument");
+  *n = 0;
+  if (db->tcap <= 0) return HMM_OK;
+  if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+  const int64_t have = std::min<int64_t>(db->trec, db->tcap);
+  const int64_t first = db->trec - have;
+  int32_t k = 0;
+  for (int64_t i = first; i < db->trec && k < cap; i++, k++) {
+    hipEvent_t *ev = &db->tev[(size_t)(i % db->tcap) * 5];
+    for (int st = 0; st < 4; st++)
+      HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + st], ev[st], ev[st + 1]), "hipEventElapsedTime");
+  }
+  *n = k;
+  db->trec = 0;
+  return HMM_OK;
+}
+
+int hmm_db_free(hmm_db *db) {
+  if (!db) return HMM_OK;
+  hipError_t e = hipSuccess;
+  if (db->searched) e = hipEventSynchronize(db->done);
+  drop_timing(db);
+  if (db->done) (void)hipEventDestroy(db->done);
+  if (db->h_lp) (void)hipHostFree(db->h_lp);
+  hipError_t e2 = db->dmem ? hipFree(db->dmem) : hipSuccess;
+  delete db;
+  if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize(db)");
+  if (e2 != hipSuccess) return fail_hip(e2, "hipFree(db)");
+  return HMM_OK;
+}
+
+int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t *max_len) {
+  if (!db) return fail(HMM_EINVAL, "db is NULL");
+  if (n_seqs) *n_seqs = db->n;
+  if (n_residues) *n_residues = db->n_res;
+  if (max_len) *max_len = db->max_len;
+  return HMM_OK;
+}
+
+int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const hmm_results *out,
+               hmm_stream stream) {
+  if (!p || !db || !t || !out) return fail(HMM_EINVAL, "NULL profile, db, thresholds or results");
+  if (std::isnan(t->F1) || std::isnan(t->F2) || std::isnan(t->F3) || !(t->F1 > 0) || !(t->F2 > 0) ||
+      !(t->F3 > 0))
+    return fail(HMM_EINVAL, "P-value cutoffs must be > 0");
+  if (db->n > 0 && (!out->msv || !out->vit || !out->fwd || !out->flags))
+    return fail(HMM_EINVAL, "NULL output buffer");
+  hipStream_t s = (hipStream_t)stream;
+  if (db->n == 0) return HMM_OK;
+  // serialise searches on this database (scratch and per-length table)
+  if (db->searched) HIP_TRY(hipStreamWaitEvent(s, db->done, 0), "hipStreamWaitEvent");
+  if (db->lp_serial != p->serial || db->lp_F[0] != t->F1 || db->lp_F[1] != t->F2 || db->lp_F[2] != t->F3) {
+    if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+    for (int L = 0; L <= db->max_len; L++) length_params(p, t, L < 1 ? 1 : L, &db->h_lp[L], nullptr);
+    HIP_TRY(hipMemcpyAsync(db->d_lp, db->h_lp, sizeof(LenParams) * ((size_t)db->max_len + 1),
+                           hipMemcpyHostToDevice, s),
+            "hipMemcpyAsync(length table)");
+    db->lp_serial = p->serial;
+    db->lp_F[0] = t->F1;
+    db->lp_F[1] = t->F2;
+    db->lp_F[2] = t->F3;
+  }
+  DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts};
+  hipEvent_t *ev = nullptr;
+  if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
+  HIP_TRY(launch_search(p->dev, db->dev, o, s, ev), "kernel launch");
+  HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
+  db->searched = true;
+  return HMM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,88 @@
+// Internal declarations shared by the host side (hmm_host.cpp) and the
+// kernels (hmm_kernels.hip) of the GPU library.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hmmgpu.h"
+
+namespace hmmgpu {
+
+constexpr int kWave = 64;           // CDNA wavefront
+constexpr int kAlpha = 20;          // residue alphabet
+constexpr int kBase8 = 190;         // MSV offset of the N/J start
+constexpr int kNeg16 = -32768;      // int16 "minus infinity"
+constexpr int32_t kNeg32 = -(1 << 30);  // int32 rescore floor
+constexpr int kMaxQ8 = 24;          // 128 cells per packed vector -> M <= 3072
+constexpr int kMaxQ32 = 48;         // 64 cells per 32-bit vector -> M <= 3072
+
+// Transition planes of the per-cell "into" layout (cell k = node k+1).
+//   MMIN/IMIN/DMIN: M_k, I_k, D_k (node k) -> M_{k+1};  MDIN/DDIN: M_k, D_k
+//   -> D_{k+1};  MI/II: M_{k+1}/I_{k+1} -> I_{k+1}.  Structural and padding
+//   cells hold the type's minus infinity (probability 0 in Forward).
+enum { TR_MMIN = 0, TR_IMIN, TR_DMIN, TR_MDIN, TR_DDIN, TR_MI, TR_II, TR_N };
+
+// Per-target-length parameters, one entry per L = 0..max_len.
+struct LenParams {
+  int32_t move8;    // MSV cost of N->B / J->B / C->T
+  int32_t thr8;     // MSV pass: msv_raw >= thr8 (0..256)
+  int32_t move16;   // Viterbi score of the moves (<= 0)
+  int32_t thr16;    // Viterbi pass: vit >= thr16
+  float loop_p;     // Forward N/C/J self-loop probability L/(L+3)
+  float move_p;     // Forward move probability 3/(L+3)
+  float fthr;       // Forward pass: fwd > fthr (nats); -inf when F3 >= 1
+  float pad;
+};
+
+// Device-side profile, passed to kernels by value.
+struct DevProfile {
+  int32_t M, Q8, Q32;
+  int32_t bias8, entry8, exit8;
+  int32_t entry16, ej16;
+  float entry_p;                // 2/(M(M+1))
+  const uint32_t *msv;          // [20][Q8][64] packed u16: cost << 8 (high byte)
+  const uint32_t *vit_emit;     // [20][2][Q8][64] packed i16: msc plane, isc plane
+  const uint32_t *vit_tr;       // [TR_N][Q8][64] packed i16
+  const int32_t *v32_emit;      // [20][2][Q32][64]
+  const int32_t *v32_tr;        // [TR_N][Q32][64]
+  const float *f_emit;          // [20][2][Q32][64] odds e/f, i/f
+  const float *f_tr;            // [TR_N + 1][Q32][64]: probabilities, then D-chain prefix products
+};
+
+// Counters in the database scratch (device int32).
+enum { CNT_VIT = 0, CNT_OVF, CNT_FWD, CNT_FWD_PASS, CNT_WORK_VIT, CNT_WORK_OVF, CNT_WORK_FWD, CNT_N = 8 };
+
+struct DevDb {
+  int64_t n;
+  int32_t max_len;
+  const uint8_t *res;           // packed residues, each target 16-byte aligned
+  const int64_t *start;         // [n] byte offset of each target (sorted order)
+  const int32_t *len;           // [n]
+  const int32_t *perm;          // [n] sorted index -> caller index
+  uint8_t *flags_sorted;        // [n] scratch
+  int32_t *list_vit;            // [n] MSV survivors (sorted indices)
+  int32_t *list_ovf;            // [n] int16 Viterbi overflows
+  int32_t *list_fwd;            // [n] Viterbi survivors
+  int32_t *counters;            // [CNT_N]
+  const LenParams *lp;          // [max_len + 1]
+};
+
+struct DevOut {
+  int16_t *msv;
+  int32_t *vit;
+  float *fwd;
+  uint8_t *flags;
+  int64_t *counts;
+};
+
+// Enqueue the whole cascade on `stream`.  When `ev` is non-null, ev[0..4]
+// are recorded before MSV and after MSV, Viterbi, rescore and Forward.
+hipError_t launch_search(const DevProfile &p, const DevDb &db, const DevOut &out, hipStream_t stream,
+                         hipEvent_t *ev);
+
+// Number of packed vectors per lane.
+inline int q8_of(int M) { return (M + 2 * kWave - 1) / (2 * kWave); }
+inline int q32_of(int M) { return (M + kWave - 1) / kWave; }
+
+}  // namespace hmmgpu

@@ -1,0 +1,802 @@
+// HIP kernels (gfx950) of the profile-HMM search cascade and their launcher.
+//
+// One wavefront scores one target.  The model dimension (profile cells) is
+// spread across the 64 lanes; database rows (residues) are processed in
+// order.  Every wave-uniform quantity (target index, length, residue, the
+// special states N/B/E/J/C) lives in scalar registers; branches on it are
+// uniform.
+//
+//  MSV      uint8 values kept in the HIGH byte of 16-bit lanes: packed
+//           saturating u16 add/sub and max then reproduce u8 saturating
+//           arithmetic exactly (the low byte never carries into the high
+//           byte's result).  Two cells per VGPR, 128 slots per wave.
+//  Viterbi  packed saturating int16, two cells per VGPR; delete chain by
+//           lazy propagation across slots.
+//  Rescore  the Viterbi recurrence in int32 with a -2^30 floor.
+//  Forward  fp32 probabilities with exact power-of-two rescaling; the
+//           delete chain crosses slots through a DPP prefix scan of affine
+//           maps, E through a DPP sum.
+//
+// Cell layout (see hmm_host.cpp): packed kernels use slot 2*lane+half and
+// cell slot*Q + q; 32-bit kernels use slot = lane and cell lane*Q + q.  The
+// left neighbour of vector q is vector q-1 of the same slot, except q = 0,
+// which takes vector Q-1 of the previous slot: one cross-lane shift per
+// state per row.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "hmm_internal.h"
+
+namespace hmmgpu {
+namespace {
+
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+
+constexpr uint32_t kNegNeg = 0x80008000u;  // two int16 -32768
+
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// --- packed 16-bit arithmetic ------------------------------------------------
+__device__ __forceinline__ uint32_t u16_max(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                __builtin_bit_cast(u16x2, b)));
+}
+__device__ __forceinline__ uint32_t u16_adds(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_add_sat(__builtin_bit_cast(u16x2, a),
+                                                                    __builtin_bit_cast(u16x2, b)));
+}
+__device__ __forceinline__ uint32_t u16_subs(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(__builtin_bit_cast(u16x2, a),
+                                                                    __builtin_bit_cast(u16x2, b)));
+}
+__device__ __forceinline__ uint32_t i16_max(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, a),
+                                                                __builtin_bit_cast(i16x2, b)));
+}
+__device__ __forceinline__ uint32_t i16_adds(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_add_sat(__builtin_bit_cast(i16x2, a),
+                                                                    __builtin_bit_cast(i16x2, b)));
+}
+__device__ __forceinline__ uint32_t splat16(int v) { return ((uint32_t)(uint16_t)v) * 0x10001u; }
+
+// --- cross-lane moves ----------------------------------------------------------
+// Lane l receives lane l-1's dword (DPP wave_shr:1); lane 0 receives 0.
+// A zero shifted into the first cell is harmless everywhere: every
+// transition into cell 0 is minus infinity (-32768, -2^30 or probability 0),
+// and adding it to 0 gives minus infinity again.
+__device__ __forceinline__ uint32_t lane_up(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x138, 0xf, 0xf, true);
+}
+__device__ __forceinline__ int lane_up_i(int v) { return (int)lane_up((uint32_t)v); }
+__device__ __forceinline__ float lane_up_f(float v) {
+  return __builtin_bit_cast(float, lane_up(__builtin_bit_cast(uint32_t, v)));
+}
+// Packed layout: shift every 16-bit slot up by one (slot 2l <- slot 2l-1,
+// slot 2l+1 <- slot 2l); slot 0 receives 0.
+__device__ __forceinline__ uint32_t slot_up16(uint32_t v) {
+  uint32_t prev = lane_up(v);
+  return __builtin_amdgcn_alignbit(v, prev, 16);
+}
+
+__device__ __forceinline__ bool any_lane(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
+
+__device__ __forceinline__ int wave_max_i32(int v) {
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off));
+  return uni(v);
+}
+
+// DPP row shift within 16-lane rows; lanes without a source get `fill`.
+template <int CTRL, int ROWMASK = 0xf>
+__device__ __forceinline__ float dpp_f(float v, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, v), CTRL, ROWMASK,
+                                                               0xf, false));
+}
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+
+// Inclusive prefix scan across the wave of affine maps x -> a + p*x
+// (composition order: lane l applies after lanes < l).
+__device__ __forceinline__ void scan_affine(float &a, float &p) {
+#define HMM_AFFINE_STEP(CTRL, MASK)                  \
+  {                                                  \
+    float ap = dpp_f<CTRL, MASK>(a, 0.0f);           \
+    float pp = dpp_f<CTRL, MASK>(p, 1.0f);           \
+    a = fmaf(p, ap, a);                              \
+    p = p * pp;                                      \
+  }
+  HMM_AFFINE_STEP(kRowShr1, 0xf)
+  HMM_AFFINE_STEP(kRowShr2, 0xf)
+  HMM_AFFINE_STEP(kRowShr4, 0xf)
+  HMM_AFFINE_STEP(kRowShr8, 0xf)
+  HMM_AFFINE_STEP(kRowBcast15, 0xa)
+  HMM_AFFINE_STEP(kRowBcast31, 0xc)
+#undef HMM_AFFINE_STEP
+}
+
+// Sum across the wave (result uniform).
+__device__ __forceinline__ float wave_sum_f(float v) {
+  v += dpp_f<kRowShr1, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr2, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr4, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr8, 0xf>(v, 0.0f);
+  v += dpp_f<kRowBcast15, 0xa>(v, 0.0f);
+  v += dpp_f<kRowBcast31, 0xc>(v, 0.0f);
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Residue stream of one target: lane j holds dword j of the current 256-byte
+// chunk; the next chunk is prefetched.  Reads may run up to 768 bytes past
+// the target, which the packed database allocation covers.
+struct ResidueStream {
+  const uint32_t *p;
+  uint32_t cur, nxt;
+  __device__ __forceinline__ void init(const uint8_t *x, int lane) {
+    p = (const uint32_t *)x;
+    cur = __builtin_nontemporal_load(p + lane);
+    nxt = __builtin_nontemporal_load(p + 64 + lane);
+  }
+  __device__ __forceinline__ void advance(int chunk, int lane) {
+    cur = nxt;
+    nxt = __builtin_nontemporal_load(p + (size_t)(chunk + 2) * 64 + lane);
+  }
+  __device__ __forceinline__ uint32_t word(int j) const { return (uint32_t)__builtin_amdgcn_readlane((int)cur, j); }
+};
+
+// ============================================================================ MSV
+//
+// Per row i (residue a), with previous-row mm and xB:
+//   xBe = xB (-) ENTRY8;  mm[k] = (max(mm[k-1], xBe) (+) BIAS8) (-) COST8_k(a)
+//   xE = max mm; overflow if xE >= 255 - BIAS8; xJ = max(xJ, xE (-) EXIT8);
+//   xB = max(BASE8 (-) MOVE8, xJ (-) MOVE8)
+// xB only depends on max(xJ, BASE8): a running per-lane maximum of all cells
+// is compared each row against the smallest value that could change xB or
+// overflow; only then is the wave-wide maximum taken.  The final xJ is the
+// running maximum (-) EXIT8.
+
+template <int Q>
+__global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOut out) {
+  extern __shared__ uint32_t lds[];
+  {
+    const uint4 *src = (const uint4 *)P.msv;
+    uint4 *dst = (uint4 *)lds;
+    for (int i = threadIdx.x; i < kAlpha * Q * kWave / 4; i += blockDim.x) dst[i] = src[i];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wpb = blockDim.x >> 6;
+  const int64_t nw = (int64_t)gridDim.x * wpb;
+  const int bias8 = P.bias8, entry8 = P.entry8, exit8 = P.exit8;
+  const uint32_t bias2 = splat16(bias8 << 8);
+  const int ovf_line = 255 - bias8;
+  for (int64_t t = (int64_t)blockIdx.x * wpb + uni(threadIdx.x >> 6); t < db.n; t += nw) {
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const int mv = lp.move8;
+    const int base = max(kBase8 - mv, 0);
+    int xJt = 0;
+    bool ovf = ovf_line <= 0;
+    uint32_t acc = 0;
+    if (!ovf) {
+      uint32_t mm[Q];
+#pragma unroll
+      for (int q = 0; q < Q; q++) mm[q] = 0;
+      int T = min(ovf_line, kBase8 + 4);
+      uint32_t thr2 = splat16((T << 8) - 1);
+      uint32_t xbe2 = splat16(max(base - entry8, 0) << 8);
+      ResidueStream rs;
+      rs.init(db.res + db.start[t], lane);
+      const uint32_t *tab = lds + lane;
+      for (int c0 = 0; c0 < L; c0 += 256) {
+        const int nwords = min(64, (L - c0 + 3) >> 2);
+        for (int j = 0; j < nwords; j++) {
+          const uint32_t w = rs.word(j);
+          const int nr = min(4, L - c0 - 4 * j);
+          for (int r = 0; r < nr; r++) {
+            const int a = (w >> (8 * r)) & 0xff;
+            const uint32_t *row = tab + a * (Q * kWave);
+            const uint32_t sh = slot_up16(mm[Q - 1]);
+#pragma unroll
+            for (int q = Q - 1; q >= 0; q--) {
+              uint32_t v = u16_max(q ? mm[q - 1] : sh, xbe2);
+              v = u16_adds(v, bias2);
+              v = u16_subs(v, row[q * kWave]);
+              acc = u16_max(acc, v);
+              mm[q] = v;
+            }
+            if (any_lane(u16_subs(acc, thr2) != 0u)) {
+              const int m = wave_max_i32((int)(max(acc & 0xffffu, acc >> 16) >> 8));
+              if (m >= ovf_line) {
+                ovf = true;
+                goto msv_done;
+              }
+              xJt = max(xJt, max(m - exit8, 0));
+              const int xB = max(base, max(xJt - mv, 0));
+              xbe2 = splat16(max(xB - entry8, 0) << 8);
+              T = min(ovf_line, max(xJt, kBase8) + 4);
+              thr2 = splat16((T << 8) - 1);
+            }
+          }
+        }
+        rs.advance(c0 >> 8, lane);
+      }
+    }
+  msv_done:
+    int raw = 255;
+    if (!ovf) {
+      const int m = wave_max_i32((int)(max(acc & 0xffffu, acc >> 16) >> 8));
+      const int xJ = max(m - exit8, 0);
+      raw = max(xJ - mv, 0);
+    }
+    const bool pass = ovf || raw >= lp.thr8;
+    const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
+    if (lane == 0) {
+      const int64_t c = db.perm[t];
+      db.flags_sorted[t] = fl;
+      out.flags[c] = fl;
+      out.msv[c] = (int16_t)raw;
+      out.vit[c] = INT32_MIN;
+      out.fwd[c] = __builtin_nanf("");
+      if (pass) db.list_vit[atomicAdd(&db.counters[CNT_VIT], 1)] = (int32_t)t;
+    }
+  }
+}
+
+// ============================================================================ Viterbi int16
+//
+// Per row, with previous-row M, I, D and xB, every add saturating on its own:
+//   M_k = sat(max(sat(xB+ENTRY16), sat(M_{k-1}+MM), sat(I_{k-1}+IM), sat(D_{k-1}+DM)) + msc_k(a))
+//   I_k = sat(max(sat(M_k+MI), sat(I_k+II)) + isc_k(a))
+//   D_k = max(sat(M_{k-1}+MD), sat(D_{k-1}+DD))          (current row)
+//   xE = max_k M_k (delete transitions are <= 0, so D_k <= max M);
+//   xJ = max(xJ, sat(xE+EJ16)); xB = max(sat(MOVE16), sat(xJ+MOVE16))
+// overflow if some M or I reaches 32767.  xB depends on max(xJ, 0) only,
+// so the wave-wide maximum is taken only when a cell reaches the value that
+// would raise it.  The delete chain is computed inside each slot, then
+// propagated across slots until no lane changes (exact: sat is monotone).
+
+// Result of one Viterbi target.
+struct VitResult {
+  int raw;
+  bool ovf;
+};
+
+template <int Q, bool EMIT_LDS>
+__device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ emit, const uint32_t (&tr)[TR_N][Q],
+                                                  const DevProfile &P, const uint8_t *x, int L,
+                                                  const LenParams &lp, int lane) {
+  uint32_t M[Q], I[Q], D[Q];
+#pragma unroll
+  for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNegNeg;
+  uint32_t accM = kNegNeg, accI = kNegNeg;
+  const int mv = lp.move16, ej = P.ej16, entry = P.entry16;
+  auto sat = [](int v) { return max(-32768, min(32767, v)); };
+  int xJt = kNeg16;
+  int xB = sat(mv);
+  uint32_t xbe2 = splat16(sat(xB + entry));
+  int T = min(-ej + 1, 32767);
+  uint32_t tm1 = splat16(T - 1);
+  bool ovf = false;
+  ResidueStream rs;
+  rs.init(x, lane);
+  for (int c0 = 0; c0 < L; c0 += 256) {
+    const int nwords = min(64, (L - c0 + 3) >> 2);
+    for (int j = 0; j < nwords; j++) {
+      const uint32_t w = rs.word(j);
+      const int nr = min(4, L - c0 - 4 * j);
+      for (int r = 0; r < nr; r++) {
+        const int a = (w >> (8 * r)) & 0xff;
+        const uint32_t *er = emit + a * (2 * Q * kWave) + lane;
+        const uint32_t msh = slot_up16(M[Q - 1]);
+        const uint32_t ish = slot_up16(I[Q - 1]);
+        const uint32_t dsh = slot_up16(D[Q - 1]);
+#pragma unroll
+        for (int q = Q - 1; q >= 0; q--) {
+          const uint32_t pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+          uint32_t m = i16_max(xbe2, i16_adds(pm, tr[TR_MMIN][q]));
+          m = i16_max(m, i16_adds(pi, tr[TR_IMIN][q]));
+          m = i16_max(m, i16_adds(pd, tr[TR_DMIN][q]));
+          const uint32_t mn = i16_adds(m, er[q * kWave]);
+          const uint32_t in =
+              i16_adds(i16_max(i16_adds(M[q], tr[TR_MI][q]), i16_adds(I[q], tr[TR_II][q])), er[(Q + q) * kWave]);
+          accM = i16_max(accM, mn);
+          accI = i16_max(accI, in);
+          M[q] = mn;
+          I[q] = in;
+        }
+        {
+          uint32_t dc = kNegNeg;
+          const uint32_t din = slot_up16(M[Q - 1]);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            D[q] = i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q]));
+            dc = D[q];
+          }
+          for (int it = 0; it < 2 * kWave; it++) {
+            dc = slot_up16(D[Q - 1]);
+            bool moved = true;
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+              if (moved) {
+                const uint32_t nd = i16_max(D[q], i16_adds(dc, tr[TR_DDIN][q]));
+                moved = any_lane(nd != D[q]);
+                D[q] = nd;
+                dc = nd;
+              }
+            }
+            if (!moved) break;
+          }
+        }
+        if (any_lane(i16_max(accM, tm1) != tm1)) {
+          const int hi = (int)(int16_t)(accM >> 16), lo = (int)(int16_t)(accM & 0xffffu);
+          const int m = wave_max_i32(max(hi, lo));
+          if (m >= 32767) {
+            ovf = true;
+            goto vit_done;
+          }
+          xJt = max(xJt, sat(m + ej));
+          xB = max(sat(mv), sat(xJt + mv));
+          xbe2 = splat16(sat(xB + entry));
+          T = min(max(xJt, 0) - ej + 1, 32767);
+          tm1 = splat16(T - 1);
+        }
+      }
+    }
+    rs.advance(c0 >> 8, lane);
+  }
+vit_done:
+  if (!ovf) {
+    const int hi = (int)(int16_t)(accI >> 16), lo = (int)(int16_t)(accI & 0xffffu);
+    ovf = any_lane(max(hi, lo) >= 32767);
+  }
+  VitResult res;
+  res.ovf = ovf;
+  if (ovf) {
+    res.raw = 32767;
+  } else {
+    const int hi = (int)(int16_t)(accM >> 16), lo = (int)(int16_t)(accM & 0xffffu);
+    const int m = wave_max_i32(max(hi, lo));
+    const int xJ = sat(m + ej);
+    res.raw = sat(xJ + mv);
+  }
+  return res;
+}
+
+template <int Q, bool EMIT_LDS>
+__global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevOut out) {
+  extern __shared__ uint32_t lds[];
+  const int lane = threadIdx.x & 63;
+  if (EMIT_LDS) {
+    const uint4 *src = (const uint4 *)P.vit_emit;
+    uint4 *dst = (uint4 *)lds;
+    for (int i = threadIdx.x; i < kAlpha * 2 * Q * kWave / 4; i += blockDim.x) dst[i] = src[i];
+    __syncthreads();
+  }
+  const uint32_t *emit = EMIT_LDS ? (const uint32_t *)lds : P.vit_emit;
+  uint32_t tr[TR_N][Q];
+#pragma unroll
+  for (int k = 0; k < TR_N; k++)
+#pragma unroll
+    for (int q = 0; q < Q; q++) tr[k][q] = P.vit_tr[(k * Q + q) * kWave + lane];
+  const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
+  for (;;) {
+    int idx = 0;
+    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_VIT], 1);
+    idx = __shfl(idx, 0);
+    idx = uni(idx);
+    if (idx >= count) break;
+    const int t = uni(db.list_vit[idx]);
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const VitResult r = vit16_target<Q, EMIT_LDS>(emit, tr, P, db.res + db.start[t], L, lp, lane);
+    const bool pass = r.ovf || r.raw >= lp.thr16;
+    if (lane == 0) {
+      const uint8_t fl = db.flags_sorted[t] | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0);
+      const int64_t c = db.perm[t];
+      db.flags_sorted[t] = fl;
+      out.flags[c] = fl;
+      out.vit[c] = r.raw;
+      if (r.ovf) db.list_ovf[atomicAdd(&db.counters[CNT_OVF], 1)] = t;
+      if (pass) db.list_fwd[atomicAdd(&db.counters[CNT_FWD], 1)] = t;
+    }
+  }
+}
+
+// ============================================================================ Viterbi int32 rescore
+//
+// The int16 recurrence in int32 with every add floored at -2^30 and no upper
+// clamp; run on the targets that overflowed int16.  Tables are read through
+// the caches (few targets).
+
+__device__ __forceinline__ int fl32(int v) { return max(v, kNeg32); }
+
+template <int Q>
+__global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
+  const int lane = threadIdx.x & 63;
+  const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
+  const int *trp = P.v32_tr + lane;
+  for (;;) {
+    int idx = 0;
+    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_OVF], 1);
+    idx = uni(__shfl(idx, 0));
+    if (idx >= count) break;
+    const int t = uni(db.list_ovf[idx]);
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const int mv = lp.move16, ej = P.ej16, entry = P.entry16;
+    int M[Q], I[Q], D[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNeg32;
+    int accM = kNeg32;
+    int xJt = kNeg32;
+    int xB = fl32(mv);
+    int xbe = fl32(xB + entry);
+    int T = -ej + 1;
+    ResidueStream rs;
+    rs.init(db.res + db.start[t], lane);
+    for (int c0 = 0; c0 < L; c0 += 256) {
+      const int nwords = min(64, (L - c0 + 3) >> 2);
+      for (int j = 0; j < nwords; j++) {
+        const uint32_t w = rs.word(j);
+        const int nr = min(4, L - c0 - 4 * j);
+        for (int r = 0; r < nr; r++) {
+          const int a = (w >> (8 * r)) & 0xff;
+          const int *er = P.v32_emit + a * (2 * Q * kWave) + lane;
+          const int msh = lane_up_i(M[Q - 1]);
+          const int ish = lane_up_i(I[Q - 1]);
+          const int dsh = lane_up_i(D[Q - 1]);
+#pragma unroll
+          for (int q = Q - 1; q >= 0; q--) {
+            const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+            int m = max(xbe, fl32(pm + trp[(TR_MMIN * Q + q) * kWave]));
+            m = max(m, fl32(pi + trp[(TR_IMIN * Q + q) * kWave]));
+            m = max(m, fl32(pd + trp[(TR_DMIN * Q + q) * kWave]));
+            const int mn = fl32(m + er[q * kWave]);
+            const int in = fl32(max(fl32(M[q] + trp[(TR_MI * Q + q) * kWave]),
+                                    fl32(I[q] + trp[(TR_II * Q + q) * kWave])) +
+                                er[(Q + q) * kWave]);
+            accM = max(accM, mn);
+            M[q] = mn;
+            I[q] = in;
+          }
+          int dc = kNeg32;
+          const int din = lane_up_i(M[Q - 1]);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            D[q] = max(fl32((q ? M[q - 1] : din) + trp[(TR_MDIN * Q + q) * kWave]),
+                       fl32(dc + trp[(TR_DDIN * Q + q) * kWave]));
+            dc = D[q];
+          }
+          for (int it = 0; it < kWave; it++) {
+            dc = lane_up_i(D[Q - 1]);
+            bool moved = true;
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+              if (moved) {
+                const int nd = max(D[q], fl32(dc + trp[(TR_DDIN * Q + q) * kWave]));
+                moved = any_lane(nd != D[q]);
+                D[q] = nd;
+                dc = nd;
+              }
+            }
+            if (!moved) break;
+          }
+          if (any_lane(accM >= T)) {
+            const int m = wave_max_i32(accM);
+            xJt = max(xJt, fl32(m + ej));
+            xB = max(fl32(mv), fl32(xJt + mv));
+            xbe = fl32(xB + entry);
+            T = max(xJt, 0) - ej + 1;
+          }
+        }
+      }
+      rs.advance(c0 >> 8, lane);
+    }
+    const int m = wave_max_i32(accM);
+    const int xJ = fl32(m + ej);
+    const int v = fl32(xJ + mv);
+    if (lane == 0) out.vit[db.perm[t]] = v;
+  }
+}
+
+// ============================================================================ Forward fp32
+//
+// Probability space, 1 = the start state.  Per row (residue a):
+//   M_k = e_k(a)/f(a) * (M_{k-1} MM + I_{k-1} IM + D_{k-1} DM + B entry)    (previous row)
+//   I_k = i_k(a)/f(a) * (M_k MI + I_k II)                                    (previous row)
+//   D_k = M_{k-1} MD + D_{k-1} DD                                            (current row)
+//   E = sum_k (M_k + D_k); J = J loop + E/2; C = C loop + E/2; N = N loop;
+//   B = (N + J) move.
+// Values are rescaled by an exact power of two whenever the largest special
+// value leaves [2^-40, 2^40]; the exponents removed are summed.  Result:
+// ln(C * move) + (sum of exponents) ln 2, in nats.
+
+template <int Q>
+__global__ void __launch_bounds__(256) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
+  const int lane = threadIdx.x & 63;
+  const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
+  const float *trp = P.f_tr + lane;
+  float tMM[Q], tIM[Q], tDM[Q], tMD[Q], tDD[Q], tMI[Q], tII[Q], cum[Q];
+#pragma unroll
+  for (int q = 0; q < Q; q++) {
+    tMM[q] = trp[(TR_MMIN * Q + q) * kWave];
+    tIM[q] = trp[(TR_IMIN * Q + q) * kWave];
+    tDM[q] = trp[(TR_DMIN * Q + q) * kWave];
+    tMD[q] = trp[(TR_MDIN * Q + q) * kWave];
+    tDD[q] = trp[(TR_DDIN * Q + q) * kWave];
+    tMI[q] = trp[(TR_MI * Q + q) * kWave];
+    tII[q] = trp[(TR_II * Q + q) * kWave];
+    cum[q] = trp[(TR_N * Q + q) * kWave];
+  }
+  const float slotP = cum[Q - 1];
+  const float entry_p = P.entry_p;
+  for (;;) {
+    int idx = 0;
+    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_FWD], 1);
+    idx = uni(__shfl(idx, 0));
+    if (idx >= count) break;
+    const int t = uni(db.list_fwd[idx]);
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const float loop = lp.loop_p, move = lp.move_p;
+    float M[Q], I[Q], D[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = 0.0f;
+    float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
+    int shift = 0;
+    ResidueStream rs;
+    rs.init(db.res + db.start[t], lane);
+    for (int c0 = 0; c0 < L; c0 += 256) {
+      const int nwords = min(64, (L - c0 + 3) >> 2);
+      for (int j = 0; j < nwords; j++) {
+        const uint32_t w = rs.word(j);
+        const int nr = min(4, L - c0 - 4 * j);
+        for (int r = 0; r < nr; r++) {
+          const int a = (w >> (8 * r)) & 0xff;
+          const float *er = P.f_emit + a * (2 * Q * kWave) + lane;
+          const float msh = lane_up_f(M[Q - 1]);
+          const float ish = lane_up_f(I[Q - 1]);
+          const float dsh = lane_up_f(D[Q - 1]);
+          const float bent = B * entry_p;
+#pragma unroll
+          for (int q = Q - 1; q >= 0; q--) {
+            const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+            const float sm = fmaf(pm, tMM[q], fmaf(pi, tIM[q], fmaf(pd, tDM[q], bent)));
+            const float si = fmaf(M[q], tMI[q], I[q] * tII[q]);
+            M[q] = er[q * kWave] * sm;
+            I[q] = er[(Q + q) * kWave] * si;
+          }
+          // delete chain: within the slot, then across slots by an affine scan
+          const float din = lane_up_f(M[Q - 1]);
+          float dc = 0.0f;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            D[q] = fmaf(q ? M[q - 1] : din, tMD[q], dc * tDD[q]);
+            dc = D[q];
+          }
+          float sa = D[Q - 1], sp = slotP;
+          scan_affine(sa, sp);
+          const float carry = lane_up_f(sa);
+          float part = 0.0f;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            D[q] = fmaf(carry, cum[q], D[q]);
+            part += M[q] + D[q];
+          }
+          const float E = wave_sum_f(part);
+          J = fmaf(J, loop, 0.5f * E);
+          C = fmaf(C, loop, 0.5f * E);
+          N = N * loop;
+          B = (N + J) * move;
+          const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
+          if (big > 0x1p40f || big < 0x1p-40f) {
+            int ex;
+            (void)frexpf(big, &ex);
+            ex = uni(ex);
+            const float s = ldexpf(1.0f, -ex);
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+              M[q] *= s;
+              I[q] *= s;
+              D[q] *= s;
+            }
+            J *= s;
+            C *= s;
+            N *= s;
+            B *= s;
+            shift += ex;
+          }
+        }
+      }
+      rs.advance(c0 >> 8, lane);
+    }
+    const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
+    const bool pass = f > lp.fthr;
+    if (lane == 0) {
+      const uint8_t fl = db.flags_sorted[t] | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0);
+      const int64_t c = db.perm[t];
+      out.fwd[c] = f;
+      out.flags[c] = fl;
+      if (pass) atomicAdd(&db.counters[CNT_FWD_PASS], 1);
+    }
+  }
+}
+
+// ============================================================================ small kernels
+
+__global__ void clear_counters(int32_t *c) {
+  if (threadIdx.x < CNT_N) c[threadIdx.x] = 0;
+}
+
+__global__ void export_counts(const int32_t *c, int64_t *counts) {
+  if (threadIdx.x == 0) {
+    counts[0] = c[CNT_VIT];
+    counts[1] = c[CNT_OVF];
+    counts[2] = c[CNT_FWD];
+    counts[3] = c[CNT_FWD_PASS];
+  }
+}
+
+// ============================================================================ launcher
+
+int g_num_cu = 0;
+
+int num_cu() {
+  if (!g_num_cu) {
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    (void)hipDeviceGetAttribute(&g_num_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (g_num_cu <= 0) g_num_cu = 256;
+  }
+  return g_num_cu;
+}
+
+template <typename K>
+int blocks_per_cu(K kernel, int threads, size_t lds) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, lds) != hipSuccess || nb < 1) nb = 1;
+  return nb;
+}
+
+template <int Q>
+hipError_t launch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  const int threads = Q >= 12 ? 1024 : 512;
+  const size_t lds = (size_t)kAlpha * Q * kWave * 4;
+  auto k = msv_kernel<Q>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(k, threads, lds);
+  const int64_t waves_needed = db.n;
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (waves_needed + threads / 64 - 1) / (threads / 64);
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), lds, s, P, db, o);
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  constexpr bool kLds = Q <= 8;
+  const int threads = 512;
+  const size_t lds = kLds ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0;
+  auto k = vit16_kernel<Q, kLds>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(k, threads, lds);
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), lds, s, P, db, o);
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t launch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  const int threads = 256;
+  auto k = vit32_kernel<Q>;
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(k, threads, 0);
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, P, db, o);
+  return hipGetLastError();
+}
+
+template <int Q>
+hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  const int threads = 256;
+  auto k = fwd_kernel<Q>;
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(k, threads, 0);
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, P, db, o);
+  return hipGetLastError();
+}
+
+#define HMM_Q8_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14) X(16) X(20) X(24)
+#define HMM_Q32_CASES(X) \
+  X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12) X(14) X(16) X(20) X(24) X(28) X(32) X(40) X(48)
+
+hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  switch (P.Q8) {
+#define HMM_CASE(q) \
+  case q:           \
+    return launch_msv<q>(P, db, o, s);
+    HMM_Q8_CASES(HMM_CASE)
+#undef HMM_CASE
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t dispatch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  switch (P.Q8) {
+#define HMM_CASE(q) \
+  case q:           \
+    return launch_vit16<q>(P, db, o, s);
+    HMM_Q8_CASES(HMM_CASE)
+#undef HMM_CASE
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t dispatch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  switch (P.Q32) {
+#define HMM_CASE(q) \
+  case q:           \
+    return launch_vit32<q>(P, db, o, s);
+    HMM_Q32_CASES(HMM_CASE)
+#undef HMM_CASE
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t dispatch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  switch (P.Q32) {
+#define HMM_CASE(q) \
+  case q:           \
+    return launch_fwd<q>(P, db, o, s);
+    HMM_Q32_CASES(HMM_CASE)
+#undef HMM_CASE
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_search(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s, hipEvent_t *ev) {
+  if (db.n <= 0) return hipSuccess;
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[i], s);
+  };
+  mark(0);
+  hipLaunchKernelGGL(clear_counters, dim3(1), dim3(64), 0, s, db.counters);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = dispatch_msv(P, db, o, s);
+  mark(1);
+  if (e == hipSuccess) e = dispatch_vit16(P, db, o, s);
+  mark(2);
+  if (e == hipSuccess) e = dispatch_vit32(P, db, o, s);
+  mark(3);
+  if (e == hipSuccess) e = dispatch_fwd(P, db, o, s);
+  if (e == hipSuccess && o.counts) {
+    hipLaunchKernelGGL(export_counts, dim3(1), dim3(64), 0, s, db.counters, o.counts);
+    e = hipGetLastError();
+  }
+  mark(4);
+  return e;
+}
+
+}  // namespace hmmgpu

@@ -1,0 +1,362 @@
+"""GPU parity: the HIP search (through the C ABI) against the CPU oracle on
+the same seeded inputs.
+
+Bar: MSV scores, Viterbi scores (int16, and exact int32 after overflow) and
+all flag bits bit-exact; Forward within 1e-3 + 1e-5 |x| nats of the fp64
+oracle.  Sizes: whole workloads where the oracle finishes in seconds;
+sampled targets (random plus every kind of planted homolog) at the full
+workload sizes, in the same launch configuration the benchmark times.
+"""
+import math
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2111_06340_amd as hg
+from conftest import random_profile
+from synth import gen
+
+pytestmark = pytest.mark.gpu
+
+FWD_ABS, FWD_REL = 1e-3, 1e-5
+NTHREADS = 16
+
+
+def announce(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    hg.lib()
+    return torch
+
+
+def run_gpu(prof, residues, offsets, calib, F, stream=None):
+    import torch
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(residues, offsets)
+    out = hg.alloc_results(D.n)
+    announce(f"search M={prof.M} n={D.n} residues={D.n_residues} max_len={D.max_len} F={F}")
+    hg.search(P, D, F, out, stream=stream)
+    torch.cuda.synchronize()
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    P.close()
+    D.close()
+    return res
+
+
+def compare(g, o, idx=None, what=""):
+    """g: GPU results (caller order), o: oracle results for targets idx."""
+    if idx is None:
+        idx = np.arange(o["msv"].size)
+    gm, gv, gf, gl = g["msv"][idx], g["vit"][idx], g["fwd"][idx], g["flags"][idx]
+    bad = np.nonzero(gm != o["msv"])[0]
+    assert bad.size == 0, f"{what} msv mismatch at {idx[bad[:5]]}: gpu {gm[bad[:5]]} oracle {o['msv'][bad[:5]]}"
+    bad = np.nonzero(gl != o["flags"])[0]
+    assert bad.size == 0, f"{what} flags mismatch at {idx[bad[:5]]}: gpu {gl[bad[:5]]} oracle {o['flags'][bad[:5]]}"
+    bad = np.nonzero(gv != o["vit"])[0]
+    assert bad.size == 0, f"{what} vit mismatch at {idx[bad[:5]]}: gpu {gv[bad[:5]]} oracle {o['vit'][bad[:5]]}"
+    ran = ~np.isnan(o["fwd"])
+    assert np.array_equal(ran, ~np.isnan(gf)), f"{what} Forward ran on different targets"
+    err = np.abs(gf[ran].astype(np.float64) - o["fwd"][ran])
+    tol = FWD_ABS + FWD_REL * np.abs(o["fwd"][ran])
+    if err.size:
+        worst = int(np.argmax(err - tol))
+        assert np.all(err <= tol), (f"{what} fwd off by {err[worst]:.3g} (tol {tol[worst]:.3g}) at "
+                                    f"{idx[ran][worst]}: gpu {gf[ran][worst]} oracle {o['fwd'][ran][worst]}")
+    return dict(n=idx.size, fwd_ran=int(ran.sum()), fwd_max_err=float(err.max()) if err.size else 0.0,
+                vit_ovf=int(np.sum((o["flags"] & oracle.F_VIT_OVF) != 0)),
+                msv_ovf=int(np.sum((o["flags"] & oracle.F_MSV_OVF) != 0)))
+
+
+def oracle_search(prof, residues, offsets, calib, F):
+    op = oracle.OracleProfile(prof)
+    return oracle.search(op, residues, offsets, calib, F, nthreads=NTHREADS)
+
+
+def sub_db(db, idx):
+    seqs = [db.seq(int(i)) for i in idx]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    return np.concatenate(seqs) if seqs else np.zeros(0, np.uint8), off
+
+
+# ------------------------------------------------------------ whole workloads
+
+def test_c1_all_stages_on_every_target():
+    w = gen.WORKLOADS["C1"]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    g = run_gpu(prof, db.residues, db.offsets, calib, w.F)
+    o = oracle_search(prof, db.residues, db.offsets, calib, w.F)
+    st = compare(g, o, what="C1")
+    assert st["fwd_ran"] == db.n            # F = 1: every target reaches Forward
+    announce(f"C1 ok {st}")
+
+
+@pytest.mark.parametrize("name,n", [("C2", 20000), ("C3", 3000), ("C5", 600)])
+def test_reduced_workload_filter_pipeline(name, n):
+    w = gen.WORKLOADS[name]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=n, prof=prof)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    g = run_gpu(prof, db.residues, db.offsets, calib, w.F)
+    o = oracle_search(prof, db.residues, db.offsets, calib, w.F)
+    st = compare(g, o, what=name)
+    assert st["fwd_ran"] > 0
+    announce(f"{name} reduced n={n} ok {st}")
+
+
+@pytest.mark.parametrize("name,n", [("C1", 5000), ("C3", 2000)])
+def test_reduced_workload_every_stage(name, n):
+    # thresholds at 1: Viterbi, rescore and Forward on every target
+    w = gen.WORKLOADS[name]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=n, prof=prof)
+    calib = (0.0, 0.0, 0.0)
+    g = run_gpu(prof, db.residues, db.offsets, calib, (1.0, 1.0, 1.0))
+    o = oracle_search(prof, db.residues, db.offsets, calib, (1.0, 1.0, 1.0))
+    st = compare(g, o, what=name)
+    assert st["fwd_ran"] == db.n
+    announce(f"{name} all-stages ok {st}")
+
+
+# ------------------------------------------------------------ full sizes, sampled
+
+_DB_CACHE = {}
+
+
+def full_db(name):
+    if name not in _DB_CACHE:
+        w = gen.WORKLOADS[name]
+        t = time.time()
+        prof = gen.workload_profile(w)
+        _DB_CACHE.clear()
+        _DB_CACHE[name] = (prof, gen.workload_database(w, prof=prof))
+        announce(f"generated {name} in {time.time() - t:.1f}s")
+    return _DB_CACHE[name]
+
+
+def sample_ids(db, n_random, n_planted, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.choice(db.n, size=min(n_random, db.n), replace=False)
+    p = db.planted[rng.choice(db.planted.size, size=min(n_planted, db.planted.size), replace=False)] \
+        if db.planted.size else np.zeros(0, np.int64)
+    return np.unique(np.concatenate([r, p]).astype(np.int64))
+
+
+@pytest.mark.parametrize("name,n_random,n_planted", [("C2", 400, 100), ("C3", 300, 80), ("C5", 200, 40)])
+def test_full_size_sampled(name, n_random, n_planted):
+    w = gen.WORKLOADS[name]
+    prof, db = full_db(name)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    g = run_gpu(prof, db.residues, db.offsets, calib, w.F)
+    idx = sample_ids(db, n_random, n_planted, seed=w.index)
+    res, off = sub_db(db, idx)
+    t = time.time()
+    o = oracle_search(prof, res, off, calib, w.F)
+    st = compare(g, o, idx, what=name)
+    announce(f"{name} full n={db.n} sampled {idx.size} (oracle {time.time() - t:.1f}s) ok {st}")
+    # whole-DB properties that need no oracle
+    fl = g["flags"]
+    assert np.all((fl & hg.HMM_VIT_RAN != 0) == (fl & hg.HMM_MSV_PASS != 0))
+    assert np.all((fl & hg.HMM_FWD_RAN != 0) == (fl & hg.HMM_VIT_PASS != 0))
+    assert np.all(g["vit"][(fl & hg.HMM_VIT_RAN) == 0] == np.iinfo(np.int32).min)
+    assert np.all(np.isnan(g["fwd"][(fl & hg.HMM_FWD_RAN) == 0]))
+    msv_pass = np.mean((fl & hg.HMM_MSV_PASS) != 0)
+    assert 0.005 < msv_pass < 0.06, msv_pass
+
+
+def test_c4_profiles_sampled():
+    prof3, db = full_db("C3")
+    profiles = gen.c4_profiles()
+    F = gen.WORKLOADS["C3"].F
+    for p_i, prof in enumerate(profiles):
+        if p_i % 8 != 0:
+            continue
+        calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+        g = run_gpu(prof, db.residues, db.offsets, calib, F)
+        idx = sample_ids(db, 60, 20, seed=100 + p_i)
+        res, off = sub_db(db, idx)
+        o = oracle_search(prof, res, off, calib, F)
+        st = compare(g, o, idx, what=f"C4 profile {p_i} M={prof.M}")
+        announce(f"C4 profile {p_i} M={prof.M} ok {st}")
+
+
+# ------------------------------------------------------------ edge cases
+
+EDGE_LENGTHS = [1, 2, 3, 4, 5, 7, 15, 16, 17, 63, 64, 65, 255, 256, 257, 511, 512, 513, 767, 768, 769,
+                1023, 1024, 1025, 2047, 4096, 7000]
+
+
+def _ragged_db(prof, seed, lengths=EDGE_LENGTHS, homolog_every=3):
+    rng = np.random.default_rng(seed)
+    seqs = []
+    homs = gen.sample_homologs(rng, prof, len(lengths))
+    for i, L in enumerate(lengths):
+        s = gen.background_residues(rng, L)
+        if i % homolog_every == 0:
+            h = homs[i][:L]
+            o = int(rng.integers(0, L - h.size + 1))
+            s[o:o + h.size] = h
+        seqs.append(s)
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    return np.concatenate(seqs), off
+
+
+@pytest.mark.parametrize("M", [1, 2, 3, 77, 127, 128, 129, 255, 256, 257, 733, 734, 1000, 1281])
+def test_edge_lengths_and_profile_sizes(M):
+    prof = gen.make_profile(M, 500 + M)
+    res, off = _ragged_db(prof, M)
+    calib = (0.0, 0.0, 0.0)
+    F = (1.0, 1.0, 1.0)
+    g = run_gpu(prof, res, off, calib, F)
+    o = oracle_search(prof, res, off, calib, F)
+    st = compare(g, o, what=f"edge M={M}")
+    announce(f"edge M={M} ok {st}")
+
+
+def test_largest_profile():
+    M = hg.HMM_MAX_M
+    prof = gen.make_profile(M, 77)
+    res, off = _ragged_db(prof, 1, lengths=[1, 31, 300, 3100, 600], homolog_every=3)
+    g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    announce(f"M={M} ok {compare(g, o, what='max M')}")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_random_transitions_exercise_insert_and_delete_paths(seed):
+    prof = random_profile(300, 40 + seed, alpha=0.3, talpha=0.6)
+    res, off = _ragged_db(prof, seed, lengths=[50, 300, 301, 700, 1200, 90, 2000, 5, 333] * 3,
+                          homolog_every=2)
+    g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    announce(f"random transitions seed={seed} ok {compare(g, o, what='random-trans')}")
+
+
+def _peaked(M, seed, p_top=0.81):
+    rng = np.random.default_rng(seed)
+    c = rng.integers(0, 19, size=M)
+    bg = np.full(20, 0.05)
+    match = np.full((M, 20), (1 - p_top) / 19)
+    match[np.arange(M), c] = p_top
+    insert = np.tile(bg, (M - 1, 1))
+    trans = np.tile([0.9, 0.05, 0.05, 0.6, 0.4, 0.5, 0.5], (M - 1, 1))
+    return gen.Profile(M, bg, match, insert, trans), c.astype(np.uint8)
+
+
+@pytest.mark.parametrize("M", [40, 200, 700])
+def test_overflow_and_rescore(M):
+    prof, c = _peaked(M, M)
+    rng = np.random.default_rng(M)
+    seqs = [c, np.concatenate([gen.background_residues(rng, 50), c, gen.background_residues(rng, 30)])]
+    for d in (0.05, 0.2, 0.4, 0.6):
+        mut = c.copy()
+        m = rng.random(M) < d
+        mut[m] = rng.integers(0, 20, size=int(m.sum()))
+        seqs.append(mut)
+    seqs.append(np.concatenate([c[: M // 2], c[M // 3:]]))           # repeat: two hits
+    seqs.append(gen.background_residues(rng, 400))
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    res = np.concatenate(seqs)
+    for F in ((1.0, 1.0, 1.0), (0.02, 1e-3, 1.0)):
+        calib = (-8.0, -9.0, -4.0)
+        g = run_gpu(prof, res, off, calib, F)
+        o = oracle_search(prof, res, off, calib, F)
+        st = compare(g, o, what=f"peaked M={M}")
+        assert st["vit_ovf"] >= 1 and st["msv_ovf"] >= 1
+        announce(f"overflow M={M} F={F} ok {st}")
+
+
+def test_degenerate_and_extreme_profiles():
+    rng = np.random.default_rng(5)
+    # BIAS8 clamps at 255: MSV overflows on every target
+    bg = np.full(20, 0.05)
+    match = np.full((30, 20), 0.05)
+    match[7, 0] = 1e-300
+    match[7, 1] += 0.05 - 1e-300
+    deg = gen.Profile(30, bg, match, np.tile(bg, (29, 1)), np.tile([0.9, 0.05, 0.05, 0.6, 0.4, 0.5, 0.5], (29, 1)))
+    # extreme: score -32768 in int16, zero inserts and zero transitions
+    ext = gen.make_profile(60, 9)
+    ext.match[3, 0] = 1e-30
+    ext.match[3, 1] += 0.5
+    ext.match[3] /= ext.match[3].sum()
+    ext.insert[2, :] = 0.0
+    ext.insert[2, 5] = 1.0
+    ext.trans[4] = [1.0, 0.0, 0.0, 1.0, 0.0, 0.0, 1.0]
+    ext.trans[10] = [0.0, 0.5, 0.5, 0.0, 1.0, 1.0, 0.0]
+    for name, prof in (("degenerate", deg), ("extreme", ext)):
+        res, off = _ragged_db(prof, 3, lengths=[1, 10, 60, 61, 300, 1000, 64, 128, 129], homolog_every=2)
+        res = res.copy()
+        res[::7] = 0                                  # many copies of the near-impossible residue
+        g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        announce(f"{name} ok {compare(g, o, what=name)}")
+    assert rng is not None
+
+
+def test_empty_and_single_target_databases():
+    import torch
+    prof = gen.make_profile(50, 1)
+    P = hg.Profile(prof, 0.0, 0.0, 0.0)
+    D0 = hg.Database(np.zeros(0, np.uint8), np.zeros(1, np.int64))
+    assert D0.n == 0
+    out = hg.alloc_results(0)
+    hg.search(P, D0, (1.0, 1.0, 1.0), out)
+    torch.cuda.synchronize()
+    for L in (1, 2, 777):
+        x = gen.background_residues(np.random.default_rng(L), L)
+        off = np.array([0, L], np.int64)
+        g = run_gpu(prof, x, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        o = oracle_search(prof, x, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        compare(g, o, what=f"single L={L}")
+    D0.close()
+    P.close()
+
+
+def test_repeated_searches_streams_and_threshold_changes():
+    import torch
+    w = gen.WORKLOADS["C2"]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=5000, prof=prof)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(db.residues, db.offsets)
+    s = torch.cuda.Stream()
+    outs = []
+    for F in ((0.02, 1e-3, 1.0), (1.0, 1.0, 1.0), (0.02, 1e-3, 1.0), (0.1, 0.01, 0.5)):
+        out = hg.alloc_results(D.n)
+        with torch.cuda.stream(s):
+            hg.search(P, D, F, out)
+        outs.append((F, out))
+    torch.cuda.synchronize()
+    for F, out in outs:
+        g = {k: v.cpu().numpy() for k, v in out.items()}
+        o = oracle_search(prof, db.residues, db.offsets, calib, F)
+        if F[2] < 1.0:
+            # FWD_PASS is an fp32 compare: check it only away from the cutoff
+            _, _, ft = np.vectorize(lambda L: oracle.thresholds(calib, F, int(L)), otypes=[int, int, float])(
+                np.diff(db.offsets))
+            close = np.abs(o["fwd"] - ft) <= FWD_ABS + FWD_REL * np.abs(o["fwd"])
+            g["flags"] = np.where(close, (g["flags"] & ~np.uint8(hg.HMM_FWD_PASS)) |
+                                  (o["flags"] & np.uint8(hg.HMM_FWD_PASS)), g["flags"])
+        st = compare(g, o, what=f"repeat F={F}")
+        counts = out["counts"].cpu().numpy()
+        fl = o["flags"]
+        assert counts[0] == np.sum((fl & hg.HMM_MSV_PASS) != 0)
+        assert counts[1] == np.sum((fl & hg.HMM_VIT_OVF) != 0)
+        assert counts[2] == np.sum((fl & hg.HMM_VIT_PASS) != 0)
+        announce(f"repeat F={F} ok {st} counts={counts.tolist()}")
+    P.close()
+    D.close()
