@@ -38,6 +38,24 @@ constexpr uint32_t kNegNeg = 0x80008000u;  // two int16 -32768
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Control flow in these kernels is wave-uniform by construction, and the
+// cross-lane operations (DPP, readlane, ballot, bpermute) rely on every lane
+// being active.  Lane-divergent branches are therefore avoided altogether:
+// per-target outputs are stored by all lanes with identical values, and the
+// work counters are bumped by one lane's increment inside a wave-wide atomic.
+
+// Wave index in the grid (scalar).
+__device__ __forceinline__ int wave_id() {
+  return (int)blockIdx.x * uni((int)(blockDim.x >> 6)) + (uni((int)threadIdx.x) >> 6);
+}
+
+// Wave-wide fetch-and-add of `inc` (added once per wave); returns the old
+// value in a scalar.
+__device__ __forceinline__ int wave_fetch_add(int32_t *p, int inc) {
+  const int lane = (int)(threadIdx.x & 63);
+  return uni(atomicAdd(p, lane == 0 ? inc : 0));
+}
+
 // --- packed 16-bit arithmetic ------------------------------------------------
 __device__ __forceinline__ uint32_t u16_max(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
@@ -166,12 +184,12 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int wpb = blockDim.x >> 6;
-  const int64_t nw = (int64_t)gridDim.x * wpb;
+  const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
   const int bias8 = P.bias8, entry8 = P.entry8, exit8 = P.exit8;
   const uint32_t bias2 = splat16(bias8 << 8);
   const int ovf_line = 255 - bias8;
-  for (int64_t t = (int64_t)blockIdx.x * wpb + uni(threadIdx.x >> 6); t < db.n; t += nw) {
+  const int n = (int)db.n;
+  for (int t = wave_id(); t < n; t += nw) {
     const int L = uni(db.len[t]);
     const LenParams lp = db.lp[L];
     const int mv = lp.move8;
@@ -232,15 +250,13 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     }
     const bool pass = ovf || raw >= lp.thr8;
     const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
-    if (lane == 0) {
-      const int64_t c = db.perm[t];
-      db.flags_sorted[t] = fl;
-      out.flags[c] = fl;
-      out.msv[c] = (int16_t)raw;
-      out.vit[c] = INT32_MIN;
-      out.fwd[c] = __builtin_nanf("");
-      if (pass) db.list_vit[atomicAdd(&db.counters[CNT_VIT], 1)] = (int32_t)t;
-    }
+    const int c = uni(db.perm[t]);
+    db.flags_sorted[t] = fl;
+    out.flags[c] = fl;
+    out.msv[c] = (int16_t)raw;
+    out.vit[c] = INT32_MIN;
+    out.fwd[c] = __builtin_nanf("");
+    if (pass) db.list_vit[wave_fetch_add(&db.counters[CNT_VIT], 1)] = t;
   }
 }
 
@@ -382,25 +398,21 @@ __global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevO
     for (int q = 0; q < Q; q++) tr[k][q] = P.vit_tr[(k * Q + q) * kWave + lane];
   const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
   for (;;) {
-    int idx = 0;
-    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_VIT], 1);
-    idx = __shfl(idx, 0);
-    idx = uni(idx);
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_VIT], 1);
     if (idx >= count) break;
     const int t = uni(db.list_vit[idx]);
     const int L = uni(db.len[t]);
     const LenParams lp = db.lp[L];
     const VitResult r = vit16_target<Q, EMIT_LDS>(emit, tr, P, db.res + db.start[t], L, lp, lane);
     const bool pass = r.ovf || r.raw >= lp.thr16;
-    if (lane == 0) {
-      const uint8_t fl = db.flags_sorted[t] | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0);
-      const int64_t c = db.perm[t];
-      db.flags_sorted[t] = fl;
-      out.flags[c] = fl;
-      out.vit[c] = r.raw;
-      if (r.ovf) db.list_ovf[atomicAdd(&db.counters[CNT_OVF], 1)] = t;
-      if (pass) db.list_fwd[atomicAdd(&db.counters[CNT_FWD], 1)] = t;
-    }
+    const uint8_t fl =
+        (uint8_t)(uni(db.flags_sorted[t]) | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0));
+    const int c = uni(db.perm[t]);
+    db.flags_sorted[t] = fl;
+    out.flags[c] = fl;
+    out.vit[c] = r.raw;
+    if (r.ovf) db.list_ovf[wave_fetch_add(&db.counters[CNT_OVF], 1)] = t;
+    if (pass) db.list_fwd[wave_fetch_add(&db.counters[CNT_FWD], 1)] = t;
   }
 }
 
@@ -418,9 +430,7 @@ __global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevO
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   const int *trp = P.v32_tr + lane;
   for (;;) {
-    int idx = 0;
-    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_OVF], 1);
-    idx = uni(__shfl(idx, 0));
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
     if (idx >= count) break;
     const int t = uni(db.list_ovf[idx]);
     const int L = uni(db.len[t]);
@@ -497,7 +507,7 @@ __global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevO
     const int m = wave_max_i32(accM);
     const int xJ = fl32(m + ej);
     const int v = fl32(xJ + mv);
-    if (lane == 0) out.vit[db.perm[t]] = v;
+    out.vit[uni(db.perm[t])] = v;
   }
 }
 
@@ -533,9 +543,7 @@ __global__ void __launch_bounds__(256) fwd_kernel(DevProfile P, DevDb db, DevOut
   const float slotP = cum[Q - 1];
   const float entry_p = P.entry_p;
   for (;;) {
-    int idx = 0;
-    if (lane == 0) idx = atomicAdd(&db.counters[CNT_WORK_FWD], 1);
-    idx = uni(__shfl(idx, 0));
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_FWD], 1);
     if (idx >= count) break;
     const int t = uni(db.list_fwd[idx]);
     const int L = uni(db.len[t]);
@@ -614,13 +622,11 @@ __global__ void __launch_bounds__(256) fwd_kernel(DevProfile P, DevDb db, DevOut
     }
     const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
     const bool pass = f > lp.fthr;
-    if (lane == 0) {
-      const uint8_t fl = db.flags_sorted[t] | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0);
-      const int64_t c = db.perm[t];
-      out.fwd[c] = f;
-      out.flags[c] = fl;
-      if (pass) atomicAdd(&db.counters[CNT_FWD_PASS], 1);
-    }
+    const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
+    const int c = uni(db.perm[t]);
+    out.fwd[c] = f;
+    out.flags[c] = fl;
+    if (pass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
   }
 }
 
