@@ -78,6 +78,8 @@ def main():
     ap.add_argument("--workload", default="C3", choices=["C1", "C2", "C3", "C5"])
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib", default=None,
+                    help="mu_msv,mu_vit,tau to use instead of calibrating on the GPU (profiling runs)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "msv_traffic_C3.json"),
                     help="HBM traffic per MSV launch measured by rocprofv3 counters (JSON), if present")
     args = ap.parse_args()
@@ -101,9 +103,12 @@ def main():
     log(f"generated {w.name}: M={prof.M}, {db.n} targets, {db.residues.size} residues "
         f"in {time.perf_counter() - t:.1f}s")
     t = time.perf_counter()
-    calib = calibrate(prof)
-    log(f"calibrated on the GPU: mu_msv={calib[0]:.4f} mu_vit={calib[1]:.4f} tau={calib[2]:.4f} "
-        f"({time.perf_counter() - t:.1f}s)")
+    if args.calib:
+        calib = tuple(float(v) for v in args.calib.split(","))
+    else:
+        calib = calibrate(prof)
+    log(f"calibration mu_msv={calib[0]!r} mu_vit={calib[1]!r} tau={calib[2]!r} "
+        f"({'given' if args.calib else 'on the GPU'}, {time.perf_counter() - t:.1f}s)")
     P = hg.Profile(prof, *calib)
     t = time.perf_counter()
     D = hg.Database(db.residues, db.offsets)
