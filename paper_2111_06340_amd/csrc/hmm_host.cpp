@@ -244,7 +244,16 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   // ---- device layouts
   const int Q8 = instantiated_q8(q8_of(M));
   const int Q32 = instantiated_q32(q32_of(M));
-  const size_t n_msv = (size_t)kAlpha * Q8 * kWave;            // dwords
+  // MSV: with BIAS8 <= 127 every effective score BIAS8 - COST8 lies in
+  // [-127, 127] and the kernel adds it with one signed saturating op; the
+  // layout then needs one extra (leading) cell.
+  const bool msv_signed = p->bias8 <= 127 && q8_of(M + 1) <= kMaxQ8;
+  const int Qm = msv_signed ? instantiated_q8(q8_of(M + 1)) : Q8;
+  if (Q8 < 0 || Q32 < 0 || Qm < 0) {
+    delete p;
+    return fail(HMM_ERANGE, "M = %d has no kernel instance", M);
+  }
+  const size_t n_msv = (size_t)kAlpha * Qm * kWave;            // dwords
   const size_t n_vemit = (size_t)kAlpha * 2 * Q8 * kWave;
   const size_t n_vtr = (size_t)TR_N * Q8 * kWave;
   const size_t n_w32emit = (size_t)kAlpha * 2 * Q32 * kWave;
@@ -296,13 +305,22 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   auto isc_cell = [&](int c, int a) -> int { return c + 1 < M ? p->isc16[(size_t)c * kAlpha + a] : kNone; };
   auto lo16 = [](int v) { return v == INT32_MIN ? kNeg16 : v; };
 
+  auto msv_entry = [&](int pos, int a) -> int {
+    if (msv_signed) {  // position 0 and positions past M are padding: score -128
+      const int c = pos - 1;
+      return (c >= 0 && c < M ? p->bias8 - p->cost8[(size_t)c * kAlpha + a] : -128) * 256;
+    }
+    return (pos < M ? p->cost8[(size_t)pos * kAlpha + a] : 255) << 8;
+  };
+  for (int a = 0; a < kAlpha; a++)
+    for (int q = 0; q < Qm; q++)
+      for (int l = 0; l < kWave; l++)
+        h_msv[(size_t)a * Qm * kWave + pk_index(q, l)] =
+            pack16(msv_entry(pk_cell(Qm, q, l, 0), a), msv_entry(pk_cell(Qm, q, l, 1), a));
   for (int a = 0; a < kAlpha; a++)
     for (int q = 0; q < Q8; q++)
       for (int l = 0; l < kWave; l++) {
         int c0 = pk_cell(Q8, q, l, 0), c1 = pk_cell(Q8, q, l, 1);
-        int v0 = c0 < M ? p->cost8[(size_t)c0 * kAlpha + a] : 255;
-        int v1 = c1 < M ? p->cost8[(size_t)c1 * kAlpha + a] : 255;
-        h_msv[(size_t)a * Q8 * kWave + pk_index(q, l)] = (uint32_t)(v0 << 8) | ((uint32_t)(v1 << 8) << 16);
         h_vemit[((size_t)a * 2 + 0) * Q8 * kWave + pk_index(q, l)] =
             pack16(lo16(msc_cell(c0, a)), lo16(msc_cell(c1, a)));
         h_vemit[((size_t)a * 2 + 1) * Q8 * kWave + pk_index(q, l)] =
@@ -359,6 +377,8 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   dv.M = M;
   dv.Q8 = Q8;
   dv.Q32 = Q32;
+  dv.Qm = Qm;
+  dv.msv_signed = msv_signed ? 1 : 0;
   dv.bias8 = p->bias8;
   dv.entry8 = p->entry8;
   dv.exit8 = p->exit8;

@@ -38,10 +38,16 @@ struct LenParams {
 // Device-side profile, passed to kernels by value.
 struct DevProfile {
   int32_t M, Q8, Q32;
+  int32_t Qm;                   // vectors per lane of the MSV table
+  int32_t msv_signed;           // MSV table layout, see msv below
   int32_t bias8, entry8, exit8;
   int32_t entry16, ej16;
   float entry_p;                // 2/(M(M+1))
-  const uint32_t *msv;          // [20][Q8][64] packed u16: cost << 8 (high byte)
+  // MSV table [20][Qm][64], packed 16-bit.  msv_signed = 1 (BIAS8 <= 127):
+  // signed scores (BIAS8 - COST8) << 8 with one leading padding cell (cell
+  // k of the profile sits at position k+1); msv_signed = 0: costs COST8 << 8
+  // (high byte), cell k at position k.
+  const uint32_t *msv;
   const uint32_t *vit_emit;     // [20][2][Q8][64] packed i16: msc plane, isc plane
   const uint32_t *vit_tr;       // [TR_N][Q8][64] packed i16
   const int32_t *v32_emit;      // [20][2][Q32][64]

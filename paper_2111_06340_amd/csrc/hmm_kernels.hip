@@ -115,25 +115,6 @@ __device__ __forceinline__ float dpp_f(float v, float fill) {
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
 constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
 
-// Inclusive prefix scan across the wave of affine maps x -> a + p*x
-// (composition order: lane l applies after lanes < l).
-__device__ __forceinline__ void scan_affine(float &a, float &p) {
-#define HMM_AFFINE_STEP(CTRL, MASK)                  \
-  {                                                  \
-    float ap = dpp_f<CTRL, MASK>(a, 0.0f);           \
-    float pp = dpp_f<CTRL, MASK>(p, 1.0f);           \
-    a = fmaf(p, ap, a);                              \
-    p = p * pp;                                      \
-  }
-  HMM_AFFINE_STEP(kRowShr1, 0xf)
-  HMM_AFFINE_STEP(kRowShr2, 0xf)
-  HMM_AFFINE_STEP(kRowShr4, 0xf)
-  HMM_AFFINE_STEP(kRowShr8, 0xf)
-  HMM_AFFINE_STEP(kRowBcast15, 0xa)
-  HMM_AFFINE_STEP(kRowBcast31, 0xc)
-#undef HMM_AFFINE_STEP
-}
-
 // Sum across the wave (result uniform).
 __device__ __forceinline__ float wave_sum_f(float v) {
   v += dpp_f<kRowShr1, 0xf>(v, 0.0f);
@@ -145,23 +126,55 @@ __device__ __forceinline__ float wave_sum_f(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
-// Residue stream of one target: lane j holds dword j of the current 256-byte
-// chunk; the next chunk is prefetched.  Reads may run up to 768 bytes past
-// the target, which the packed database allocation covers.
-struct ResidueStream {
-  const uint32_t *p;
-  uint32_t cur, nxt;
-  __device__ __forceinline__ void init(const uint8_t *x, int lane) {
-    p = (const uint32_t *)x;
-    cur = __builtin_nontemporal_load(p + lane);
-    nxt = __builtin_nontemporal_load(p + 64 + lane);
-  }
-  __device__ __forceinline__ void advance(int chunk, int lane) {
+// Row driver.  The residues of one target arrive 256 at a time: lane j of
+// `cur` holds dword j of the current 256-byte chunk, `nxt` the next chunk
+// (loaded a chunk ahead).  Rows are processed four per dword with two table
+// buffers in alternation: while row r is computed from one buffer, the
+// table entries of row r+1 are read into the other, so memory latency is
+// hidden behind a whole row of arithmetic and no buffer copy is needed.
+//   load(buf, a): read the table entries of residue a into buf
+//   row(buf):     compute one row from buf; return true to stop early
+// Reads run at most 1 KB past a target, inside the database's zero-filled
+// tail, so prefetched residue codes are always valid (and clamped anyway).
+// Returns true if a row stopped the target early.
+template <typename Buf, typename Load, typename Row>
+__device__ __forceinline__ bool drive_rows(const uint8_t *x, int L, int lane, Buf &ba, Buf &bb, Load load, Row row) {
+  const uint32_t *p = (const uint32_t *)x;
+  uint32_t cur = __builtin_nontemporal_load(p + lane);
+  uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
+  auto code = [](uint32_t w, int r) { return min((int)((w >> (8 * r)) & 0xffu), kAlpha - 1); };
+  uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, 0);
+  load(ba, code(w, 0));
+  for (int c0 = 0; c0 < L; c0 += 256) {
+    const int nwords = min(kWave, (L - c0 + 3) >> 2);
+    for (int j = 0; j < nwords; j++) {
+      uint32_t wn;
+      if (j == kWave - 1)
+        wn = (uint32_t)__builtin_amdgcn_readlane((int)nxt, 0);
+      else
+        wn = (uint32_t)__builtin_amdgcn_readlane((int)cur, j + 1);
+      const int left = L - c0 - 4 * j;
+      load(bb, code(w, 1));
+      if (row(ba)) return true;
+      if (left <= 1) return false;
+      load(ba, code(w, 2));
+      if (row(bb)) return true;
+      if (left <= 2) return false;
+      load(bb, code(w, 3));
+      if (row(ba)) return true;
+      if (left <= 3) return false;
+      load(ba, code(wn, 0));
+      if (row(bb)) return true;
+      w = wn;
+    }
     cur = nxt;
-    nxt = __builtin_nontemporal_load(p + (size_t)(chunk + 2) * 64 + lane);
+    nxt = __builtin_nontemporal_load(p + (size_t)((c0 >> 8) + 2) * kWave + lane);
   }
-  __device__ __forceinline__ uint32_t word(int j) const { return (uint32_t)__builtin_amdgcn_readlane((int)cur, j); }
-};
+  return false;
+}
+
+__device__ __forceinline__ int sat16(int v) { return max(-32768, min(32767, v)); }
+__device__ __forceinline__ int hmax16(uint32_t v) { return max((int)(int16_t)(v >> 16), (int)(int16_t)(v & 0xffffu)); }
 
 // ============================================================================ MSV
 //
@@ -172,9 +185,23 @@ struct ResidueStream {
 // xB only depends on max(xJ, BASE8): a running per-lane maximum of all cells
 // is compared each row against the smallest value that could change xB or
 // overflow; only then is the wave-wide maximum taken.  The final xJ is the
-// running maximum (-) EXIT8.
+// running maximum (-) EXIT8.  The cost row of the next residue is read from
+// LDS while the current row is computed.
 
-template <int Q>
+// Two encodings of the uint8 values in 16-bit lanes:
+//  SIGNED = false: v in the high byte of an unsigned lane; (v (+) BIAS8)
+//    (-) COST8 is one saturating unsigned add and one saturating subtract.
+//  SIGNED = true (BIAS8 <= 127): X = 256 v - 32768 in a signed lane (the low
+//    byte is don't-care).  The two steps fold into one signed saturating add
+//    of 256 (BIAS8 - COST8): the floor at v = 0 is the int16 floor, and the
+//    255 ceiling of the biased add never binds, because a row is only
+//    computed while every cell stays below the overflow line 255 - BIAS8
+//    (the trigger is never above it), so v + BIAS8 < 255.  Cell k sits at
+//    position k+1: position 0 is padding with score -128, so the zero that
+//    the lane shift feeds in (which encodes v = 128) becomes
+//    max(0, xBe - 128) <= xBe there, and cell 0 sees xBe as required.
+//    Padding never exceeds the row's maximum, so xE is unaffected.
+template <int Q, bool SIGNED>
 __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ uint32_t lds[];
   {
@@ -188,6 +215,12 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   const int bias8 = P.bias8, entry8 = P.entry8, exit8 = P.exit8;
   const uint32_t bias2 = splat16(bias8 << 8);
   const int ovf_line = 255 - bias8;
+  // encoding of a uint8 value v and decoding of a lane maximum
+  auto enc = [](int v) { return SIGNED ? v * 256 - 32768 : v << 8; };
+  auto dec_max = [](uint32_t a) -> int {
+    return SIGNED ? (hmax16(a) + 32768) >> 8 : (int)(max(a & 0xffffu, a >> 16) >> 8);
+  };
+  const uint32_t *tab = lds + lane;
   const int n = (int)db.n;
   for (int t = wave_id(); t < n; t += nw) {
     const int L = uni(db.len[t]);
@@ -196,55 +229,57 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     const int base = max(kBase8 - mv, 0);
     int xJt = 0;
     bool ovf = ovf_line <= 0;
-    uint32_t acc = 0;
+    uint32_t acc = splat16(enc(0));
     if (!ovf) {
       uint32_t mm[Q];
 #pragma unroll
-      for (int q = 0; q < Q; q++) mm[q] = 0;
+      for (int q = 0; q < Q; q++) mm[q] = splat16(enc(0));
       int T = min(ovf_line, kBase8 + 4);
-      uint32_t thr2 = splat16((T << 8) - 1);
-      uint32_t xbe2 = splat16(max(base - entry8, 0) << 8);
-      ResidueStream rs;
-      rs.init(db.res + db.start[t], lane);
-      const uint32_t *tab = lds + lane;
-      for (int c0 = 0; c0 < L; c0 += 256) {
-        const int nwords = min(64, (L - c0 + 3) >> 2);
-        for (int j = 0; j < nwords; j++) {
-          const uint32_t w = rs.word(j);
-          const int nr = min(4, L - c0 - 4 * j);
-          for (int r = 0; r < nr; r++) {
-            const int a = (w >> (8 * r)) & 0xff;
-            const uint32_t *row = tab + a * (Q * kWave);
-            const uint32_t sh = slot_up16(mm[Q - 1]);
+      uint32_t thr2 = splat16(enc(T) - 1);
+      uint32_t xbe2 = splat16(enc(max(base - entry8, 0)));
+      // The trigger value and xBe stay fixed (scalars) until some cell
+      // reaches the trigger; then xJ and xB are updated, or the target stops
+      // on overflow.
+      auto load = [&](uint32_t(&c)[Q], int a) {
+        const uint32_t *row = tab + a * (Q * kWave);
 #pragma unroll
-            for (int q = Q - 1; q >= 0; q--) {
-              uint32_t v = u16_max(q ? mm[q - 1] : sh, xbe2);
-              v = u16_adds(v, bias2);
-              v = u16_subs(v, row[q * kWave]);
-              acc = u16_max(acc, v);
-              mm[q] = v;
-            }
-            if (any_lane(u16_subs(acc, thr2) != 0u)) {
-              const int m = wave_max_i32((int)(max(acc & 0xffffu, acc >> 16) >> 8));
-              if (m >= ovf_line) {
-                ovf = true;
-                goto msv_done;
-              }
-              xJt = max(xJt, max(m - exit8, 0));
-              const int xB = max(base, max(xJt - mv, 0));
-              xbe2 = splat16(max(xB - entry8, 0) << 8);
-              T = min(ovf_line, max(xJt, kBase8) + 4);
-              thr2 = splat16((T << 8) - 1);
-            }
+        for (int q = 0; q < Q; q++) c[q] = row[q * kWave];
+      };
+      auto row = [&](const uint32_t(&c)[Q]) -> bool {
+        const uint32_t sh = slot_up16(mm[Q - 1]);
+#pragma unroll
+        for (int q = Q - 1; q >= 0; q--) {
+          uint32_t v;
+          if (SIGNED) {
+            v = i16_max(q ? mm[q - 1] : sh, xbe2);
+            v = i16_adds(v, c[q]);
+            acc = i16_max(acc, v);
+          } else {
+            v = u16_max(q ? mm[q - 1] : sh, xbe2);
+            v = u16_adds(v, bias2);
+            v = u16_subs(v, c[q]);
+            acc = u16_max(acc, v);
           }
+          mm[q] = v;
         }
-        rs.advance(c0 >> 8, lane);
-      }
+        const bool trig = SIGNED ? any_lane(i16_max(acc, thr2) != thr2) : any_lane(u16_subs(acc, thr2) != 0u);
+        if (trig) {
+          const int m = wave_max_i32(dec_max(acc));
+          if (m >= ovf_line) return true;
+          xJt = max(xJt, max(m - exit8, 0));
+          const int xB = max(base, max(xJt - mv, 0));
+          xbe2 = splat16(enc(max(xB - entry8, 0)));
+          T = min(ovf_line, max(xJt, kBase8) + 4);
+          thr2 = splat16(enc(T) - 1);
+        }
+        return false;
+      };
+      uint32_t ca[Q], cb[Q];
+      ovf = drive_rows(db.res + db.start[t], L, lane, ca, cb, load, row);
     }
-  msv_done:
     int raw = 255;
     if (!ovf) {
-      const int m = wave_max_i32((int)(max(acc & 0xffffu, acc >> 16) >> 8));
+      const int m = wave_max_i32(dec_max(acc));
       const int xJ = max(m - exit8, 0);
       raw = max(xJ - mv, 0);
     }
@@ -273,13 +308,13 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
 // would raise it.  The delete chain is computed inside each slot, then
 // propagated across slots until no lane changes (exact: sat is monotone).
 
-// Result of one Viterbi target.
 struct VitResult {
   int raw;
   bool ovf;
 };
 
-template <int Q, bool EMIT_LDS>
+
+template <int Q>
 __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ emit, const uint32_t (&tr)[TR_N][Q],
                                                   const DevProfile &P, const uint8_t *x, int L,
                                                   const LenParams &lp, int lane) {
@@ -288,94 +323,76 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
   for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNegNeg;
   uint32_t accM = kNegNeg, accI = kNegNeg;
   const int mv = lp.move16, ej = P.ej16, entry = P.entry16;
-  auto sat = [](int v) { return max(-32768, min(32767, v)); };
   int xJt = kNeg16;
-  int xB = sat(mv);
-  uint32_t xbe2 = splat16(sat(xB + entry));
+  int xB = sat16(mv);
+  uint32_t xbe2 = splat16(sat16(xB + entry));
   int T = min(-ej + 1, 32767);
   uint32_t tm1 = splat16(T - 1);
   bool ovf = false;
-  ResidueStream rs;
-  rs.init(x, lane);
-  for (int c0 = 0; c0 < L; c0 += 256) {
-    const int nwords = min(64, (L - c0 + 3) >> 2);
-    for (int j = 0; j < nwords; j++) {
-      const uint32_t w = rs.word(j);
-      const int nr = min(4, L - c0 - 4 * j);
-      for (int r = 0; r < nr; r++) {
-        const int a = (w >> (8 * r)) & 0xff;
-        const uint32_t *er = emit + a * (2 * Q * kWave) + lane;
-        const uint32_t msh = slot_up16(M[Q - 1]);
-        const uint32_t ish = slot_up16(I[Q - 1]);
-        const uint32_t dsh = slot_up16(D[Q - 1]);
+  auto load = [&](uint32_t(&e)[2 * Q], int a) {
+    const uint32_t *er = emit + a * (2 * Q * kWave);
 #pragma unroll
-        for (int q = Q - 1; q >= 0; q--) {
-          const uint32_t pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-          uint32_t m = i16_max(xbe2, i16_adds(pm, tr[TR_MMIN][q]));
-          m = i16_max(m, i16_adds(pi, tr[TR_IMIN][q]));
-          m = i16_max(m, i16_adds(pd, tr[TR_DMIN][q]));
-          const uint32_t mn = i16_adds(m, er[q * kWave]);
-          const uint32_t in =
-              i16_adds(i16_max(i16_adds(M[q], tr[TR_MI][q]), i16_adds(I[q], tr[TR_II][q])), er[(Q + q) * kWave]);
-          accM = i16_max(accM, mn);
-          accI = i16_max(accI, in);
-          M[q] = mn;
-          I[q] = in;
-        }
-        {
-          uint32_t dc = kNegNeg;
-          const uint32_t din = slot_up16(M[Q - 1]);
+    for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+  };
+  auto row = [&](const uint32_t(&em)[2 * Q]) -> bool {
+    const uint32_t msh = slot_up16(M[Q - 1]);
+    const uint32_t ish = slot_up16(I[Q - 1]);
+    const uint32_t dsh = slot_up16(D[Q - 1]);
 #pragma unroll
-          for (int q = 0; q < Q; q++) {
-            D[q] = i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q]));
-            dc = D[q];
-          }
-          for (int it = 0; it < 2 * kWave; it++) {
-            dc = slot_up16(D[Q - 1]);
-            bool moved = true;
+    for (int q = Q - 1; q >= 0; q--) {
+      const uint32_t pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+      uint32_t m = i16_max(xbe2, i16_adds(pm, tr[TR_MMIN][q]));
+      m = i16_max(m, i16_adds(pi, tr[TR_IMIN][q]));
+      m = i16_max(m, i16_adds(pd, tr[TR_DMIN][q]));
+      const uint32_t mn = i16_adds(m, em[q]);
+      const uint32_t in = i16_adds(i16_max(i16_adds(M[q], tr[TR_MI][q]), i16_adds(I[q], tr[TR_II][q])), em[Q + q]);
+      accM = i16_max(accM, mn);
+      accI = i16_max(accI, in);
+      M[q] = mn;
+      I[q] = in;
+    }
+    uint32_t dc = kNegNeg;
+    const uint32_t din = slot_up16(M[Q - 1]);
 #pragma unroll
-            for (int q = 0; q < Q; q++) {
-              if (moved) {
-                const uint32_t nd = i16_max(D[q], i16_adds(dc, tr[TR_DDIN][q]));
-                moved = any_lane(nd != D[q]);
-                D[q] = nd;
-                dc = nd;
-              }
-            }
-            if (!moved) break;
-          }
-        }
-        if (any_lane(i16_max(accM, tm1) != tm1)) {
-          const int hi = (int)(int16_t)(accM >> 16), lo = (int)(int16_t)(accM & 0xffffu);
-          const int m = wave_max_i32(max(hi, lo));
-          if (m >= 32767) {
-            ovf = true;
-            goto vit_done;
-          }
-          xJt = max(xJt, sat(m + ej));
-          xB = max(sat(mv), sat(xJt + mv));
-          xbe2 = splat16(sat(xB + entry));
-          T = min(max(xJt, 0) - ej + 1, 32767);
-          tm1 = splat16(T - 1);
+    for (int q = 0; q < Q; q++) {
+      D[q] = i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q]));
+      dc = D[q];
+    }
+    for (int it = 0; it < 2 * kWave; it++) {
+      dc = slot_up16(D[Q - 1]);
+      bool moved = true;
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        if (moved) {
+          const uint32_t nd = i16_max(D[q], i16_adds(dc, tr[TR_DDIN][q]));
+          moved = any_lane(nd != D[q]);
+          D[q] = nd;
+          dc = nd;
         }
       }
+      if (!moved) break;
     }
-    rs.advance(c0 >> 8, lane);
-  }
-vit_done:
-  if (!ovf) {
-    const int hi = (int)(int16_t)(accI >> 16), lo = (int)(int16_t)(accI & 0xffffu);
-    ovf = any_lane(max(hi, lo) >= 32767);
-  }
+    if (any_lane(i16_max(accM, tm1) != tm1)) {
+      const int m = wave_max_i32(hmax16(accM));
+      if (m >= 32767) return true;
+      xJt = max(xJt, sat16(m + ej));
+      xB = max(sat16(mv), sat16(xJt + mv));
+      xbe2 = splat16(sat16(xB + entry));
+      T = min(max(xJt, 0) - ej + 1, 32767);
+      tm1 = splat16(T - 1);
+    }
+    return false;
+  };
+  uint32_t ea[2 * Q], eb[2 * Q];
+  ovf = drive_rows(x, L, lane, ea, eb, load, row);
+  if (!ovf) ovf = any_lane(hmax16(accI) >= 32767);
   VitResult res;
   res.ovf = ovf;
   if (ovf) {
     res.raw = 32767;
   } else {
-    const int hi = (int)(int16_t)(accM >> 16), lo = (int)(int16_t)(accM & 0xffffu);
-    const int m = wave_max_i32(max(hi, lo));
-    const int xJ = sat(m + ej);
-    res.raw = sat(xJ + mv);
+    const int m = wave_max_i32(hmax16(accM));
+    res.raw = sat16(sat16(m + ej) + mv);
   }
   return res;
 }
@@ -390,7 +407,7 @@ __global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevO
     for (int i = threadIdx.x; i < kAlpha * 2 * Q * kWave / 4; i += blockDim.x) dst[i] = src[i];
     __syncthreads();
   }
-  const uint32_t *emit = EMIT_LDS ? (const uint32_t *)lds : P.vit_emit;
+  const uint32_t *emit = (EMIT_LDS ? (const uint32_t *)lds : P.vit_emit) + lane;
   uint32_t tr[TR_N][Q];
 #pragma unroll
   for (int k = 0; k < TR_N; k++)
@@ -403,7 +420,7 @@ __global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevO
     const int t = uni(db.list_vit[idx]);
     const int L = uni(db.len[t]);
     const LenParams lp = db.lp[L];
-    const VitResult r = vit16_target<Q, EMIT_LDS>(emit, tr, P, db.res + db.start[t], L, lp, lane);
+    const VitResult r = vit16_target<Q>(emit, tr, P, db.res + db.start[t], L, lp, lane);
     const bool pass = r.ovf || r.raw >= lp.thr16;
     const uint8_t fl =
         (uint8_t)(uni(db.flags_sorted[t]) | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0));
@@ -419,16 +436,37 @@ __global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevO
 // ============================================================================ Viterbi int32 rescore
 //
 // The int16 recurrence in int32 with every add floored at -2^30 and no upper
-// clamp; run on the targets that overflowed int16.  Tables are read through
-// the caches (few targets).
+// clamp; run on the targets that overflowed int16.  Emission rows come from
+// LDS when the table fits (else global memory), prefetched a row ahead;
+// transitions stay in registers up to 16 vectors per lane, else in LDS.
 
 __device__ __forceinline__ int fl32(int v) { return max(v, kNeg32); }
 
-template <int Q>
-__global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
+template <int Q, bool EMIT_LDS, bool TR_LDS>
+__global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
+  extern __shared__ int32_t lds32[];
   const int lane = threadIdx.x & 63;
+  constexpr int kEmit = kAlpha * 2 * Q * kWave;   // dwords
+  constexpr int kTr = TR_N * Q * kWave;
+  if (EMIT_LDS || TR_LDS) {
+    if (EMIT_LDS)
+      for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_emit)[i];
+    if (TR_LDS)
+      for (int i = threadIdx.x; i < kTr / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_tr)[i];
+    __syncthreads();
+  }
+  const int *emit = (EMIT_LDS ? (const int *)lds32 : P.v32_emit) + lane;
+  const int *trp = (TR_LDS ? (const int *)lds32 : P.v32_tr) + lane;
+  constexpr int kTrRegs = TR_LDS ? 1 : Q;
+  int tr[TR_N][kTrRegs];
+  if (!TR_LDS) {
+#pragma unroll
+    for (int k = 0; k < TR_N; k++)
+#pragma unroll
+      for (int q = 0; q < kTrRegs; q++) tr[k][q] = trp[(k * Q + q) * kWave];
+  }
+  auto TR = [&](int k, int q) -> int { return TR_LDS ? trp[(k * Q + q) * kWave] : tr[k][TR_LDS ? 0 : q]; };
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
-  const int *trp = P.v32_tr + lane;
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
     if (idx >= count) break;
@@ -444,69 +482,61 @@ __global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevO
     int xB = fl32(mv);
     int xbe = fl32(xB + entry);
     int T = -ej + 1;
-    ResidueStream rs;
-    rs.init(db.res + db.start[t], lane);
-    for (int c0 = 0; c0 < L; c0 += 256) {
-      const int nwords = min(64, (L - c0 + 3) >> 2);
-      for (int j = 0; j < nwords; j++) {
-        const uint32_t w = rs.word(j);
-        const int nr = min(4, L - c0 - 4 * j);
-        for (int r = 0; r < nr; r++) {
-          const int a = (w >> (8 * r)) & 0xff;
-          const int *er = P.v32_emit + a * (2 * Q * kWave) + lane;
-          const int msh = lane_up_i(M[Q - 1]);
-          const int ish = lane_up_i(I[Q - 1]);
-          const int dsh = lane_up_i(D[Q - 1]);
+    auto load = [&](int(&e)[2 * Q], int a) {
+      const int *er = emit + a * (2 * Q * kWave);
 #pragma unroll
-          for (int q = Q - 1; q >= 0; q--) {
-            const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-            int m = max(xbe, fl32(pm + trp[(TR_MMIN * Q + q) * kWave]));
-            m = max(m, fl32(pi + trp[(TR_IMIN * Q + q) * kWave]));
-            m = max(m, fl32(pd + trp[(TR_DMIN * Q + q) * kWave]));
-            const int mn = fl32(m + er[q * kWave]);
-            const int in = fl32(max(fl32(M[q] + trp[(TR_MI * Q + q) * kWave]),
-                                    fl32(I[q] + trp[(TR_II * Q + q) * kWave])) +
-                                er[(Q + q) * kWave]);
-            accM = max(accM, mn);
-            M[q] = mn;
-            I[q] = in;
-          }
-          int dc = kNeg32;
-          const int din = lane_up_i(M[Q - 1]);
+      for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+    };
+    auto row = [&](const int(&em)[2 * Q]) -> bool {
+      const int msh = lane_up_i(M[Q - 1]);
+      const int ish = lane_up_i(I[Q - 1]);
+      const int dsh = lane_up_i(D[Q - 1]);
 #pragma unroll
-          for (int q = 0; q < Q; q++) {
-            D[q] = max(fl32((q ? M[q - 1] : din) + trp[(TR_MDIN * Q + q) * kWave]),
-                       fl32(dc + trp[(TR_DDIN * Q + q) * kWave]));
-            dc = D[q];
-          }
-          for (int it = 0; it < kWave; it++) {
-            dc = lane_up_i(D[Q - 1]);
-            bool moved = true;
+      for (int q = Q - 1; q >= 0; q--) {
+        const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+        int m = max(xbe, fl32(pm + TR(TR_MMIN, q)));
+        m = max(m, fl32(pi + TR(TR_IMIN, q)));
+        m = max(m, fl32(pd + TR(TR_DMIN, q)));
+        const int mn = fl32(m + em[q]);
+        const int in = fl32(max(fl32(M[q] + TR(TR_MI, q)), fl32(I[q] + TR(TR_II, q))) + em[Q + q]);
+        accM = max(accM, mn);
+        M[q] = mn;
+        I[q] = in;
+      }
+      int dc = kNeg32;
+      const int din = lane_up_i(M[Q - 1]);
 #pragma unroll
-            for (int q = 0; q < Q; q++) {
-              if (moved) {
-                const int nd = max(D[q], fl32(dc + trp[(TR_DDIN * Q + q) * kWave]));
-                moved = any_lane(nd != D[q]);
-                D[q] = nd;
-                dc = nd;
-              }
-            }
-            if (!moved) break;
-          }
-          if (any_lane(accM >= T)) {
-            const int m = wave_max_i32(accM);
-            xJt = max(xJt, fl32(m + ej));
-            xB = max(fl32(mv), fl32(xJt + mv));
-            xbe = fl32(xB + entry);
-            T = max(xJt, 0) - ej + 1;
+      for (int q = 0; q < Q; q++) {
+        D[q] = max(fl32((q ? M[q - 1] : din) + TR(TR_MDIN, q)), fl32(dc + TR(TR_DDIN, q)));
+        dc = D[q];
+      }
+      for (int it = 0; it < kWave; it++) {
+        dc = lane_up_i(D[Q - 1]);
+        bool moved = true;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          if (moved) {
+            const int nd = max(D[q], fl32(dc + TR(TR_DDIN, q)));
+            moved = any_lane(nd != D[q]);
+            D[q] = nd;
+            dc = nd;
           }
         }
+        if (!moved) break;
       }
-      rs.advance(c0 >> 8, lane);
-    }
+      if (any_lane(accM >= T)) {
+        const int m = wave_max_i32(accM);
+        xJt = max(xJt, fl32(m + ej));
+        xB = max(fl32(mv), fl32(xJt + mv));
+        xbe = fl32(xB + entry);
+        T = max(xJt, 0) - ej + 1;
+      }
+      return false;
+    };
+    int ea[2 * Q], eb[2 * Q];
+    (void)drive_rows(db.res + db.start[t], L, lane, ea, eb, load, row);
     const int m = wave_max_i32(accM);
-    const int xJ = fl32(m + ej);
-    const int v = fl32(xJ + mv);
+    const int v = fl32(fl32(m + ej) + mv);
     out.vit[uni(db.perm[t])] = v;
   }
 }
@@ -519,29 +549,54 @@ __global__ void __launch_bounds__(256) vit32_kernel(DevProfile P, DevDb db, DevO
 //   D_k = M_{k-1} MD + D_{k-1} DD                                            (current row)
 //   E = sum_k (M_k + D_k); J = J loop + E/2; C = C loop + E/2; N = N loop;
 //   B = (N + J) move.
-// Values are rescaled by an exact power of two whenever the largest special
-// value leaves [2^-40, 2^40]; the exponents removed are summed.  Result:
-// ln(C * move) + (sum of exponents) ln 2, in nats.
+// The delete chain runs inside each slot with a zero entry value; the values
+// entering the slots follow from an inclusive scan of the affine maps
+// x -> D_out + P x across lanes (P = product of the slot's DD), whose P part
+// is profile-constant and precomputed.  Values are rescaled by an exact power
+// of two whenever the largest special value leaves [2^-40, 2^40]; the removed
+// exponents are summed.  Result: ln(C move) + (sum of exponents) ln 2, nats.
 
-template <int Q>
-__global__ void __launch_bounds__(256) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
+template <int Q, bool EMIT_LDS, bool TR_LDS>
+__global__ void __launch_bounds__(512) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
+  extern __shared__ float ldsf[];
   const int lane = threadIdx.x & 63;
-  const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
-  const float *trp = P.f_tr + lane;
-  float tMM[Q], tIM[Q], tDM[Q], tMD[Q], tDD[Q], tMI[Q], tII[Q], cum[Q];
-#pragma unroll
-  for (int q = 0; q < Q; q++) {
-    tMM[q] = trp[(TR_MMIN * Q + q) * kWave];
-    tIM[q] = trp[(TR_IMIN * Q + q) * kWave];
-    tDM[q] = trp[(TR_DMIN * Q + q) * kWave];
-    tMD[q] = trp[(TR_MDIN * Q + q) * kWave];
-    tDD[q] = trp[(TR_DDIN * Q + q) * kWave];
-    tMI[q] = trp[(TR_MI * Q + q) * kWave];
-    tII[q] = trp[(TR_II * Q + q) * kWave];
-    cum[q] = trp[(TR_N * Q + q) * kWave];
+  constexpr int kEmit = kAlpha * 2 * Q * kWave;
+  constexpr int kTr = (TR_N + 1) * Q * kWave;
+  if (EMIT_LDS || TR_LDS) {
+    if (EMIT_LDS)
+      for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_emit)[i];
+    if (TR_LDS)
+      for (int i = threadIdx.x; i < kTr / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_tr)[i];
+    __syncthreads();
   }
-  const float slotP = cum[Q - 1];
+  const float *emit = (EMIT_LDS ? (const float *)ldsf : P.f_emit) + lane;
+  const float *trp = (TR_LDS ? (const float *)ldsf : P.f_tr) + lane;
+  constexpr int kR = TR_LDS ? 1 : Q;
+  float tr[TR_N + 1][kR];
+  if (!TR_LDS) {
+#pragma unroll
+    for (int k = 0; k <= TR_N; k++)
+#pragma unroll
+      for (int q = 0; q < kR; q++) tr[k][q] = trp[(k * Q + q) * kWave];
+  }
+  auto TR = [&](int k, int q) -> float { return TR_LDS ? trp[(k * Q + q) * kWave] : tr[k][TR_LDS ? 0 : q]; };
+  // P part of the delete-chain scan: the lane's P before each of the six steps
+  float pstep[6];
+  {
+    float p = P.f_tr[(TR_N * Q + Q - 1) * kWave + lane];
+#define HMM_PSTEP(I, CTRL, MASK)           \
+  pstep[I] = p;                            \
+  p = p * dpp_f<CTRL, MASK>(p, 1.0f);
+    HMM_PSTEP(0, kRowShr1, 0xf)
+    HMM_PSTEP(1, kRowShr2, 0xf)
+    HMM_PSTEP(2, kRowShr4, 0xf)
+    HMM_PSTEP(3, kRowShr8, 0xf)
+    HMM_PSTEP(4, kRowBcast15, 0xa)
+    HMM_PSTEP(5, kRowBcast31, 0xc)
+#undef HMM_PSTEP
+  }
   const float entry_p = P.entry_p;
+  const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_FWD], 1);
     if (idx >= count) break;
@@ -554,72 +609,72 @@ __global__ void __launch_bounds__(256) fwd_kernel(DevProfile P, DevDb db, DevOut
     for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = 0.0f;
     float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
     int shift = 0;
-    ResidueStream rs;
-    rs.init(db.res + db.start[t], lane);
-    for (int c0 = 0; c0 < L; c0 += 256) {
-      const int nwords = min(64, (L - c0 + 3) >> 2);
-      for (int j = 0; j < nwords; j++) {
-        const uint32_t w = rs.word(j);
-        const int nr = min(4, L - c0 - 4 * j);
-        for (int r = 0; r < nr; r++) {
-          const int a = (w >> (8 * r)) & 0xff;
-          const float *er = P.f_emit + a * (2 * Q * kWave) + lane;
-          const float msh = lane_up_f(M[Q - 1]);
-          const float ish = lane_up_f(I[Q - 1]);
-          const float dsh = lane_up_f(D[Q - 1]);
-          const float bent = B * entry_p;
+    auto load = [&](float(&e)[2 * Q], int a) {
+      const float *er = emit + a * (2 * Q * kWave);
 #pragma unroll
-          for (int q = Q - 1; q >= 0; q--) {
-            const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-            const float sm = fmaf(pm, tMM[q], fmaf(pi, tIM[q], fmaf(pd, tDM[q], bent)));
-            const float si = fmaf(M[q], tMI[q], I[q] * tII[q]);
-            M[q] = er[q * kWave] * sm;
-            I[q] = er[(Q + q) * kWave] * si;
-          }
-          // delete chain: within the slot, then across slots by an affine scan
-          const float din = lane_up_f(M[Q - 1]);
-          float dc = 0.0f;
+      for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+    };
+    auto row = [&](const float(&em)[2 * Q]) -> bool {
+      const float msh = lane_up_f(M[Q - 1]);
+      const float ish = lane_up_f(I[Q - 1]);
+      const float dsh = lane_up_f(D[Q - 1]);
+      const float bent = B * entry_p;
 #pragma unroll
-          for (int q = 0; q < Q; q++) {
-            D[q] = fmaf(q ? M[q - 1] : din, tMD[q], dc * tDD[q]);
-            dc = D[q];
-          }
-          float sa = D[Q - 1], sp = slotP;
-          scan_affine(sa, sp);
-          const float carry = lane_up_f(sa);
-          float part = 0.0f;
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            D[q] = fmaf(carry, cum[q], D[q]);
-            part += M[q] + D[q];
-          }
-          const float E = wave_sum_f(part);
-          J = fmaf(J, loop, 0.5f * E);
-          C = fmaf(C, loop, 0.5f * E);
-          N = N * loop;
-          B = (N + J) * move;
-          const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
-          if (big > 0x1p40f || big < 0x1p-40f) {
-            int ex;
-            (void)frexpf(big, &ex);
-            ex = uni(ex);
-            const float s = ldexpf(1.0f, -ex);
-#pragma unroll
-            for (int q = 0; q < Q; q++) {
-              M[q] *= s;
-              I[q] *= s;
-              D[q] *= s;
-            }
-            J *= s;
-            C *= s;
-            N *= s;
-            B *= s;
-            shift += ex;
-          }
-        }
+      for (int q = Q - 1; q >= 0; q--) {
+        const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+        const float sm = fmaf(pm, TR(TR_MMIN, q), fmaf(pi, TR(TR_IMIN, q), fmaf(pd, TR(TR_DMIN, q), bent)));
+        const float si = fmaf(M[q], TR(TR_MI, q), I[q] * TR(TR_II, q));
+        M[q] = em[q] * sm;
+        I[q] = em[Q + q] * si;
       }
-      rs.advance(c0 >> 8, lane);
-    }
+      const float din = lane_up_f(M[Q - 1]);
+      float dc = 0.0f;
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        D[q] = fmaf(q ? M[q - 1] : din, TR(TR_MDIN, q), dc * TR(TR_DDIN, q));
+        dc = D[q];
+      }
+      float sa = D[Q - 1];
+      sa = fmaf(pstep[0], dpp_f<kRowShr1, 0xf>(sa, 0.0f), sa);
+      sa = fmaf(pstep[1], dpp_f<kRowShr2, 0xf>(sa, 0.0f), sa);
+      sa = fmaf(pstep[2], dpp_f<kRowShr4, 0xf>(sa, 0.0f), sa);
+      sa = fmaf(pstep[3], dpp_f<kRowShr8, 0xf>(sa, 0.0f), sa);
+      sa = fmaf(pstep[4], dpp_f<kRowBcast15, 0xa>(sa, 0.0f), sa);
+      sa = fmaf(pstep[5], dpp_f<kRowBcast31, 0xc>(sa, 0.0f), sa);
+      const float carry = lane_up_f(sa);
+      float part = 0.0f;
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        D[q] = fmaf(carry, TR(TR_N, q), D[q]);
+        part += M[q] + D[q];
+      }
+      const float E = wave_sum_f(part);
+      J = fmaf(J, loop, 0.5f * E);
+      C = fmaf(C, loop, 0.5f * E);
+      N = N * loop;
+      B = (N + J) * move;
+      const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
+      if (big > 0x1p40f || big < 0x1p-40f) {
+        int ex;
+        (void)frexpf(big, &ex);
+        ex = uni(ex);
+        const float s = ldexpf(1.0f, -ex);
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          M[q] *= s;
+          I[q] *= s;
+          D[q] *= s;
+        }
+        J *= s;
+        C *= s;
+        N *= s;
+        B *= s;
+        shift += ex;
+      }
+      return false;
+    };
+    float ea[2 * Q], eb[2 * Q];
+    (void)drive_rows(db.res + db.start[t], L, lane, ea, eb, load, row);
     const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
     const bool pass = f > lp.fthr;
     const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
@@ -666,11 +721,11 @@ int blocks_per_cu(K kernel, int threads, size_t lds) {
   return nb;
 }
 
-template <int Q>
+template <int Q, bool SIGNED>
 hipError_t launch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   const int threads = Q >= 12 ? 1024 : 512;
   const size_t lds = (size_t)kAlpha * Q * kWave * 4;
-  auto k = msv_kernel<Q>;
+  auto k = msv_kernel<Q, SIGNED>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -705,30 +760,46 @@ hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, h
   return hipGetLastError();
 }
 
-template <int Q>
-hipError_t launch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  const int threads = 256;
-  auto k = vit32_kernel<Q>;
-  static int bpc = 0;
-  if (!bpc) bpc = blocks_per_cu(k, threads, 0);
+// Persistent launch of a list kernel: as many blocks as fit, at most one
+// wave per database target.
+template <typename K>
+hipError_t launch_list_kernel(K k, int &bpc, size_t lds, const DevProfile &P, const DevDb &db, const DevOut &o,
+                              hipStream_t s) {
+  const int threads = 512;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  if (!bpc) bpc = blocks_per_cu(k, threads, lds);
   int64_t blocks = (int64_t)bpc * num_cu();
   const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
   if (blocks > cap) blocks = cap;
-  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, P, db, o);
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), lds, s, P, db, o);
   return hipGetLastError();
+}
+
+// Tables of the 32-bit kernels: emissions in LDS up to 12 vectors per lane
+// (120 KB), transitions in registers up to 16, else in LDS.
+template <int Q>
+constexpr bool kEmitLds32 = Q <= 12;
+template <int Q>
+constexpr bool kTrLds32 = Q > 16;
+static_assert(!(kEmitLds32<16> && kTrLds32<16>), "the two LDS tables share offset 0");
+
+template <int Q>
+hipError_t launch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
+  const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)TR_N * Q * kWave * 4 : 0);
+  static int bpc = 0;
+  return launch_list_kernel(vit32_kernel<Q, E, T>, bpc, lds, P, db, o, s);
 }
 
 template <int Q>
 hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  const int threads = 256;
-  auto k = fwd_kernel<Q>;
+  constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
+  const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)(TR_N + 1) * Q * kWave * 4 : 0);
   static int bpc = 0;
-  if (!bpc) bpc = blocks_per_cu(k, threads, 0);
-  int64_t blocks = (int64_t)bpc * num_cu();
-  const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
-  if (blocks > cap) blocks = cap;
-  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, s, P, db, o);
-  return hipGetLastError();
+  return launch_list_kernel(fwd_kernel<Q, E, T>, bpc, lds, P, db, o, s);
 }
 
 #define HMM_Q8_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14) X(16) X(20) X(24)
@@ -736,10 +807,10 @@ hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hip
   X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12) X(14) X(16) X(20) X(24) X(28) X(32) X(40) X(48)
 
 hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  switch (P.Q8) {
+  switch (P.Qm) {
 #define HMM_CASE(q) \
   case q:           \
-    return launch_msv<q>(P, db, o, s);
+    return P.msv_signed ? launch_msv<q, true>(P, db, o, s) : launch_msv<q, false>(P, db, o, s);
     HMM_Q8_CASES(HMM_CASE)
 #undef HMM_CASE
   }

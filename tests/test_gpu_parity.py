@@ -203,7 +203,7 @@ def _ragged_db(prof, seed, lengths=EDGE_LENGTHS, homolog_every=3):
     homs = gen.sample_homologs(rng, prof, len(lengths)) if homolog_every <= len(lengths) else []
     for i, L in enumerate(lengths):
         s = gen.background_residues(rng, L)
-        if i % homolog_every == 0:
+        if homs and i % homolog_every == 0:
             h = homs[i][:L]
             o = int(rng.integers(0, L - h.size + 1))
             s[o:o + h.size] = h
@@ -296,9 +296,16 @@ def test_degenerate_and_extreme_profiles():
     ext.insert[2, 5] = 1.0
     ext.trans[4] = [1.0, 0.0, 0.0, 1.0, 0.0, 0.0, 1.0]
     ext.trans[10] = [0.0, 0.5, 0.5, 0.0, 1.0, 1.0, 0.0]
+    # BIAS8 between 128 and 254: the MSV kernel's unsigned (two-step) path
+    mid = gen.make_profile(80, 10)
+    mid.match[5, 0] = 1e-15
+    mid.match[5, 1] += 0.3
+    mid.match[5] /= mid.match[5].sum()
+    assert 128 <= hg.hmm_debug_tables(mid)["bias8"] <= 254
+    assert hg.hmm_debug_tables(gen.make_profile(80, 10))["bias8"] <= 127
     # (ext has I->I = 1 at node 3: no finite path can be sampled from it, so
     # its targets are background sequences with the rare residue injected)
-    for name, prof, every in (("degenerate", deg, 2), ("extreme", ext, 10**9)):
+    for name, prof, every in (("degenerate", deg, 2), ("extreme", ext, 10**9), ("bias128+", mid, 2)):
         res, off = _ragged_db(prof, 3, lengths=[1, 10, 60, 61, 300, 1000, 64, 128, 129], homolog_every=every)
         res = res.copy()
         res[::7] = 0                                  # many copies of the near-impossible residue
