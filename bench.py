@@ -80,6 +80,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib", default=None,
                     help="mu_msv,mu_vit,tau to use instead of calibrating on the GPU (profiling runs)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
+                    help="run one plain device copy of MB MiB first (scales rocprofv3 byte counters)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "msv_traffic_C3.json"),
                     help="HBM traffic per MSV launch measured by rocprofv3 counters (JSON), if present")
     args = ap.parse_args()
@@ -116,6 +118,14 @@ def main():
     log(f"database packed and uploaded in {upload_s:.2f}s (host buffers, PCIe included; not timed below)")
     out = hg.alloc_results(D.n)
     stream = torch.cuda.current_stream()
+    if args.copy_probe:
+        src = torch.ones(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: {src.numel()} bytes read and written once")
+        del src, dst
     for _ in range(args.warmup):
         hg.search(P, D, w.F, out, stream=stream)
     torch.cuda.synchronize()
