@@ -167,6 +167,16 @@ inline int w_cell(int Q, int q, int lane) { return lane * Q + q; }
 
 uint32_t pack16(int lo, int hi) { return (uint32_t)(uint16_t)lo | ((uint32_t)(uint16_t)hi << 16); }
 
+// IEEE binary16 encoding of an integer with |v| <= 2048 (exact).
+uint16_t half_of_int(int v) {
+  if (v == 0) return 0;
+  const uint16_t sign = v < 0 ? 0x8000 : 0;
+  const unsigned a = (unsigned)(v < 0 ? -v : v);
+  const int e = 31 - __builtin_clz(a);                       // a = 2^e * 1.m
+  const unsigned m = e <= 10 ? (a << (10 - e)) & 0x3ffu : (a >> (e - 10)) & 0x3ffu;
+  return (uint16_t)(sign | ((unsigned)(e + 15) << 10) | m);
+}
+
 // Host quantisation of a validated descriptor into p's host tables.
 void quantize(const hmm_profile_desc *d, hmm_profile *p) {
   const int M = d->M;
@@ -244,16 +254,15 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   // ---- device layouts
   const int Q8 = instantiated_q8(q8_of(M));
   const int Q32 = instantiated_q32(q32_of(M));
-  // MSV: with BIAS8 <= 127 every effective score BIAS8 - COST8 lies in
-  // [-127, 127] and the kernel adds it with one signed saturating op; the
-  // layout then needs one extra (leading) cell.
-  const bool msv_signed = p->bias8 <= 127 && q8_of(M + 1) <= kMaxQ8;
-  const int Qm = msv_signed ? instantiated_q8(q8_of(M + 1)) : Q8;
+  // MSV: diagonal layout when M + 1 cells fit a kernel instance of at most
+  // kMaxQDiag vectors per lane (it needs one padding cell), else striped.
+  const bool msv_diag = q8_of(M + 1) <= kMaxQDiag;
+  const int Qm = msv_diag ? instantiated_q8(q8_of(M + 1)) : instantiated_q8(std::max(q8_of(M), kMaxQDiag));
   if (Q8 < 0 || Q32 < 0 || Qm < 0) {
     delete p;
     return fail(HMM_ERANGE, "M = %d has no kernel instance", M);
   }
-  const size_t n_msv = (size_t)kAlpha * Qm * kWave;            // dwords
+  const size_t n_msv = (size_t)kAlpha * Qm * kWave * (msv_diag ? 2 : 1);  // dwords
   const size_t n_vemit = (size_t)kAlpha * 2 * Q8 * kWave;
   const size_t n_vtr = (size_t)TR_N * Q8 * kWave;
   const size_t n_w32emit = (size_t)kAlpha * 2 * Q32 * kWave;
@@ -305,18 +314,22 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   auto isc_cell = [&](int c, int a) -> int { return c + 1 < M ? p->isc16[(size_t)c * kAlpha + a] : kNone; };
   auto lo16 = [](int v) { return v == INT32_MIN ? kNeg16 : v; };
 
-  auto msv_entry = [&](int pos, int a) -> int {
-    if (msv_signed) {  // position 0 and positions past M are padding: score -128
-      const int c = pos - 1;
-      return (c >= 0 && c < M ? p->bias8 - p->cost8[(size_t)c * kAlpha + a] : -128) * 256;
-    }
-    return (pos < M ? p->cost8[(size_t)pos * kAlpha + a] : 255) << 8;
+  // MSV scores E = BIAS8 - COST8 as fp16 (exact small integers); padding -1024.
+  auto msv_e = [&](int c, int a) -> uint16_t {
+    return half_of_int(c < M ? p->bias8 - (int)p->cost8[(size_t)c * kAlpha + a] : -1024);
   };
-  for (int a = 0; a < kAlpha; a++)
-    for (int q = 0; q < Qm; q++)
-      for (int l = 0; l < kWave; l++)
-        h_msv[(size_t)a * Qm * kWave + pk_index(q, l)] =
-            pack16(msv_entry(pk_cell(Qm, q, l, 0), a), msv_entry(pk_cell(Qm, q, l, 1), a));
+  if (msv_diag) {
+    const int P = 2 * Qm * kWave;
+    for (int a = 0; a < kAlpha; a++)
+      for (int c = 0; c < P; c++)
+        h_msv[(size_t)a * P + c] = (uint32_t)msv_e(c, a) | ((uint32_t)msv_e((c + P / 2) % P, a) << 16);
+  } else {
+    for (int a = 0; a < kAlpha; a++)
+      for (int q = 0; q < Qm; q++)
+        for (int l = 0; l < kWave; l++)
+          h_msv[(size_t)a * Qm * kWave + pk_index(q, l)] =
+              (uint32_t)msv_e(pk_cell(Qm, q, l, 0), a) | ((uint32_t)msv_e(pk_cell(Qm, q, l, 1), a) << 16);
+  }
   for (int a = 0; a < kAlpha; a++)
     for (int q = 0; q < Q8; q++)
       for (int l = 0; l < kWave; l++) {
@@ -378,7 +391,7 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   dv.Q8 = Q8;
   dv.Q32 = Q32;
   dv.Qm = Qm;
-  dv.msv_signed = msv_signed ? 1 : 0;
+  dv.msv_diag = msv_diag ? 1 : 0;
   dv.bias8 = p->bias8;
   dv.entry8 = p->entry8;
   dv.exit8 = p->exit8;

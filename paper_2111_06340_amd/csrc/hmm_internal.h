@@ -15,6 +15,7 @@ constexpr int kBase8 = 190;         // MSV offset of the N/J start
 constexpr int kNeg16 = -32768;      // int16 "minus infinity"
 constexpr int32_t kNeg32 = -(1 << 30);  // int32 rescore floor
 constexpr int kMaxQ8 = 24;          // 128 cells per packed vector -> M <= 3072
+constexpr int kMaxQDiag = 14;       // largest MSV diagonal-layout instance (LDS 10 KB per vector)
 constexpr int kMaxQ32 = 48;         // 64 cells per 32-bit vector -> M <= 3072
 
 // Transition planes of the per-cell "into" layout (cell k = node k+1).
@@ -38,15 +39,14 @@ struct LenParams {
 // Device-side profile, passed to kernels by value.
 struct DevProfile {
   int32_t M, Q8, Q32;
-  int32_t Qm;                   // vectors per lane of the MSV table
-  int32_t msv_signed;           // MSV table layout, see msv below
+  int32_t Qm;                   // vectors per lane of the MSV kernel
+  int32_t msv_diag;             // MSV layout: 1 diagonal, 0 striped (see msv below)
   int32_t bias8, entry8, exit8;
   int32_t entry16, ej16;
   float entry_p;                // 2/(M(M+1))
-  // MSV table [20][Qm][64], packed 16-bit.  msv_signed = 1 (BIAS8 <= 127):
-  // signed scores (BIAS8 - COST8) << 8 with one leading padding cell (cell
-  // k of the profile sits at position k+1); msv_signed = 0: costs COST8 << 8
-  // (high byte), cell k at position k.
+  // MSV table, packed fp16 scores E = BIAS8 - COST8 (padding cells -1024).
+  // msv_diag = 1: [20][P], P = 128 Qm, dword c = (E_c, E_{(c + P/2) mod P});
+  // msv_diag = 0: [20][Qm][64] in the striped packed layout.
   const uint32_t *msv;
   const uint32_t *vit_emit;     // [20][2][Q8][64] packed i16: msc plane, isc plane
   const uint32_t *vit_tr;       // [TR_N][Q8][64] packed i16

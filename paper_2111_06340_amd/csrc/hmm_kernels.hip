@@ -6,10 +6,10 @@
 // special states N/B/E/J/C) lives in scalar registers; branches on it are
 // uniform.
 //
-//  MSV      uint8 values kept in the HIGH byte of 16-bit lanes: packed
-//           saturating u16 add/sub and max then reproduce u8 saturating
-//           arithmetic exactly (the low byte never carries into the high
-//           byte's result).  Two cells per VGPR, 128 slots per wave.
+//  MSV      the uint8 recurrence rewritten exactly in packed fp16 (small
+//           integers), two cells per VGPR: one add and one 3-way maximum
+//           per cell pair; each lane position follows one DP diagonal, so
+//           no cross-lane move is needed (striped layout for large M).
 //  Viterbi  packed saturating int16, two cells per VGPR; delete chain by
 //           lazy propagation across slots.
 //  Rescore  the Viterbi recurrence in int32 with a -2^30 floor.
@@ -18,7 +18,8 @@
 //           maps, E through a DPP sum.
 //
 // Cell layout (see hmm_host.cpp): packed kernels use slot 2*lane+half and
-// cell slot*Q + q; 32-bit kernels use slot = lane and cell lane*Q + q.  The
+// cell slot*Q + q (MSV's diagonal layout aside); 32-bit kernels use
+// slot = lane and cell lane*Q + q.  The
 // left neighbour of vector q is vector q-1 of the same slot, except q = 0,
 // which takes vector Q-1 of the previous slot: one cross-lane shift per
 // state per row.
@@ -133,44 +134,105 @@ __device__ __forceinline__ float wave_sum_f(float v) {
 // table entries of row r+1 are read into the other, so memory latency is
 // hidden behind a whole row of arithmetic and no buffer copy is needed.
 //   load(buf, a): read the table entries of residue a into buf
-//   row(buf):     compute one row from buf; return true to stop early
-// Reads run at most 1 KB past a target, inside the database's zero-filled
-// tail, so prefetched residue codes are always valid (and clamped anyway).
-// Returns true if a row stopped the target early.
-template <typename Buf, typename Load, typename Row>
-__device__ __forceinline__ bool drive_rows(const uint8_t *x, int L, int lane, Buf &ba, Buf &bb, Load load, Row row) {
-  const uint32_t *p = (const uint32_t *)x;
+//   row(buf):     compute one row from buf; return true to stop
+// Rows r0 .. L-1 are run: a start inside a dword runs its first rows one at
+// a time, then whole dwords (4 rows), then the last 0..3 rows one at a
+// time.  With LIMIT, rows from `limit` on (a multiple of 4) are not run.
+// Returns true if a row stopped the driver (`stop` = that row) or the limit
+// was reached (`stop` = limit - 1).  Residue codes are valid (0..19): the
+// database upload checks them, and reads run at most 1 KB past a target,
+// inside the database's zero-filled tail.
+// An empty use of a prefetched table buffer on a driver exit: with it the
+// buffer is live on both sides of the row's stop test, so the compiler keeps
+// its loads ahead of the row (otherwise they sink below the test and every
+// row waits for its own table entries).
+template <typename T, int N>
+__device__ __forceinline__ void keep_loaded(const T (&b)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i++) asm volatile("" ::"v"(b[i]));
+}
+
+template <bool LIMIT = false, typename Buf, typename Load, typename Row>
+__device__ __forceinline__ bool drive_rows(const uint8_t *x, int L, int r0, int limit, int &stop, int lane, Buf &ba,
+                                           Buf &bb, Load load, Row row) {
+  auto code = [](uint32_t w, int r) { return (int)((w >> (8 * r)) & 0xffu); };
+  int r = r0;
+  for (; (r & 3) != 0; r++) {
+    if (r >= L) return false;
+    load(ba, uni((int)x[r]));
+    if (row(ba)) {
+      stop = r;
+      return true;
+    }
+  }
+  if (r >= L) return false;
+  const int cs = r & ~255;
+  const uint32_t *p = (const uint32_t *)(x + cs);
   uint32_t cur = __builtin_nontemporal_load(p + lane);
   uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
-  auto code = [](uint32_t w, int r) { return min((int)((w >> (8 * r)) & 0xffu), kAlpha - 1); };
-  uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, 0);
+  int j0 = (r & 255) >> 2;
+  uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, j0);
   load(ba, code(w, 0));
-  for (int c0 = 0; c0 < L; c0 += 256) {
-    const int nwords = min(kWave, (L - c0 + 3) >> 2);
-    for (int j = 0; j < nwords; j++) {
+  for (int c0 = cs;; c0 += 256) {
+    const int nfull = min(kWave, (L - c0) >> 2);  // whole dwords of rows in this chunk
+    for (int j = j0; j < nfull; j++) {
+      const int rr = c0 + 4 * j;
+      if (LIMIT && rr >= limit) {
+        stop = rr - 1;
+        return true;
+      }
       uint32_t wn;
       if (j == kWave - 1)
         wn = (uint32_t)__builtin_amdgcn_readlane((int)nxt, 0);
       else
         wn = (uint32_t)__builtin_amdgcn_readlane((int)cur, j + 1);
-      const int left = L - c0 - 4 * j;
       load(bb, code(w, 1));
-      if (row(ba)) return true;
-      if (left <= 1) return false;
+      if (row(ba)) {
+        keep_loaded(bb);
+        stop = rr;
+        return true;
+      }
       load(ba, code(w, 2));
-      if (row(bb)) return true;
-      if (left <= 2) return false;
+      if (row(bb)) {
+        keep_loaded(ba);
+        stop = rr + 1;
+        return true;
+      }
       load(bb, code(w, 3));
-      if (row(ba)) return true;
-      if (left <= 3) return false;
+      if (row(ba)) {
+        keep_loaded(bb);
+        stop = rr + 2;
+        return true;
+      }
       load(ba, code(wn, 0));
-      if (row(bb)) return true;
+      if (row(bb)) {
+        keep_loaded(ba);
+        stop = rr + 3;
+        return true;
+      }
       w = wn;
     }
+    if (nfull < kWave) {  // the target's last 0..3 rows, from dword w (row 0's table already in ba)
+      const int rt = c0 + 4 * nfull;
+      if (rt >= L) return false;
+      if (LIMIT && rt >= limit) {
+        stop = rt - 1;
+        return true;
+      }
+      for (int k = 0; rt + k < L; k++) {
+        if (k) load(ba, code(w, k));
+        if (row(ba)) {
+          stop = rt + k;
+          return true;
+        }
+      }
+      return false;
+    }
+    if (c0 + 256 >= L) return false;
+    j0 = 0;
     cur = nxt;
-    nxt = __builtin_nontemporal_load(p + (size_t)((c0 >> 8) + 2) * kWave + lane);
+    nxt = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 2) * kWave + lane);
   }
-  return false;
 }
 
 __device__ __forceinline__ int sat16(int v) { return max(-32768, min(32767, v)); }
@@ -178,108 +240,168 @@ __device__ __forceinline__ int hmax16(uint32_t v) { return max((int)(int16_t)(v 
 
 // ============================================================================ MSV
 //
-// Per row i (residue a), with previous-row mm and xB:
-//   xBe = xB (-) ENTRY8;  mm[k] = (max(mm[k-1], xBe) (+) BIAS8) (-) COST8_k(a)
-//   xE = max mm; overflow if xE >= 255 - BIAS8; xJ = max(xJ, xE (-) EXIT8);
+// Per row i (residue a), with previous-row values v and xB (uint8 semantics,
+// (+)/(-) saturating):
+//   xBe = xB (-) ENTRY8;  v_k = (max(v_{k-1}, xBe) (+) BIAS8) (-) COST8_k(a)
+//   xE = max v; overflow if xE >= 255 - BIAS8; xJ = max(xJ, xE (-) EXIT8);
 //   xB = max(BASE8 (-) MOVE8, xJ (-) MOVE8)
-// xB only depends on max(xJ, BASE8): a running per-lane maximum of all cells
-// is compared each row against the smallest value that could change xB or
-// overflow; only then is the wave-wide maximum taken.  The final xJ is the
-// running maximum (-) EXIT8.  The cost row of the next residue is read from
-// LDS while the current row is computed.
+//
+// Exact reformulation in fp16 (every quantity is an integer of magnitude
+// below 2048, so fp16 adds and maxima are exact).  Rows are only computed
+// while every cell is below the overflow line 255 - BIAS8, so v_{k-1} (+)
+// BIAS8 never saturates and only xBe can reach the 255 ceiling.  With
+// E = BIAS8 - COST8 and Bx = min(xBe, 255 - BIAS8):
+//   v_k = max(v_{k-1} + E, Bx + E, 0).
+// The kernel keeps w = v - Bx, so that
+//   w_k = max3(w_{k-1} + E, E, -Bx)
+// is one packed add and one packed 3-way maximum (v_pk_maximum3_f16) per
+// pair of cells, with E read straight from the table.  A running maximum of
+// all cells (one more 3-way maximum per two vectors) is compared each row
+// against the smallest value that could change xB or overflow; only then is
+// the wave-wide maximum taken, xB updated and w re-based to the new Bx.
+// A predecessor value w = 0 (v = Bx) or w = -Bx (v = 0) both give cell 0 its
+// correct value max(E, -Bx), so cell 0 needs no special case, and padding
+// cells (E = -1024) stay at w = -Bx, below every real cell.
+//
+// Two layouts of the cells over the 64 lanes x 2 halves x Q vectors:
+//  DIAG (M + 1 <= 128 Q): MSV cells depend only on their diagonal
+//    predecessor, so each of the P = 128 Q positions follows one diagonal of
+//    the DP matrix: at row r position p holds cell (p + r) mod P, and its
+//    predecessor is the same position's previous value.  No cross-lane
+//    operation is needed.  The table row of residue a holds
+//    D[c] = (E_c, E_{(c + P/2) mod P}) for c in [0, P); position dword
+//    k = q*64 + lane (halves: diagonals k and k + P/2) reads D[k + r mod P/2],
+//    and every P/2 rows the two halves of each state dword swap roles.  The
+//    padding cell between cell M-1 and cell 0 (P >= M + 1) keeps diagonals
+//    apart.
+//  striped (larger M): slot 2*lane + half holds cells slot*Q + q; vector 0
+//    takes vector Q-1 of the previous slot through one DPP lane shift and
+//    one v_alignbit per row.
+typedef _Float16 h16x2 __attribute__((ext_vector_type(2)));
 
-// Two encodings of the uint8 values in 16-bit lanes:
-//  SIGNED = false: v in the high byte of an unsigned lane; (v (+) BIAS8)
-//    (-) COST8 is one saturating unsigned add and one saturating subtract.
-//  SIGNED = true (BIAS8 <= 127): X = 256 v - 32768 in a signed lane (the low
-//    byte is don't-care).  The two steps fold into one signed saturating add
-//    of 256 (BIAS8 - COST8): the floor at v = 0 is the int16 floor, and the
-//    255 ceiling of the biased add never binds, because a row is only
-//    computed while every cell stays below the overflow line 255 - BIAS8
-//    (the trigger is never above it), so v + BIAS8 < 255.  Cell k sits at
-//    position k+1: position 0 is padding with score -128, so the zero that
-//    the lane shift feeds in (which encodes v = 128) becomes
-//    max(0, xBe - 128) <= xBe there, and cell 0 sees xBe as required.
-//    Padding never exceeds the row's maximum, so xE is unaffected.
-template <int Q, bool SIGNED>
+__device__ __forceinline__ h16x2 as_h2(uint32_t v) { return __builtin_bit_cast(h16x2, v); }
+__device__ __forceinline__ uint32_t as_u(h16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ __forceinline__ h16x2 h2_splat(int v) {
+  const _Float16 h = (_Float16)(float)v;
+  return h16x2{h, h};
+}
+__device__ __forceinline__ h16x2 h2_max3(h16x2 a, h16x2 b, h16x2 c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+__device__ __forceinline__ int h2_hmax(h16x2 v) { return (int)(float)__builtin_elementwise_maximum(v.x, v.y); }
+
+template <int Q, bool DIAG>
 __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOut out) {
+  constexpr int kHalf = Q * kWave;                 // P/2 in DIAG, dwords per table row otherwise
+  constexpr int kRow = DIAG ? 2 * kHalf : kHalf;   // dwords per residue in the table
   extern __shared__ uint32_t lds[];
   {
     const uint4 *src = (const uint4 *)P.msv;
     uint4 *dst = (uint4 *)lds;
-    for (int i = threadIdx.x; i < kAlpha * Q * kWave / 4; i += blockDim.x) dst[i] = src[i];
+    for (int i = threadIdx.x; i < kAlpha * kRow / 4; i += blockDim.x) dst[i] = src[i];
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
-  const int bias8 = P.bias8, entry8 = P.entry8, exit8 = P.exit8;
-  const uint32_t bias2 = splat16(bias8 << 8);
-  const int ovf_line = 255 - bias8;
-  // encoding of a uint8 value v and decoding of a lane maximum
-  auto enc = [](int v) { return SIGNED ? v * 256 - 32768 : v << 8; };
-  auto dec_max = [](uint32_t a) -> int {
-    return SIGNED ? (hmax16(a) + 32768) >> 8 : (int)(max(a & 0xffffu, a >> 16) >> 8);
-  };
+  const int entry8 = P.entry8, exit8 = P.exit8;
+  const int ovf_line = 255 - P.bias8;
   const uint32_t *tab = lds + lane;
   const int n = (int)db.n;
+  // packed fp16 pair (v, v) as a wave-uniform dword
+  auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
   for (int t = wave_id(); t < n; t += nw) {
     const int L = uni(db.len[t]);
     const LenParams lp = db.lp[L];
     const int mv = lp.move8;
     const int base = max(kBase8 - mv, 0);
     int xJt = 0;
+    int Bx = min(max(base - entry8, 0), max(ovf_line, 0));
     bool ovf = ovf_line <= 0;
-    uint32_t acc = splat16(enc(0));
+    h16x2 acc = as_h2(splat(-Bx));
     if (!ovf) {
-      uint32_t mm[Q];
+      h16x2 w[Q];
 #pragma unroll
-      for (int q = 0; q < Q; q++) mm[q] = splat16(enc(0));
-      int T = min(ovf_line, kBase8 + 4);
-      uint32_t thr2 = splat16(enc(T) - 1);
-      uint32_t xbe2 = splat16(enc(max(base - entry8, 0)));
-      // The trigger value and xBe stay fixed (scalars) until some cell
-      // reaches the trigger; then xJ and xB are updated, or the target stops
-      // on overflow.
+      for (int q = 0; q < Q; q++) w[q] = acc;
+      uint32_t nbx = splat(-Bx);
+      // Trigger: some cell reaches T, the smallest value that could change
+      // xB or overflow; in w units, some w > T - Bx - 1.
+      auto trigger_thr = [&]() { return splat(min(ovf_line, max(xJt, kBase8) + 4) - Bx - 1); };
+      uint32_t thr = trigger_thr();
+      // DIAG: byte offset of the next load's row in the table, 4 (row mod
+      // P/2).  The driver stops at every multiple of P/2 rows, so at most one
+      // (discarded) prefetch reads one dword row past P/2: still inside
+      // the residue's table row, which holds P dwords.
+      int lofs = 0;
       auto load = [&](uint32_t(&c)[Q], int a) {
-        const uint32_t *row = tab + a * (Q * kWave);
+        const uint32_t *row = (const uint32_t *)((const char *)tab + a * (kRow * 4) + (DIAG ? lofs : 0));
 #pragma unroll
         for (int q = 0; q < Q; q++) c[q] = row[q * kWave];
+        if (DIAG) lofs += 4;
       };
+      // One row.  Only w and the running maximum change here, on every row:
+      // a trigger stops the row driver, and so does (DIAG) the end of a
+      // P/2-row phase; the caller then updates xJ and xB, re-bases or swaps
+      // w, and resumes at the next row.
       auto row = [&](const uint32_t(&c)[Q]) -> bool {
-        const uint32_t sh = slot_up16(mm[Q - 1]);
+        if (DIAG) {
 #pragma unroll
-        for (int q = Q - 1; q >= 0; q--) {
-          uint32_t v;
-          if (SIGNED) {
-            v = i16_max(q ? mm[q - 1] : sh, xbe2);
-            v = i16_adds(v, c[q]);
-            acc = i16_max(acc, v);
-          } else {
-            v = u16_max(q ? mm[q - 1] : sh, xbe2);
-            v = u16_adds(v, bias2);
-            v = u16_subs(v, c[q]);
-            acc = u16_max(acc, v);
+          for (int q = 0; q < Q; q++) {
+            const h16x2 e = as_h2(c[q]);
+            w[q] = h2_max3(w[q] + e, e, as_h2(nbx));
           }
-          mm[q] = v;
+        } else {
+          const uint32_t sh = slot_up16(as_u(w[Q - 1]));
+#pragma unroll
+          for (int q = Q - 1; q >= 0; q--) {
+            const h16x2 e = as_h2(c[q]);
+            w[q] = h2_max3((q ? w[q - 1] : as_h2(sh)) + e, e, as_h2(nbx));
+          }
         }
-        const bool trig = SIGNED ? any_lane(i16_max(acc, thr2) != thr2) : any_lane(u16_subs(acc, thr2) != 0u);
-        if (trig) {
-          const int m = wave_max_i32(dec_max(acc));
-          if (m >= ovf_line) return true;
-          xJt = max(xJt, max(m - exit8, 0));
-          const int xB = max(base, max(xJt - mv, 0));
-          xbe2 = splat16(enc(max(xB - entry8, 0)));
-          T = min(ovf_line, max(xJt, kBase8) + 4);
-          thr2 = splat16(enc(T) - 1);
-        }
-        return false;
+#pragma unroll
+        for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
+        if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
+        return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr);
       };
       uint32_t ca[Q], cb[Q];
-      ovf = drive_rows(db.res + db.start[t], L, lane, ca, cb, load, row);
+      const uint8_t *x = db.res + db.start[t];
+      int r = 0;
+      for (;;) {
+        int stop = 0;
+        const int limit = DIAG ? (r / kHalf + 1) * kHalf : 0;   // end of the current phase
+        if (!drive_rows<DIAG>(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
+        const int m = wave_max_i32(h2_hmax(acc)) + Bx;      // largest cell so far
+        if (m >= ovf_line) {
+          ovf = true;
+          break;
+        }
+        xJt = max(xJt, max(m - exit8, 0));
+        const int nBx = min(max(max(base, max(xJt - mv, 0)) - entry8, 0), ovf_line);
+        if (nBx != Bx) {  // re-base w (and the running maximum) to the new Bx
+          const h16x2 d = as_h2(splat(Bx - nBx));
+#pragma unroll
+          for (int q = 0; q < Q; q++) w[q] += d;
+          acc += d;
+          Bx = nBx;
+          nbx = splat(-Bx);
+        }
+        thr = trigger_thr();
+        r = stop + 1;
+        if (r >= L) break;
+        if (DIAG) {
+          lofs = 4 * (r % kHalf);
+          if (lofs == 0) {  // the halves of every state dword swap diagonals
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+              const uint32_t u = as_u(w[q]);
+              w[q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
+            }
+          }
+        }
+      }
     }
     int raw = 255;
     if (!ovf) {
-      const int m = wave_max_i32(dec_max(acc));
+      const int m = wave_max_i32(h2_hmax(acc)) + Bx;
       const int xJ = max(m - exit8, 0);
       raw = max(xJ - mv, 0);
     }
@@ -384,7 +506,8 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     return false;
   };
   uint32_t ea[2 * Q], eb[2 * Q];
-  ovf = drive_rows(x, L, lane, ea, eb, load, row);
+  int stop;
+  ovf = drive_rows(x, L, 0, 0, stop, lane, ea, eb, load, row);
   if (!ovf) ovf = any_lane(hmax16(accI) >= 32767);
   VitResult res;
   res.ovf = ovf;
@@ -534,7 +657,8 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
       return false;
     };
     int ea[2 * Q], eb[2 * Q];
-    (void)drive_rows(db.res + db.start[t], L, lane, ea, eb, load, row);
+    int stop;
+    (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
     const int m = wave_max_i32(accM);
     const int v = fl32(fl32(m + ej) + mv);
     out.vit[uni(db.perm[t])] = v;
@@ -674,7 +798,8 @@ __global__ void __launch_bounds__(512) fwd_kernel(DevProfile P, DevDb db, DevOut
       return false;
     };
     float ea[2 * Q], eb[2 * Q];
-    (void)drive_rows(db.res + db.start[t], L, lane, ea, eb, load, row);
+    int stop;
+    (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
     const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
     const bool pass = f > lp.fthr;
     const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
@@ -721,20 +846,19 @@ int blocks_per_cu(K kernel, int threads, size_t lds) {
   return nb;
 }
 
-template <int Q, bool SIGNED>
+template <int Q, bool DIAG>
 hipError_t launch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  const int threads = Q >= 12 ? 1024 : 512;
-  const size_t lds = (size_t)kAlpha * Q * kWave * 4;
-  auto k = msv_kernel<Q, SIGNED>;
+  const int threads = 1024;
+  const size_t lds = (size_t)kAlpha * Q * kWave * 4 * (DIAG ? 2 : 1);
+  auto k = msv_kernel<Q, DIAG>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
   static int bpc = 0;
   if (!bpc) bpc = blocks_per_cu(k, threads, lds);
-  const int64_t waves_needed = db.n;
   int64_t blocks = (int64_t)bpc * num_cu();
-  const int64_t cap = (waves_needed + threads / 64 - 1) / (threads / 64);
+  const int64_t cap = (db.n + threads / 64 - 1) / (threads / 64);
   if (blocks > cap) blocks = cap;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), lds, s, P, db, o);
@@ -806,13 +930,28 @@ hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hip
 #define HMM_Q32_CASES(X) \
   X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12) X(14) X(16) X(20) X(24) X(28) X(32) X(40) X(48)
 
+// MSV instances: diagonal layout up to 14 vectors per lane (table 10 KB per
+// vector in LDS), striped above.
+#define HMM_MSV_DIAG_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14)
+#define HMM_MSV_STRIPED_CASES(X) X(14) X(16) X(20) X(24)
+
 hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  switch (P.Qm) {
+  if (P.msv_diag) {
+    switch (P.Qm) {
 #define HMM_CASE(q) \
   case q:           \
-    return P.msv_signed ? launch_msv<q, true>(P, db, o, s) : launch_msv<q, false>(P, db, o, s);
-    HMM_Q8_CASES(HMM_CASE)
+    return launch_msv<q, true>(P, db, o, s);
+      HMM_MSV_DIAG_CASES(HMM_CASE)
 #undef HMM_CASE
+    }
+  } else {
+    switch (P.Qm) {
+#define HMM_CASE(q) \
+  case q:           \
+    return launch_msv<q, false>(P, db, o, s);
+      HMM_MSV_STRIPED_CASES(HMM_CASE)
+#undef HMM_CASE
+    }
   }
   return hipErrorInvalidValue;
 }

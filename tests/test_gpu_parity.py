@@ -279,6 +279,41 @@ def test_overflow_and_rescore(M):
         announce(f"overflow M={M} F={F} ok {st}")
 
 
+def _high_bias_profiles():
+    """Small profiles whose BIAS8 is pushed up by one near-impossible
+    residue, so that xB - ENTRY8 + BIAS8 exceeds 255 on short targets: the
+    uint8 add of BIAS8 then saturates before COST8 is subtracted (the MSV
+    corner where the saturation order matters)."""
+    out = []
+    for seed in range(12):
+        rng = np.random.default_rng(1000 + seed)
+        M = int(rng.integers(1, 12))
+        prof = gen.make_profile(M, 1000 + seed)
+        k, r = int(rng.integers(0, M)), int(rng.integers(0, 20))
+        prof.match[k, r] = 10.0 ** (-float(rng.uniform(9, 14)))
+        prof.match[k] /= prof.match[k].sum()
+        out.append((prof, r))
+    return out
+
+
+def test_msv_biased_entry_saturates_before_cost():
+    hit = 0
+    for i, (prof, rare) in enumerate(_high_bias_profiles()):
+        sc = oracle.OracleProfile(prof).scalars()
+        hit += oracle.BASE8 - 1 - sc["entry8"] + sc["bias8"] > 255   # xB - ENTRY8 at L = 1
+        rng = np.random.default_rng(77 + i)
+        lengths = rng.integers(1, 31, 500)
+        res = rng.integers(0, 20, int(lengths.sum())).astype(np.uint8)
+        res[rng.random(res.size) < 0.3] = rare
+        off = np.zeros(lengths.size + 1, np.int64)
+        off[1:] = np.cumsum(lengths)
+        g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+        announce(f"high-bias profile {i} M={prof.M} bias8={sc['bias8']} entry8={sc['entry8']} "
+                 f"ok {compare(g, o, what=f'high-bias {i}')}")
+    assert hit >= 4, "too few profiles reach the saturation corner"
+
+
 def test_degenerate_and_extreme_profiles():
     rng = np.random.default_rng(5)
     # BIAS8 clamps at 255: MSV overflows on every target
