@@ -142,7 +142,10 @@ int hmm_db_free(hmm_db *db);
 /* Search one profile against a database: MSV on every target, Viterbi on
  * MSV survivors, int32 rescore of int16-overflowed targets, Forward on
  * Viterbi survivors.  Enqueued on `stream` without host synchronisation
- * (except when the cutoffs change, see below); allocates nothing.
+ * (except when the cutoffs change, see below); allocates nothing.  The
+ * rescore runs on a stream owned by the database, forked from `stream`
+ * after the int16 Viterbi and joined back before the search ends, so all
+ * of the search's work is ordered on `stream`.
  * Searches on one database are serialised by the library (a search on a
  * second stream waits for the previous one on the GPU).  Changing the
  * cutoffs or the profile between searches on a database rebuilds a small
@@ -161,10 +164,14 @@ int hmm_db_stage_timing(hmm_db *db, int32_t capacity);
 
 /* Stage durations (ms) of the recorded searches, oldest first:
  * out_ms[4*i + s] for search i and stage s = MSV, Viterbi int16, int32
- * rescore, Forward (each including its small list/counter kernels).  At
- * most `cap` searches are returned, their number in *n.  Waits for the
- * recorded searches to finish and clears the record.  Errors: HMM_EINVAL,
- * HMM_EDEVICE. */
+ * rescore, Forward (each including its small list/counter kernels).  The
+ * rescore and Forward run concurrently (the rescore on a stream internal to
+ * the database, forked from and joined back into the search stream): both
+ * are timed from the end of the int16 Viterbi stage, the rescore to its own
+ * end and Forward to the end of both, so Forward's figure is the time the
+ * two together add to the search.  At most `cap` searches are returned,
+ * their number in *n.  Waits for the recorded searches to finish and
+ * clears the record.  Errors: HMM_EINVAL, HMM_EDEVICE. */
 int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n);
 
 /* Database properties: number of targets, total residues, longest target. */

@@ -108,11 +108,18 @@ struct hmm_db {
   double lp_F[3] = {-1, -1, -1};
   hipEvent_t done = nullptr;   // completion of the latest search
   bool searched = false;
+  // The int32 rescore runs on `aux`, concurrently with Forward on the search
+  // stream, between the events fork (recorded on the search stream) and
+  // join (recorded on aux).
+  hipStream_t aux = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   // stage timing ring (profiling hook)
   std::vector<hipEvent_t> tev;  // capacity * 5
   int32_t tcap = 0;
   int64_t trec = 0;             // searches recorded since the last read
 };
+
+static void release_sync(hmm_db *db);
 
 namespace {
 
@@ -606,7 +613,11 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   (void)hipHostFree(stage);
   if (e == hipSuccess) e = hipHostMalloc((void **)&db->h_lp, sz_lp, hipHostMallocDefault);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&db->done, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->join, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&db->aux, hipStreamNonBlocking);
   if (e != hipSuccess) {
+    release_sync(db);
     (void)hipFree(db->dmem);
     if (db->h_lp) (void)hipHostFree(db->h_lp);
     delete db;
@@ -629,6 +640,15 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   dv.lp = db->d_lp;
   *out = db;
   return HMM_OK;
+}
+
+static void release_sync(hmm_db *db) {
+  if (db->aux) (void)hipStreamDestroy(db->aux);
+  if (db->join) (void)hipEventDestroy(db->join);
+  if (db->fork) (void)hipEventDestroy(db->fork);
+  if (db->done) (void)hipEventDestroy(db->done);
+  db->aux = nullptr;
+  db->join = db->fork = db->done = nullptr;
 }
 
 static void drop_timing(hmm_db *db) {
@@ -665,8 +685,12 @@ int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n) {
   int32_t k = 0;
   for (int64_t i = first; i < db->trec && k < cap; i++, k++) {
     hipEvent_t *ev = &db->tev[(size_t)(i % db->tcap) * 5];
-    for (int st = 0; st < 4; st++)
-      HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + st], ev[st], ev[st + 1]), "hipEventElapsedTime");
+    // ev: search start, MSV end, Viterbi end (fork), rescore end (aux
+    // stream), end of Forward and rescore (join)
+    HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + 0], ev[0], ev[1]), "hipEventElapsedTime");
+    HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + 1], ev[1], ev[2]), "hipEventElapsedTime");
+    HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + 2], ev[2], ev[3]), "hipEventElapsedTime");
+    HIP_TRY(hipEventElapsedTime(&out_ms[4 * k + 3], ev[2], ev[4]), "hipEventElapsedTime");
   }
   *n = k;
   db->trec = 0;
@@ -678,7 +702,7 @@ int hmm_db_free(hmm_db *db) {
   hipError_t e = hipSuccess;
   if (db->searched) e = hipEventSynchronize(db->done);
   drop_timing(db);
-  if (db->done) (void)hipEventDestroy(db->done);
+  release_sync(db);
   if (db->h_lp) (void)hipHostFree(db->h_lp);
   hipError_t e2 = db->dmem ? hipFree(db->dmem) : hipSuccess;
   delete db;
@@ -721,7 +745,7 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts};
   hipEvent_t *ev = nullptr;
   if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
-  HIP_TRY(launch_search(p->dev, db->dev, o, s, ev), "kernel launch");
+  HIP_TRY(launch_search(p->dev, db->dev, o, s, db->aux, db->fork, db->join, ev), "kernel launch");
   HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
   db->searched = true;
   return HMM_OK;

@@ -82,10 +82,14 @@ struct DevOut {
   int64_t *counts;
 };
 
-// Enqueue the whole cascade on `stream`.  When `ev` is non-null, ev[0..4]
-// are recorded before MSV and after MSV, Viterbi, rescore and Forward.
+// Enqueue the whole cascade on `stream`.  The int32 rescore runs on `aux`,
+// concurrently with Forward: it forks after the int16 Viterbi (event
+// `fork`) and joins before the final counter export (event `join`), so all
+// work stays ordered on `stream`.  When `ev` is non-null, ev[0..4] are
+// recorded at the start, after MSV, after Viterbi (the fork), after the
+// rescore (on aux) and after the join.
 hipError_t launch_search(const DevProfile &p, const DevDb &db, const DevOut &out, hipStream_t stream,
-                         hipEvent_t *ev);
+                         hipStream_t aux, hipEvent_t fork, hipEvent_t join, hipEvent_t *ev);
 
 // Number of packed vectors per lane.
 inline int q8_of(int M) { return (M + 2 * kWave - 1) / (2 * kWave); }

@@ -309,8 +309,20 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   const int n = (int)db.n;
   // packed fp16 pair (v, v) as a wave-uniform dword
   auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
-  for (int t = wave_id(); t < n; t += nw) {
-    const int L = uni(db.len[t]);
+  // The next target's length and start are read during the current
+  // target's epilogue, so a target starts with one round trip (its length
+  // parameters and first residue chunks, in parallel) instead of three.
+  int t = wave_id();
+  int Lnext = 0;
+  int64_t snext = 0;
+  if (t < n) {
+    Lnext = uni(db.len[t]);
+    snext = db.start[t];
+  }
+  for (; t < n; t += nw) {
+    const int L = Lnext;
+    const uint8_t *x = db.res + snext;
+    const int cperm = db.perm[t];  // read now, used at the end
     const LenParams lp = db.lp[L];
     const int mv = lp.move8;
     const int base = max(kBase8 - mv, 0);
@@ -363,7 +375,6 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
         return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr);
       };
       uint32_t ca[Q], cb[Q];
-      const uint8_t *x = db.res + db.start[t];
       int r = 0;
       for (;;) {
         int stop = 0;
@@ -399,6 +410,10 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
         }
       }
     }
+    if (t + nw < n) {
+      Lnext = uni(db.len[t + nw]);
+      snext = db.start[t + nw];
+    }
     int raw = 255;
     if (!ovf) {
       const int m = wave_max_i32(h2_hmax(acc)) + Bx;
@@ -407,7 +422,7 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     }
     const bool pass = ovf || raw >= lp.thr8;
     const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
-    const int c = uni(db.perm[t]);
+    const int c = uni(cperm);
     db.flags_sorted[t] = fl;
     out.flags[c] = fl;
     out.msv[c] = (int16_t)raw;
@@ -614,14 +629,16 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
       const int msh = lane_up_i(M[Q - 1]);
       const int ish = lane_up_i(I[Q - 1]);
       const int dsh = lane_up_i(D[Q - 1]);
+      // Every state and table value is >= -2^30, so each add fits in int32,
+      // and the floor of every add inside a maximum is one floor of the
+      // maximum: max(fl32(a), fl32(b)) = max(a, b, -2^30).  The M maximum
+      // includes xBe >= -2^30 and needs no floor at all.
 #pragma unroll
       for (int q = Q - 1; q >= 0; q--) {
         const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-        int m = max(xbe, fl32(pm + TR(TR_MMIN, q)));
-        m = max(m, fl32(pi + TR(TR_IMIN, q)));
-        m = max(m, fl32(pd + TR(TR_DMIN, q)));
+        const int m = max(max(xbe, pm + TR(TR_MMIN, q)), max(pi + TR(TR_IMIN, q), pd + TR(TR_DMIN, q)));
         const int mn = fl32(m + em[q]);
-        const int in = fl32(max(fl32(M[q] + TR(TR_MI, q)), fl32(I[q] + TR(TR_II, q))) + em[Q + q]);
+        const int in = fl32(max(max(M[q] + TR(TR_MI, q), I[q] + TR(TR_II, q)), kNeg32) + em[Q + q]);
         accM = max(accM, mn);
         M[q] = mn;
         I[q] = in;
@@ -630,7 +647,7 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
       const int din = lane_up_i(M[Q - 1]);
 #pragma unroll
       for (int q = 0; q < Q; q++) {
-        D[q] = max(fl32((q ? M[q - 1] : din) + TR(TR_MDIN, q)), fl32(dc + TR(TR_DDIN, q)));
+        D[q] = max(max((q ? M[q - 1] : din) + TR(TR_MDIN, q), dc + TR(TR_DDIN, q)), kNeg32);
         dc = D[q];
       }
       for (int it = 0; it < kWave; it++) {
@@ -639,7 +656,7 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
 #pragma unroll
         for (int q = 0; q < Q; q++) {
           if (moved) {
-            const int nd = max(D[q], fl32(dc + TR(TR_DDIN, q)));
+            const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= -2^30 already
             moved = any_lane(nd != D[q]);
             D[q] = nd;
             dc = nd;
@@ -991,27 +1008,34 @@ hipError_t dispatch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, h
 
 }  // namespace
 
-hipError_t launch_search(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s, hipEvent_t *ev) {
+hipError_t launch_search(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s, hipStream_t aux,
+                         hipEvent_t fork, hipEvent_t join, hipEvent_t *ev) {
   if (db.n <= 0) return hipSuccess;
   hipError_t e = hipSuccess;
-  auto mark = [&](int i) {
-    if (ev && e == hipSuccess) e = hipEventRecord(ev[i], s);
+  auto mark = [&](int i, hipStream_t st) {
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[i], st);
   };
-  mark(0);
+  mark(0, s);
   hipLaunchKernelGGL(clear_counters, dim3(1), dim3(64), 0, s, db.counters);
   e = hipGetLastError();
   if (e == hipSuccess) e = dispatch_msv(P, db, o, s);
-  mark(1);
+  mark(1, s);
   if (e == hipSuccess) e = dispatch_vit16(P, db, o, s);
-  mark(2);
-  if (e == hipSuccess) e = dispatch_vit32(P, db, o, s);
-  mark(3);
+  mark(2, s);
+  // An int16 overflow passes the Viterbi filter whatever its exact score,
+  // so Forward needs nothing from the rescore: the two run side by side.
+  if (e == hipSuccess) e = hipEventRecord(fork, s);
+  if (e == hipSuccess) e = hipStreamWaitEvent(aux, fork, 0);
+  if (e == hipSuccess) e = dispatch_vit32(P, db, o, aux);
+  mark(3, aux);
   if (e == hipSuccess) e = dispatch_fwd(P, db, o, s);
+  if (e == hipSuccess) e = hipEventRecord(join, aux);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
   if (e == hipSuccess && o.counts) {
     hipLaunchKernelGGL(export_counts, dim3(1), dim3(64), 0, s, db.counters, o.counts);
     e = hipGetLastError();
   }
-  mark(4);
+  mark(4, s);
   return e;
 }
 
