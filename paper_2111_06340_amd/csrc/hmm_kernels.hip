@@ -445,6 +445,15 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
 // would raise it.  The delete chain is computed inside each slot, then
 // propagated across slots until no lane changes (exact: sat is monotone).
 
+// Threads per block of the Viterbi, rescore and Forward kernels.  Large
+// instances run one wave per SIMD (4 waves per block): each wave may then
+// use the whole register file, architectural and accumulation registers,
+// and spills go to accumulation registers rather than to scratch memory.
+template <int Q>
+constexpr int kThreads16 = Q >= 16 ? 256 : 512;   // packed int16 Viterbi
+template <int Q>
+constexpr int kThreads32 = Q >= 14 ? 256 : 512;   // int32 rescore and Forward
+
 struct VitResult {
   int raw;
   bool ovf;
@@ -536,7 +545,7 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
 }
 
 template <int Q, bool EMIT_LDS>
-__global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevOut out) {
+__global__ void __launch_bounds__(kThreads16<Q>) vit16_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x & 63;
   if (EMIT_LDS) {
@@ -581,7 +590,7 @@ __global__ void __launch_bounds__(512) vit16_kernel(DevProfile P, DevDb db, DevO
 __device__ __forceinline__ int fl32(int v) { return max(v, kNeg32); }
 
 template <int Q, bool EMIT_LDS, bool TR_LDS>
-__global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
+__global__ void __launch_bounds__(kThreads32<Q>) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ int32_t lds32[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;   // dwords
@@ -603,7 +612,11 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
 #pragma unroll
       for (int q = 0; q < kTrRegs; q++) tr[k][q] = trp[(k * Q + q) * kWave];
   }
-  auto TR = [&](int k, int q) -> int { return TR_LDS ? trp[(k * Q + q) * kWave] : tr[k][TR_LDS ? 0 : q]; };
+  // Transitions read from LDS are re-read on every row: `trofs` (always 0)
+  // is hidden from the compiler once per row, so the reads cannot be hoisted
+  // out of the row loop into registers (which would spill).
+  int trofs = 0;
+  auto TR = [&](int k, int q) -> int { return TR_LDS ? trp[(k * Q + q) * kWave + trofs] : tr[k][TR_LDS ? 0 : q]; };
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
@@ -626,6 +639,7 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
       for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
     };
     auto row = [&](const int(&em)[2 * Q]) -> bool {
+      if (TR_LDS) asm volatile("" : "+v"(trofs));
       const int msh = lane_up_i(M[Q - 1]);
       const int ish = lane_up_i(I[Q - 1]);
       const int dsh = lane_up_i(D[Q - 1]);
@@ -698,7 +712,7 @@ __global__ void __launch_bounds__(512) vit32_kernel(DevProfile P, DevDb db, DevO
 // exponents are summed.  Result: ln(C move) + (sum of exponents) ln 2, nats.
 
 template <int Q, bool EMIT_LDS, bool TR_LDS>
-__global__ void __launch_bounds__(512) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
+__global__ void __launch_bounds__(kThreads32<Q>) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ float ldsf[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;
@@ -720,7 +734,9 @@ __global__ void __launch_bounds__(512) fwd_kernel(DevProfile P, DevDb db, DevOut
 #pragma unroll
       for (int q = 0; q < kR; q++) tr[k][q] = trp[(k * Q + q) * kWave];
   }
-  auto TR = [&](int k, int q) -> float { return TR_LDS ? trp[(k * Q + q) * kWave] : tr[k][TR_LDS ? 0 : q]; };
+  // Transitions read from LDS are re-read on every row (see the rescore).
+  int trofs = 0;
+  auto TR = [&](int k, int q) -> float { return TR_LDS ? trp[(k * Q + q) * kWave + trofs] : tr[k][TR_LDS ? 0 : q]; };
   // P part of the delete-chain scan: the lane's P before each of the six steps
   float pstep[6];
   {
@@ -756,6 +772,7 @@ __global__ void __launch_bounds__(512) fwd_kernel(DevProfile P, DevDb db, DevOut
       for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
     };
     auto row = [&](const float(&em)[2 * Q]) -> bool {
+      if (TR_LDS) asm volatile("" : "+v"(trofs));
       const float msh = lane_up_f(M[Q - 1]);
       const float ish = lane_up_f(I[Q - 1]);
       const float dsh = lane_up_f(D[Q - 1]);
@@ -885,7 +902,7 @@ hipError_t launch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hip
 template <int Q>
 hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   constexpr bool kLds = Q <= 8;
-  const int threads = 512;
+  const int threads = kThreads16<Q>;
   const size_t lds = kLds ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0;
   auto k = vit16_kernel<Q, kLds>;
   if (lds > 64 * 1024) {
@@ -904,9 +921,8 @@ hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, h
 // Persistent launch of a list kernel: as many blocks as fit, at most one
 // wave per database target.
 template <typename K>
-hipError_t launch_list_kernel(K k, int &bpc, size_t lds, const DevProfile &P, const DevDb &db, const DevOut &o,
-                              hipStream_t s) {
-  const int threads = 512;
+hipError_t launch_list_kernel(K k, int threads, int &bpc, size_t lds, const DevProfile &P, const DevDb &db,
+                              const DevOut &o, hipStream_t s) {
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -932,7 +948,7 @@ hipError_t launch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, h
   constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
   const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)TR_N * Q * kWave * 4 : 0);
   static int bpc = 0;
-  return launch_list_kernel(vit32_kernel<Q, E, T>, bpc, lds, P, db, o, s);
+  return launch_list_kernel(vit32_kernel<Q, E, T>, kThreads32<Q>, bpc, lds, P, db, o, s);
 }
 
 template <int Q>
@@ -940,7 +956,7 @@ hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hip
   constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
   const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)(TR_N + 1) * Q * kWave * 4 : 0);
   static int bpc = 0;
-  return launch_list_kernel(fwd_kernel<Q, E, T>, bpc, lds, P, db, o, s);
+  return launch_list_kernel(fwd_kernel<Q, E, T>, kThreads32<Q>, bpc, lds, P, db, o, s);
 }
 
 #define HMM_Q8_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14) X(16) X(20) X(24)
