@@ -8,14 +8,20 @@ Prints one JSON line on stdout; progress goes to stderr.
 Metric: GCUPS = M x (database residues) / (seconds per step) / 1e9.
 Default workload: M = 734 profile against 1,000,000 synthetic sequences
 (~348M residues, 0.5 % planted homologs), MSV P < 0.02 -> Viterbi
-P < 1e-3 -> Forward on survivors.
+P < 1e-3 -> Forward on survivors.  Other modes: --workload C1/C2/C5 (the
+other single-profile configurations), --workload C4 (64 profiles, M 50-400,
+against the C3 database; one step searches all 64, reported as aggregate
+GCUPS and queries/hour), --cutoffs F1,F2,F3 (e.g. 1,1e-3,1 runs Viterbi on
+every target).
 
 Roofline of the dominant kernel (MSV): plain packed-int16 VALU arithmetic,
 4 element-ops per cell (max, saturating add, saturating subtract, max), so
 achieved = 4 x cells / (average MSV duration), against the MI355X packed
 16-bit VALU peak 256 CU x 64 lanes x 2 elements x 2.4 GHz = 78.64 Tops/s.
 The MSV duration is measured with HIP events that the library records on
-the search stream around the stage.
+the search stream around the stage.  `stage_roofline` gives the same
+fraction for every stage (Viterbi 18 ops/cell, rescore 17 int32 ops/cell
+against 39.32 Tops/s, Forward 18 flops/cell against 157.3 TFLOP/s).
 """
 from __future__ import annotations
 
@@ -30,8 +36,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_PK16_TOPS = 256 * 64 * 2 * 2.4e9 / 1e12      # 78.64
+PEAK_I32_TOPS = 256 * 64 * 2.4e9 / 1e12           # 39.32
+PEAK_FP32_TFLOPS = 157.3                          # datasheet (packed fp32 FMA)
 MSV_OPS_PER_CELL = 4
 VIT_OPS_PER_CELL = 18
+RESCORE_OPS_PER_CELL = 17
+FWD_FLOPS_PER_CELL = 18
 
 
 def log(msg):
@@ -70,12 +80,36 @@ def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
             "seconds": round(t, 2)}
 
 
+def stage_roofline(M_list, res_total, ran_cells, st_ms):
+    """Per-stage fractions of the relevant VALU peak: algorithmic ops of the
+    cells each stage processed, over its measured time (HIP events)."""
+    msv_ops = MSV_OPS_PER_CELL * sum(M * res_total for M in M_list)
+    out = {}
+
+    def entry(ops, ms, peak, unit):
+        ach = ops / (ms / 1e3) / 1e12 if ms > 0 else 0.0
+        return {"achieved": round(ach, 3), "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
+
+    out["msv"] = entry(msv_ops, st_ms[0], round(PEAK_PK16_TOPS, 2), "Tops/s packed 16-bit, 4 ops/cell")
+    out["viterbi"] = entry(VIT_OPS_PER_CELL * ran_cells["viterbi"], st_ms[1], round(PEAK_PK16_TOPS, 2),
+                           "Tops/s packed 16-bit, 18 ops/cell")
+    out["rescore"] = entry(RESCORE_OPS_PER_CELL * ran_cells["rescore"], st_ms[2], round(PEAK_I32_TOPS, 2),
+                           "Tops/s 32-bit, 17 ops/cell")
+    # Forward runs beside the rescore; its figure here uses the time both take
+    out["forward"] = entry(FWD_FLOPS_PER_CELL * ran_cells["forward"], st_ms[3], PEAK_FP32_TFLOPS,
+                           "TFLOP/s fp32, 18 flops/cell (datasheet peak counts packed fp32)")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="C3", choices=["C1", "C2", "C3", "C5"])
+    ap.add_argument("--workload", default="C3", choices=["C1", "C2", "C3", "C4", "C5"],
+                    help="C4 = 64 profiles (M 50-400) against the C3 database; one step searches all 64")
+    ap.add_argument("--cutoffs", default=None, metavar="F1,F2,F3",
+                    help="P-value cutoffs instead of the workload's (1,1e-3,1 runs Viterbi on every target)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib", default=None,
@@ -98,25 +132,30 @@ def main():
     from synth import gen
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
-    w = gen.WORKLOADS[args.workload]
+    batched = args.workload == "C4"
+    w = gen.WORKLOADS["C3" if batched else args.workload]
+    F = tuple(float(v) for v in args.cutoffs.split(",")) if args.cutoffs else w.F
     t = time.perf_counter()
-    prof = gen.workload_profile(w)
-    db = gen.workload_database(w, prof=prof)
-    log(f"generated {w.name}: M={prof.M}, {db.n} targets, {db.residues.size} residues "
+    dbprof = gen.workload_profile(w)
+    profs = gen.c4_profiles() if batched else [dbprof]
+    db = gen.workload_database(w, prof=dbprof)
+    log(f"generated {args.workload}: {len(profs)} profile(s), M={[p.M for p in profs][:8]}"
+        f"{'...' if len(profs) > 8 else ''}, {db.n} targets, {db.residues.size} residues "
         f"in {time.perf_counter() - t:.1f}s")
     t = time.perf_counter()
     if args.calib:
-        calib = tuple(float(v) for v in args.calib.split(","))
+        assert not batched, "--calib gives one profile's calibration"
+        calibs = [tuple(float(v) for v in args.calib.split(","))]
     else:
-        calib = calibrate(prof)
-    log(f"calibration mu_msv={calib[0]!r} mu_vit={calib[1]!r} tau={calib[2]!r} "
-        f"({'given' if args.calib else 'on the GPU'}, {time.perf_counter() - t:.1f}s)")
-    P = hg.Profile(prof, *calib)
+        calibs = [calibrate(p) for p in profs]
+    log(f"calibration {'given' if args.calib else 'on the GPU'} ({time.perf_counter() - t:.1f}s): "
+        f"{calibs[0]!r}{' ...' if batched else ''}")
+    Ps = [hg.Profile(p, *c) for p, c in zip(profs, calibs)]
     t = time.perf_counter()
     D = hg.Database(db.residues, db.offsets)
     upload_s = time.perf_counter() - t
     log(f"database packed and uploaded in {upload_s:.2f}s (host buffers, PCIe included; not timed below)")
-    out = hg.alloc_results(D.n)
+    outs = [hg.alloc_results(D.n) for _ in Ps]
     stream = torch.cuda.current_stream()
     if args.copy_probe:
         src = torch.ones(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
@@ -126,35 +165,57 @@ def main():
         torch.cuda.synchronize()
         log(f"copy probe: {src.numel()} bytes read and written once")
         del src, dst
+
+    def step():
+        for P, out in zip(Ps, outs):
+            hg.search(P, D, F, out, stream=stream)
+
     for _ in range(args.warmup):
-        hg.search(P, D, w.F, out, stream=stream)
+        step()
     torch.cuda.synchronize()
-    hg.hmm_db_stage_timing(D.handle, args.steps)
+    hg.hmm_db_stage_timing(D.handle, args.steps * len(Ps))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        hg.search(P, D, w.F, out, stream=stream)
+        step()
     torch.cuda.synchronize()
     total = time.perf_counter() - t0
-    stages = hg.hmm_db_stage_times(D.handle, args.steps)
+    stages = hg.hmm_db_stage_times(D.handle, args.steps * len(Ps))
     hg.hmm_db_stage_timing(D.handle, 0)
     ms_step = total / args.steps * 1e3
-    cells = prof.M * D.n_residues
+    M_list = [p.M for p in profs]
+    cells = sum(M_list) * D.n_residues
     gcups = cells / (ms_step / 1e3) / 1e9
-    counts = out["counts"].cpu().numpy().tolist()
-    fl = out["flags"].cpu().numpy()
-    vit_cells = prof.M * int(np.diff(db.offsets)[(fl & hg.HMM_VIT_RAN) != 0].sum())
-    st_ms = stages.mean(axis=0) if stages.size else np.zeros(4)
+    lengths = np.diff(db.offsets)
+    counts = np.zeros(4, np.int64)
+    ran = {"viterbi": 0, "rescore": 0, "forward": 0}
+    for p, out in zip(profs, outs):
+        counts += out["counts"].cpu().numpy()
+        fl = out["flags"].cpu().numpy()
+        ran["viterbi"] += p.M * int(lengths[(fl & hg.HMM_VIT_RAN) != 0].sum())
+        ran["rescore"] += p.M * int(lengths[(fl & hg.HMM_VIT_OVF) != 0].sum())
+        ran["forward"] += p.M * int(lengths[(fl & hg.HMM_FWD_RAN) != 0].sum())
+    counts = counts.tolist()
+    # stage times summed over the profiles of one step
+    st_ms = [float(v) for v in
+             (stages.reshape(-1, len(Ps), 4).sum(axis=1).mean(axis=0) if stages.size else np.zeros(4))]
     msv_ms = float(st_ms[0])
     achieved = MSV_OPS_PER_CELL * cells / (msv_ms / 1e3) / 1e12
     log(f"{ms_step:.3f} ms/step, {gcups:.1f} GCUPS; stages ms: MSV {st_ms[0]:.3f} Viterbi {st_ms[1]:.3f} "
         f"rescore {st_ms[2]:.3f} (concurrent with) Forward {st_ms[3]:.3f}; counts {counts}")
     traffic = None
-    if os.path.exists(args.traffic):
+    if os.path.exists(args.traffic) and not batched and not args.cutoffs:
         with open(args.traffic) as f:
             tr = json.load(f)
         if tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha():
             traffic = tr.get("bytes_per_launch")
+    if batched:
+        wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
+              f"against {D.n} synthetic sequences ({D.n_residues} residues, the C3 database)")
+    else:
+        wl = (f"{w.name}: Plan7 profile M={profs[0].M} vs {D.n} synthetic sequences ({D.n_residues} residues, "
+              f"{w.planted * 100:g}% planted homologs)")
+    wl += f", MSV P<{F[0]:g} -> Viterbi P<{F[1]:g} -> Forward"
     rec = {
         "metric": "GCUPS (profile cols x DB residues /s), MSV+Viterbi+Forward, M=734 vs 1M seqs",
         "value": round(gcups, 2),
@@ -168,28 +229,32 @@ def main():
         "vs_baseline": None,
         "dtype": "u8/i16/i32/f32",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: Plan7 profile M={prof.M} vs {D.n} synthetic sequences "
-                               f"({D.n_residues} residues, {w.planted * 100:g}% planted homologs), "
-                               f"MSV P<{w.F[0]:g} -> Viterbi P<{w.F[1]:g} -> Forward",
-                   "M": prof.M, "n_seqs": D.n, "residues": D.n_residues, "cutoffs": list(w.F)},
+        "config": {"workload": wl, "M": M_list if batched else M_list[0], "n_seqs": D.n,
+                   "residues": D.n_residues, "cutoffs": list(F)},
         # rescore and Forward run concurrently after Viterbi: both are timed
         # from Viterbi's end, Forward until both are done
         "stage_ms": {"msv": round(float(st_ms[0]), 4), "viterbi": round(float(st_ms[1]), 4),
                      "rescore": round(float(st_ms[2]), 4), "forward_and_rescore": round(float(st_ms[3]), 4)},
         "survivors": {"msv_pass": counts[0], "vit_overflow": counts[1], "vit_pass": counts[2],
-                      "fwd_pass": counts[3], "viterbi_cells": vit_cells},
+                      "fwd_pass": counts[3], "viterbi_cells": ran["viterbi"], "rescore_cells": ran["rescore"],
+                      "forward_cells": ran["forward"]},
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
                      "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic,
-                     "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_launch": cells},
+                     "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_launch": cells // len(Ps)},
+        "stage_roofline": stage_roofline(M_list, D.n_residues, ran, st_ms),
         "upload_s": round(upload_s, 3),
+        "calib": list(calibs[0]),
     }
-    P.close()
+    if batched:
+        rec["queries_per_hour"] = round(len(Ps) / (ms_step / 1e3) * 3600.0, 1)
+    for P in Ps:
+        P.close()
     D.close()
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not batched:
         threads = min(16, len(os.sched_getaffinity(0)))
         log(f"CPU oracle baseline on {threads} threads ...")
-        rec["cpu_baseline"] = cpu_baseline(prof, db, w.F, args.cpu_seconds, threads)
+        rec["cpu_baseline"] = cpu_baseline(profs[0], db, F, args.cpu_seconds, threads)
         log(f"CPU oracle: {rec['cpu_baseline']['value']} GCUPS")
     print(json.dumps(rec), flush=True)
 
