@@ -87,6 +87,15 @@ def load(path: str):
         getattr(L, f).argtypes = [vp, vp, ip]
     L.orc_search.restype = ip
     L.orc_search.argtypes = [vp, vp, vp, C.c_int64, vp, vp, ip, ip, vp, vp, vp, vp, vp]
+    if hasattr(L, "orc_decode"):
+        L.orc_decode.restype = ip
+        L.orc_decode.argtypes = [vp, vp, ip, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_regions.restype = ip
+        L.orc_regions.argtypes = [vp, ip, dp, dp, vp, ip]
+        L.orc_oa_align.restype = dp
+        L.orc_oa_align.argtypes = [vp, ip, vp, vp, vp, ip, ip, vp, vp]
+        L.orc_oa_path_score.restype = dp
+        L.orc_oa_path_score.argtypes = [vp, ip, vp, vp, vp, ip, ip, vp, vp]
     return L
 
 
@@ -253,3 +262,72 @@ def search(p: OracleProfile, residues, offsets, calib, F, nthreads: int = 8,
     if rc != 0:
         raise ValueError("oracle search rejected its input")
     return out
+
+
+# ------------------------------------------------------------ posterior decoding
+
+RT1 = 0.25      # a region needs one residue with core posterior >= RT1 ...
+RT2 = 0.10      # ... and extends over the run of residues with core posterior >= RT2
+
+
+def decode(p: OracleProfile, x) -> dict:
+    """Forward/Backward posterior decoding of one target (fp64 log space).
+
+    tot = (Forward total, Backward total) in nats; per residue i (0-based
+    here, residue i+1 of the model's notation): core = P(emitted by a match
+    or insert state), njc[:, 0..2] = P(emitted by N, J, C), beg = P(B at row
+    i) (a domain starts at residue i+1), end = P(E at row i+1) (a domain ends
+    at residue i+1); pM, pI [L, M]: P(M_k / I_k emits residue i+1)."""
+    x = _seq(x)
+    L, M = x.size, p.M
+    out = dict(tot=np.zeros(2), core=np.zeros(L), njc=np.zeros((L, 3)), beg=np.zeros(L),
+               end=np.zeros(L), pM=np.zeros((L, M)), pI=np.zeros((L, M)))
+    rc = p.lib.orc_decode(p.h, _ptr(x), L, _ptr(out["tot"]), _ptr(out["core"]), _ptr(out["njc"]),
+                          _ptr(out["beg"]), _ptr(out["end"]), _ptr(out["pM"]), _ptr(out["pI"]))
+    if rc != 0:
+        raise MemoryError("oracle decode failed")
+    return out
+
+
+def regions(core, rt1: float = RT1, rt2: float = RT2, library=None) -> list:
+    """Domain regions: 1-based inclusive residue ranges (s, e)."""
+    c = np.ascontiguousarray(core, np.float64)
+    cap = max(1, c.size)
+    se = np.zeros(2 * cap, np.int32)
+    n = (lib() if library is None else library).orc_regions(_ptr(c), c.size, rt1, rt2, _ptr(se), cap)
+    return [(int(se[2 * r]), int(se[2 * r + 1])) for r in range(n)]
+
+
+def oa_align(p: OracleProfile, dec: dict, s: int, e: int) -> dict:
+    """Optimal-accuracy alignment of region [s, e] (1-based, inclusive)."""
+    L = dec["core"].size
+    code = np.zeros(e - s + 1, np.int16)
+    abk = np.zeros(4, np.int32)
+    sc = p.lib.orc_oa_align(p.h, L, _ptr(dec["core"]), _ptr(dec["pM"]), _ptr(dec["pI"]), s, e,
+                            _ptr(code), _ptr(abk))
+    return dict(score=float(sc), code=code, a=int(abk[0]), b=int(abk[1]), k1=int(abk[2]), k2=int(abk[3]))
+
+
+def oa_path_score(p: OracleProfile, dec: dict, s: int, e: int, code) -> tuple[float, bool]:
+    """(objective value, validity) of a given alignment of region [s, e]."""
+    L = dec["core"].size
+    c = np.ascontiguousarray(code, np.int16)
+    assert c.size == e - s + 1
+    valid = C.c_int(0)
+    sc = p.lib.orc_oa_path_score(p.h, L, _ptr(dec["core"]), _ptr(dec["pM"]), _ptr(dec["pI"]), s, e,
+                                 _ptr(c), C.byref(valid))
+    return float(sc), bool(valid.value)
+
+
+def domains(p: OracleProfile, x, rt1: float = RT1, rt2: float = RT2) -> tuple[dict, list]:
+    """Posterior decoding, regions and one optimal-accuracy alignment per
+    region.  Each domain: s, e (region), a, b (aligned residues), k1, k2
+    (model nodes), score (objective), nexp (expected domain ends in the
+    region), code (per residue of the region: +k M_k, -k I_k, 0 unaligned)."""
+    dec = decode(p, x)
+    out = []
+    for s, e in regions(dec["core"], rt1, rt2, p.lib):
+        d = oa_align(p, dec, s, e)
+        d.update(s=s, e=e, nexp=float(dec["end"][s - 1:e].sum()))
+        out.append(d)
+    return dec, out

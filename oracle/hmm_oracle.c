@@ -601,3 +601,351 @@ int orc_search(const orc_profile *p, const uint8_t *res, const int64_t *off, int
   free(th); free(thr8); free(thr16); free(fthr);
   return 0;
 }
+
+/* ---------------------------------------------------------------- posterior decoding
+ *
+ * The step after the filter cascade: for a target that passed it, the
+ * posterior probability of every state at every residue, from Forward and
+ * Backward in fp64 log space (readings, stated here):
+ *
+ *  Backward, row i = L..0 (a = x_{i+1}; values are log P(rest | state at i)):
+ *    bC(L) = MOVE;  bJ(L) = bN(L) = bB(L) = -inf
+ *    bB(i) = OP_k { ENTRY + msc_k(a) + bM_k(i+1) }                   (i < L)
+ *    bJ(i) = OP{ LOOP + bJ(i+1), MOVE + bB(i) };  bN likewise;  bC(i) = LOOP + bC(i+1)
+ *    bE(i) = OP{ EC + bC(i), EJ + bJ(i) }
+ *    bD_k(i) = OP{ bE(i), DM_k + msc_{k+1}(a) + bM_{k+1}(i+1), DD_k + bD_{k+1}(i) }
+ *    bM_k(i) = OP{ bE(i), MM_k + msc_{k+1}(a) + bM_{k+1}(i+1),
+ *                  MI_k + isc_k(a) + bI_k(i+1), MD_k + bD_{k+1}(i) }
+ *    bI_k(i) = OP{ IM_k + msc_{k+1}(a) + bM_{k+1}(i+1), II_k + isc_k(a) + bI_k(i+1) }
+ *    (terms through node k+1 or I_k exist for k < M only; row L has no
+ *    emitting successor).  bN(0) equals the Forward total.
+ *
+ *  Posteriors, Z = Forward total (residue i = 1..L):
+ *    P(M_k emits x_i) = exp(fM_k(i) + bM_k(i) - Z), I_k likewise;
+ *    core(i) = sum_k of both;
+ *    P(N emits x_i) = exp(fN(i) + bN(i) - Z)  (N occupied at row i >= 1);
+ *    P(J emits x_i) = exp(fJ(i-1) + LOOP + bJ(i) - Z), C likewise;
+ *    core + N + J + C = 1 at every residue;
+ *    begin(i) = P(B at row i) = exp(fB(i) + bB(i) - Z), i = 0..L-1 (a domain
+ *      starts at residue i+1);
+ *    end(i) = P(E at row i) = exp(fE(i) + bE(i) - Z), i = 1..L (a domain
+ *      ends at residue i).  Sum of begins = sum of ends = expected number of
+ *      domains.
+ */
+int orc_decode(const orc_profile *p, const uint8_t *x, int L, double *tot, double *pcore,
+               double *pnjc, double *pbeg, double *pend, double *pM, double *pI) {
+  int M = p->M;
+  if (L < 1) return -1;
+  const double loop = orc_loop(L), move = orc_move(L), half = log(0.5);
+  const size_t W = (size_t)M + 2;
+  double *fM = malloc(sizeof(double) * (L + 1) * W), *fI = malloc(sizeof(double) * (L + 1) * W);
+  double *sp = malloc(sizeof(double) * (L + 1) * 5);      /* fN fB fE fJ fC per row */
+  double *Dp = malloc(sizeof(double) * W), *Dc = malloc(sizeof(double) * W);
+  double *bMn = malloc(sizeof(double) * W), *bIn = malloc(sizeof(double) * W);
+  double *bMc = malloc(sizeof(double) * W), *bIc = malloc(sizeof(double) * W);
+  double *bDc = malloc(sizeof(double) * W);
+  if (!fM || !fI || !sp || !Dp || !Dc || !bMn || !bIn || !bMc || !bIc || !bDc) {
+    free(fM); free(fI); free(sp); free(Dp); free(Dc); free(bMn); free(bIn); free(bMc); free(bIc); free(bDc);
+    return -1;
+  }
+#define FN(i) sp[(i) * 5 + 0]
+#define FB(i) sp[(i) * 5 + 1]
+#define FE(i) sp[(i) * 5 + 2]
+#define FJ(i) sp[(i) * 5 + 3]
+#define FC(i) sp[(i) * 5 + 4]
+  for (size_t k = 0; k < W; k++) fM[k] = fI[k] = Dp[k] = -INFINITY;
+  FN(0) = 0.0; FB(0) = move; FE(0) = FJ(0) = FC(0) = -INFINITY;
+  for (int i = 1; i <= L; i++) {
+    const int a = x[i - 1];
+    double *Mp = fM + (size_t)(i - 1) * W, *Ip = fI + (size_t)(i - 1) * W;
+    double *Mc = fM + (size_t)i * W, *Ic = fI + (size_t)i * W;
+    Mc[0] = Ic[0] = Mc[M + 1] = Ic[M + 1] = -INFINITY;
+    for (int k = 1; k <= M; k++) {
+      double m = FB(i - 1) + p->entry;
+      if (k > 1) {
+        const double *t = p->tr + (k - 2) * 7;
+        m = lse(m, Mp[k - 1] + t[0]);
+        m = lse(m, Ip[k - 1] + t[3]);
+        m = lse(m, Dp[k - 1] + t[5]);
+      }
+      Mc[k] = m + p->msc[(k - 1) * KA + a];
+      if (k < M) {
+        const double *t = p->tr + (k - 1) * 7;
+        Ic[k] = p->isc[(k - 1) * KA + a] + lse(Mp[k] + t[1], Ip[k] + t[4]);
+      } else {
+        Ic[k] = -INFINITY;
+      }
+    }
+    Dc[1] = -INFINITY;
+    for (int k = 2; k <= M; k++) {
+      const double *t = p->tr + (k - 2) * 7;
+      Dc[k] = lse(Mc[k - 1] + t[2], Dc[k - 1] + t[6]);
+    }
+    double E = -INFINITY;
+    for (int k = 1; k <= M; k++) E = lse(lse(E, Mc[k]), Dc[k]);
+    FE(i) = E;
+    FJ(i) = lse(FJ(i - 1) + loop, E + half);
+    FC(i) = lse(FC(i - 1) + loop, E + half);
+    FN(i) = FN(i - 1) + loop;
+    FB(i) = lse(FN(i) + move, FJ(i) + move);
+    double *tmp = Dp; Dp = Dc; Dc = tmp;
+  }
+  const double Z = FC(L) + move;
+
+  /* Backward.  Row L first (no emitting successor), then rows L-1 .. 0. */
+  double bC = move, bJ = -INFINITY, bN = -INFINITY, bB = -INFINITY;
+  double bE = lse(half + bC, half + bJ);
+  for (size_t k = 0; k < W; k++) bMc[k] = bIc[k] = bDc[k] = -INFINITY;
+  for (int k = M; k >= 1; k--) {
+    double dnext = k < M ? p->tr[(k - 1) * 7 + 6] + bDc[k + 1] : -INFINITY;
+    double mdnext = k < M ? p->tr[(k - 1) * 7 + 2] + bDc[k + 1] : -INFINITY;
+    bDc[k] = lse(bE, dnext);
+    bMc[k] = lse(bE, mdnext);
+    bIc[k] = -INFINITY;
+  }
+  for (int i = L;; i--) {
+    /* posteriors of row i from the forward values and the backward row i */
+    if (i >= 1) {
+      const double *Mf = fM + (size_t)i * W, *If = fI + (size_t)i * W;
+      double core = 0.0;
+      for (int k = 1; k <= M; k++) {
+        double pm = exp(Mf[k] + bMc[k] - Z);
+        double pi = k < M ? exp(If[k] + bIc[k] - Z) : 0.0;
+        if (pM) pM[(size_t)(i - 1) * M + (k - 1)] = pm;
+        if (pI) pI[(size_t)(i - 1) * M + (k - 1)] = pi;
+        core += pm + pi;
+      }
+      if (pcore) pcore[i - 1] = core;
+      if (pnjc) {
+        pnjc[3 * (i - 1) + 0] = exp(FN(i) + bN - Z);
+        pnjc[3 * (i - 1) + 1] = exp(FJ(i - 1) + loop + bJ - Z);
+        pnjc[3 * (i - 1) + 2] = exp(FC(i - 1) + loop + bC - Z);
+      }
+      if (pend) pend[i - 1] = exp(FE(i) + bE - Z);
+    }
+    if (i < L && pbeg) pbeg[i] = exp(FB(i) + bB - Z);
+    if (i == 0) break;
+    /* backward row i-1 from row i; a = x_i (1-based), the residue row i emitted */
+    const int a = x[i - 1];
+    double *tmp;
+    tmp = bMn; bMn = bMc; bMc = tmp;
+    tmp = bIn; bIn = bIc; bIc = tmp;
+    double nB = -INFINITY;
+    for (int k = 1; k <= M; k++) nB = lse(nB, p->entry + p->msc[(k - 1) * KA + a] + bMn[k]);
+    bB = nB;
+    bJ = lse(loop + bJ, move + bB);
+    bN = lse(loop + bN, move + bB);
+    bC = loop + bC;
+    bE = lse(half + bC, half + bJ);
+    bDc[M + 1] = -INFINITY;
+    for (int k = M; k >= 1; k--) {
+      if (k < M) {
+        const double *t = p->tr + (k - 1) * 7;
+        const double mn = p->msc[k * KA + a] + bMn[k + 1];
+        const double in = p->isc[(k - 1) * KA + a] + bIn[k];
+        bDc[k] = lse(bE, lse(t[5] + mn, t[6] + bDc[k + 1]));
+        bMc[k] = lse(lse(bE, t[0] + mn), lse(t[1] + in, t[2] + bDc[k + 1]));
+        bIc[k] = lse(t[3] + mn, t[4] + in);
+      } else {
+        bDc[k] = bE;
+        bMc[k] = bE;
+        bIc[k] = -INFINITY;
+      }
+    }
+  }
+  if (tot) { tot[0] = Z; tot[1] = bN; }
+#undef FN
+#undef FB
+#undef FE
+#undef FJ
+#undef FC
+  free(fM); free(fI); free(sp); free(Dp); free(Dc); free(bMn); free(bIn); free(bMc); free(bIc); free(bDc);
+  return 0;
+}
+
+/*
+ * Domain regions (reading): maximal runs of residues whose core posterior
+ * is at least rt2, kept when some residue of the run reaches rt1.  Regions
+ * are written as 1-based inclusive residue ranges se[2r], se[2r+1] (at most
+ * cap of them); the return value is the number found.
+ */
+int orc_regions(const double *pcore, int L, double rt1, double rt2, int32_t *se, int cap) {
+  int n = 0;
+  for (int i = 0; i < L;) {
+    if (!(pcore[i] >= rt2)) { i++; continue; }
+    int j = i, hit = 0;
+    while (j < L && pcore[j] >= rt2) { if (pcore[j] >= rt1) hit = 1; j++; }
+    if (hit) {
+      if (n < cap) { se[2 * n] = i + 1; se[2 * n + 1] = j; }
+      n++;
+    }
+    i = j;
+  }
+  return n;
+}
+
+/*
+ * Optimal-accuracy alignment of one region [s, e] (1-based, inclusive):
+ * among single core paths B -> M_k1 ... M_k2 -> E that emit a contiguous
+ * residue range [a, b] inside the region (transitions of zero probability
+ * not allowed; the path starts and ends in a match state), maximise
+ *    sum_{i in [a,b]} P(state of i emits x_i) + sum_{i in region, outside [a,b]} (1 - core(i)),
+ * i.e. every residue earns the posterior of what the alignment says about
+ * it: aligned to M_k / I_k, or not aligned to the model.
+ * DP over rows i = s..e (G(i) = sum_{j=s}^{i} (1 - core(j))):
+ *    OM_k(i) = pM_k(i) + max{ G(i-1), OM_{k-1}(i-1) [MM], OI_{k-1}(i-1) [IM], OD_{k-1}(i-1) [DM] }
+ *    OI_k(i) = pI_k(i) + max{ OM_k(i-1) [MI], OI_k(i-1) [II] }          (k < M)
+ *    OD_k(i) = max{ OM_{k-1}(i) [MD], OD_{k-1}(i) [DD] }                 (k >= 2)
+ *    score = max_{i,k} OM_k(i) + G(e) - G(i)
+ * Ties: the first candidate in the orders written above wins, the end cell
+ * is the first maximum in row-major order.  Output code[i-s] for residues of
+ * the region: +k (M_k), -k (I_k), 0 (not aligned); abk = {a, b, k1, k2}.
+ * pM, pI: [L][M] posteriors of orc_decode.  Returns the score (or -inf if
+ * the region is empty or no alignment exists).
+ */
+double orc_oa_align(const orc_profile *p, int L, const double *pcore, const double *pM, const double *pI,
+                    int s, int e, int16_t *code, int32_t *abk) {
+  const int M = p->M;
+  if (s < 1 || e > L || s > e) return -INFINITY;
+  const int R = e - s + 1;
+  const size_t W = (size_t)M + 1;
+  double *OMp = malloc(sizeof(double) * W), *OIp = malloc(sizeof(double) * W), *ODp = malloc(sizeof(double) * W);
+  double *OMc = malloc(sizeof(double) * W), *OIc = malloc(sizeof(double) * W), *ODc = malloc(sizeof(double) * W);
+  uint8_t *tb = malloc((size_t)R * W * 3);    /* per cell: M, I, D predecessor */
+  double *G = malloc(sizeof(double) * (R + 1));
+  if (!OMp || !OIp || !ODp || !OMc || !OIc || !ODc || !tb || !G) {
+    free(OMp); free(OIp); free(ODp); free(OMc); free(OIc); free(ODc); free(tb); free(G);
+    return -INFINITY;
+  }
+  enum { FROM_B = 0, FROM_M = 1, FROM_I = 2, FROM_D = 3 };
+  G[0] = 0.0;
+  for (int r = 0; r < R; r++) G[r + 1] = G[r] + (1.0 - pcore[s - 1 + r]);
+  for (size_t k = 0; k < W; k++) OMp[k] = OIp[k] = ODp[k] = -INFINITY;
+  double best = -INFINITY;
+  int bi = -1, bk = -1;
+  for (int r = 0; r < R; r++) {
+    const int i = s + r;
+    const double *pm = pM + (size_t)(i - 1) * M, *pi = pI + (size_t)(i - 1) * M;
+    uint8_t *t = tb + (size_t)r * W * 3;
+    OMc[0] = OIc[0] = ODc[0] = -INFINITY;
+    for (int k = 1; k <= M; k++) {
+      double v = G[r];
+      int from = FROM_B;
+      if (k > 1 && r > 0) {
+        const double *tr = p->tr + (k - 2) * 7;
+        if (tr[0] > -INFINITY && OMp[k - 1] > v) { v = OMp[k - 1]; from = FROM_M; }
+        if (tr[3] > -INFINITY && OIp[k - 1] > v) { v = OIp[k - 1]; from = FROM_I; }
+        if (tr[5] > -INFINITY && ODp[k - 1] > v) { v = ODp[k - 1]; from = FROM_D; }
+      }
+      OMc[k] = pm[k - 1] + v;
+      t[3 * k + 0] = (uint8_t)from;
+      OIc[k] = -INFINITY;
+      t[3 * k + 1] = FROM_M;
+      if (k < M && r > 0) {
+        const double *tr = p->tr + (k - 1) * 7;
+        double u = -INFINITY;
+        int f = FROM_M;
+        if (tr[1] > -INFINITY && OMp[k] > u) { u = OMp[k]; f = FROM_M; }
+        if (tr[4] > -INFINITY && OIp[k] > u) { u = OIp[k]; f = FROM_I; }
+        if (u > -INFINITY) OIc[k] = pi[k - 1] + u;
+        t[3 * k + 1] = (uint8_t)f;
+      }
+    }
+    ODc[1] = -INFINITY;
+    t[3 * 1 + 2] = FROM_M;
+    for (int k = 2; k <= M; k++) {
+      const double *tr = p->tr + (k - 2) * 7;
+      double u = -INFINITY;
+      int f = FROM_M;
+      if (tr[2] > -INFINITY && OMc[k - 1] > u) { u = OMc[k - 1]; f = FROM_M; }
+      if (tr[6] > -INFINITY && ODc[k - 1] > u) { u = ODc[k - 1]; f = FROM_D; }
+      ODc[k] = u;
+      t[3 * k + 2] = (uint8_t)f;
+    }
+    for (int k = 1; k <= M; k++) {
+      double sc = OMc[k] + (G[R] - G[r + 1]);
+      if (sc > best) { best = sc; bi = r; bk = k; }
+    }
+    double *tmp;
+    tmp = OMp; OMp = OMc; OMc = tmp;
+    tmp = OIp; OIp = OIc; OIc = tmp;
+    tmp = ODp; ODp = ODc; ODc = tmp;
+  }
+  if (bi >= 0) {
+    for (int r = 0; r < R; r++) code[r] = 0;
+    int r = bi, k = bk, st = FROM_M;
+    abk[1] = s + bi;
+    abk[3] = bk;
+    for (;;) {
+      const uint8_t *t = tb + (size_t)r * W * 3;
+      if (st == FROM_M) {
+        code[r] = (int16_t)k;
+        const int f = t[3 * k + 0];
+        if (f == FROM_B) { abk[0] = s + r; abk[2] = k; break; }
+        r--; k--; st = f;
+      } else if (st == FROM_I) {
+        code[r] = (int16_t)(-k);
+        const int f = t[3 * k + 1];
+        r--; st = f;
+      } else {  /* D_k, same row: predecessor M_{k-1} or D_{k-1} */
+        const int f = t[3 * k + 2];
+        k--; st = f;
+      }
+    }
+  }
+  free(OMp); free(OIp); free(ODp); free(OMc); free(OIc); free(ODc); free(tb); free(G);
+  return best;
+}
+
+/*
+ * Score of a given alignment of region [s, e] under the objective of
+ * orc_oa_align, and whether it is a valid path: codes 0 outside one
+ * contiguous aligned range [a, b], which starts and ends in a match state;
+ * consecutive aligned residues follow M_k -> M_{k+1} (MM), M_k -> I_k (MI),
+ * I_k -> I_k (II), I_k -> M_{k+1} (IM), or M_k -> D_{k+1} .. D_{k'-1} ->
+ * M_{k'} (MD, DD.., DM), each transition of non-zero probability.
+ * *valid receives 1 or 0.
+ */
+double orc_oa_path_score(const orc_profile *p, int L, const double *pcore, const double *pM, const double *pI,
+                         int s, int e, const int16_t *code, int *valid) {
+  const int M = p->M;
+  *valid = 0;
+  if (s < 1 || e > L || s > e) return -INFINITY;
+  const int R = e - s + 1;
+  int a = -1, b = -1;
+  for (int r = 0; r < R; r++)
+    if (code[r] != 0) { if (a < 0) a = r; b = r; }
+  if (a < 0) return -INFINITY;
+  double sc = 0.0;
+  for (int r = 0; r < R; r++) {
+    const int i = s + r, c = code[r];
+    if (r < a || r > b) { sc += 1.0 - pcore[i - 1]; continue; }
+    if (c == 0 || c > M || c < -(M - 1)) return -INFINITY;
+    sc += c > 0 ? pM[(size_t)(i - 1) * M + (c - 1)] : pI[(size_t)(i - 1) * M + (-c - 1)];
+  }
+  if (code[a] <= 0 || code[b] <= 0) return -INFINITY;
+  for (int r = a; r < b; r++) {
+    const int c0 = code[r], c1 = code[r + 1];
+    if (c0 > 0 && c1 > 0) {            /* M_k -> M_k' */
+      const int k = c0, k2 = c1;
+      if (k2 <= k) return -INFINITY;
+      const double *t = p->tr + (k - 1) * 7;
+      if (k2 == k + 1) {
+        if (t[0] == -INFINITY) return -INFINITY;
+      } else {
+        if (t[2] == -INFINITY) return -INFINITY;                          /* M_k -> D_{k+1} */
+        for (int j = k + 1; j < k2 - 1; j++)
+          if (p->tr[(j - 1) * 7 + 6] == -INFINITY) return -INFINITY;     /* D_j -> D_{j+1} */
+        if (p->tr[(k2 - 2) * 7 + 5] == -INFINITY) return -INFINITY;      /* D_{k2-1} -> M_k2 */
+      }
+    } else if (c0 > 0 && c1 < 0) {     /* M_k -> I_k */
+      if (-c1 != c0 || p->tr[(c0 - 1) * 7 + 1] == -INFINITY) return -INFINITY;
+    } else if (c0 < 0 && c1 < 0) {     /* I_k -> I_k */
+      if (c1 != c0 || p->tr[(-c0 - 1) * 7 + 4] == -INFINITY) return -INFINITY;
+    } else {                           /* I_k -> M_{k+1} */
+      if (c1 != -c0 + 1 || p->tr[(-c0 - 1) * 7 + 3] == -INFINITY) return -INFINITY;
+    }
+  }
+  *valid = 1;
+  return sc;
+}

@@ -160,3 +160,138 @@ def msv_parses(sc8, x, M: int, base8: int, move8: int, entry8: int, exit8: int) 
             extend(r1, v - move8)
     extend(0, base8 - move8)
     return best
+
+
+# ------------------------------------------------------------ annotated paths
+
+def all_paths(S: Scores, x) -> list:
+    """Every Plan7 path as (score, emit, begins, ends): emit[i] names the
+    state that emitted residue i+1 (("M", k), ("I", k), ("N",), ("J",),
+    ("C",)); begins / ends are the rows at which the path visits B / E.
+    Written from the same grammar as all_path_scores, with bookkeeping."""
+    L = len(x)
+    M = S.M
+    out = []
+
+    def at_N(i, s, em, bg, en):
+        if i < L:
+            at_N(i + 1, s + S.loop, em + (("N",),), bg, en)
+        at_B(i, s + S.move, em, bg, en)
+
+    def at_B(i, s, em, bg, en):
+        if i < L:
+            for k in range(1, M + 1):
+                at_M(k, i + 1, s + S.entry + S.msc(k, x[i]), em + (("M", k),), bg + (i,), en)
+
+    def at_M(k, i, s, em, bg, en):
+        at_E(i, s, em, bg, en)
+        if k < M:
+            if i < L:
+                at_M(k + 1, i + 1, s + S.t(k, "MM") + S.msc(k + 1, x[i]), em + (("M", k + 1),), bg, en)
+                at_I(k, i + 1, s + S.t(k, "MI") + S.isc(k, x[i]), em + (("I", k),), bg, en)
+            at_D(k + 1, i, s + S.t(k, "MD"), em, bg, en)
+
+    def at_I(k, i, s, em, bg, en):
+        if i < L:
+            at_I(k, i + 1, s + S.t(k, "II") + S.isc(k, x[i]), em + (("I", k),), bg, en)
+            at_M(k + 1, i + 1, s + S.t(k, "IM") + S.msc(k + 1, x[i]), em + (("M", k + 1),), bg, en)
+
+    def at_D(k, i, s, em, bg, en):
+        at_E(i, s, em, bg, en)
+        if k < M:
+            if i < L:
+                at_M(k + 1, i + 1, s + S.t(k, "DM") + S.msc(k + 1, x[i]), em + (("M", k + 1),), bg, en)
+            at_D(k + 1, i, s + S.t(k, "DD"), em, bg, en)
+
+    def at_E(i, s, em, bg, en):
+        at_J(i, s + S.ej, em, bg, en + (i,))
+        at_C(i, s + S.ec, em, bg, en + (i,))
+
+    def at_J(i, s, em, bg, en):
+        if i < L:
+            at_J(i + 1, s + S.loop, em + (("J",),), bg, en)
+        at_B(i, s + S.move, em, bg, en)
+
+    def at_C(i, s, em, bg, en):
+        if i < L:
+            at_C(i + 1, s + S.loop, em + (("C",),), bg, en)
+        else:
+            out.append((s + S.move, em, bg, en))
+
+    at_N(0, 0, (), (), ())
+    return out
+
+
+def posteriors(S: Scores, x) -> dict:
+    """Posterior probabilities by weighting every path with exp(score):
+    core / njc / pM / pI per residue, beg[i] = P(B at row i), i = 0..L-1,
+    end[i] = P(E at row i+1)."""
+    L, M = len(x), S.M
+    paths = all_paths(S, x)
+    top = max(p[0] for p in paths)
+    w = [math.exp(p[0] - top) for p in paths]
+    Z = sum(w)
+    out = dict(core=[0.0] * L, njc=[[0.0] * 3 for _ in range(L)], beg=[0.0] * L, end=[0.0] * L,
+               pM=[[0.0] * M for _ in range(L)], pI=[[0.0] * M for _ in range(L)],
+               tot=top + math.log(Z))
+    for (sc, em, bg, en), wi in zip(paths, w):
+        f = wi / Z
+        for i, st in enumerate(em):
+            if st[0] == "M":
+                out["pM"][i][st[1] - 1] += f
+                out["core"][i] += f
+            elif st[0] == "I":
+                out["pI"][i][st[1] - 1] += f
+                out["core"][i] += f
+            else:
+                out["njc"][i]["NJC".index(st[0])] += f
+        for r in bg:
+            out["beg"][r] += f
+        for r in en:
+            out["end"][r - 1] += f
+    return out
+
+
+def oa_best(M: int, allowed, core, pM, pI, s: int, e: int) -> float:
+    """Best value of the optimal-accuracy objective over every alignment of
+    region [s, e] (1-based), enumerated: a contiguous aligned range [a, b],
+    a core walk that starts in M_k1 at residue a and ends in M_k2 at residue
+    b, moving M->M (next node, next residue), M->I / I->I (same node, next
+    residue), I->M (next node, next residue) or M->D..D->M (skipping nodes,
+    next residue), using only allowed(k, name) transitions.  Residues of the
+    region outside [a, b] earn 1 - core."""
+    best = -math.inf
+    flank = [1.0 - core[i - 1] for i in range(1, len(core) + 1)]
+
+    def walk(state, k, i, b, acc):
+        # state emitted residue i; acc includes it
+        nonlocal best
+        if i == b:
+            if state == "M":
+                best = max(best, acc + sum(flank[j - 1] for j in range(b + 1, e + 1)))
+            return
+        if state == "M":
+            if k < M and allowed(k, "MM"):
+                walk("M", k + 1, i + 1, b, acc + pM[i][k])
+            if k < M and allowed(k, "MI"):
+                walk("I", k, i + 1, b, acc + pI[i][k - 1])
+            if k < M and allowed(k, "MD"):
+                j = k + 1                      # in D_j
+                while j < M:
+                    if allowed(j, "DM"):
+                        walk("M", j + 1, i + 1, b, acc + pM[i][j])
+                    if not allowed(j, "DD"):
+                        break
+                    j += 1
+        else:
+            if allowed(k, "II"):
+                walk("I", k, i + 1, b, acc + pI[i][k - 1])
+            if allowed(k, "IM"):
+                walk("M", k + 1, i + 1, b, acc + pM[i][k])
+
+    for a in range(s, e + 1):
+        pre = sum(flank[j - 1] for j in range(s, a))
+        for b in range(a, e + 1):
+            for k1 in range(1, M + 1):
+                walk("M", k1, a, b, pre + pM[a - 1][k1 - 1])
+    return best

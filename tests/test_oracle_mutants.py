@@ -16,6 +16,7 @@ from test_oracle_brute import delete_favoring_case, model_sequence
 import oracle
 from conftest import random_profile
 from test_oracle_closed_forms import _exact_odds_profile, _peaked_profile
+from test_oracle_decode import _allowed, _zero_transition_profile, forbidden_skip_case
 
 MUTANTS = {
     "im_uses_mm_transition": ("m = imax(m, ADD(Ip[k - 1], t[3]));", "m = imax(m, ADD(Ip[k - 1], t[0]));"),
@@ -36,6 +37,23 @@ MUTANTS = {
     "vit_transposed_mi_ii": ("int v = imax(ADD(Mp[k], t[1]), ADD(Ip[k], t[4]));",
                              "int v = imax(ADD(Mp[k], t[4]), ADD(Ip[k], t[1]));"),
     "msv_cost_wrong_node": ("p->cost8[(k - 1) * KA + a]", "p->cost8[(k > 1 ? k - 2 : 0) * KA + a]"),
+    # posterior decoding, regions and alignment
+    "bwd_match_drops_exit": ("bMc[k] = lse(lse(bE, t[0] + mn), lse(t[1] + in, t[2] + bDc[k + 1]));",
+                             "bMc[k] = lse(t[0] + mn, lse(t[1] + in, t[2] + bDc[k + 1]));"),
+    "bwd_insert_scores_match_emission": ("const double in = p->isc[(k - 1) * KA + a] + bIn[k];",
+                                         "const double in = p->msc[(k - 1) * KA + a] + bIn[k];"),
+    "bwd_delete_chain_skips_dd": ("bDc[k] = lse(bE, lse(t[5] + mn, t[6] + bDc[k + 1]));",
+                                  "bDc[k] = lse(bE, t[5] + mn);"),
+    "bwd_begin_without_emission": ("nB = lse(nB, p->entry + p->msc[(k - 1) * KA + a] + bMn[k]);",
+                                   "nB = lse(nB, p->entry + bMn[k]);"),
+    "post_j_emission_without_loop": ("pnjc[3 * (i - 1) + 1] = exp(FJ(i - 1) + loop + bJ - Z);",
+                                     "pnjc[3 * (i - 1) + 1] = exp(FJ(i) + bJ - Z);"),
+    "oa_flank_earns_core": ("G[r + 1] = G[r] + (1.0 - pcore[s - 1 + r]);", "G[r + 1] = G[r] + pcore[s - 1 + r];"),
+    "oa_ignores_zero_dd": ("if (tr[6] > -INFINITY && ODc[k - 1] > u)", "if (ODc[k - 1] > u)"),
+    "regions_strict_rt2": ("if (!(pcore[i] >= rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
+                           "    while (j < L && pcore[j] >= rt2)",
+                           "if (!(pcore[i] > rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
+                           "    while (j < L && pcore[j] > rt2)"),
 }
 
 
@@ -82,6 +100,29 @@ def _battery(lib) -> list:
     lp = oracle.length_params(2, lib)
     best = brute.viterbi(brute.int_scores(op.tables(), 3, sc["entry16"], lp["move16"], sc["ej16"]), x)
     check("vit_delete_path", oracle.vit32(op, x) == best and oracle.vit16(op, x) == (best, 0))
+    # posterior decoding and optimal-accuracy alignment against enumeration
+    for M, L, seed, zero in [(2, 3, 0, False), (3, 3, 1, False), (3, 4, 2, False), (3, 4, 0, True),
+                             (3, 3, 1, True), (3, 4, 2, True), (2, 4, 3, True)]:
+        prof = _zero_transition_profile(M, seed) if zero else random_profile(M, seed, alpha=0.1, talpha=0.3)
+        op = oracle.OracleProfile(prof, lib)
+        x = model_sequence(prof, L, 3000 + seed) if seed % 2 else \
+            np.random.default_rng(1000 + seed).integers(0, 20, size=L).astype(np.uint8)
+        d = oracle.decode(op, x)
+        bp = brute.posteriors(brute.float_scores(prof, L), x)
+        for key in ("core", "njc", "beg", "end", "pM", "pI"):
+            check("post_" + key, np.allclose(d[key], np.array(bp[key]), rtol=0, atol=1e-9))
+        for s in range(1, L + 1):
+            for e in range(s, L + 1):
+                want = brute.oa_best(M, _allowed(prof), bp["core"], bp["pM"], bp["pI"], s, e)
+                check("oa", math.isclose(oracle.oa_align(op, d, s, e)["score"], want, abs_tol=1e-9))
+    prof, x = forbidden_skip_case()
+    op = oracle.OracleProfile(prof, lib)
+    d = oracle.decode(op, x)
+    bp = brute.posteriors(brute.float_scores(prof, 2), x)
+    want = brute.oa_best(4, _allowed(prof), bp["core"], bp["pM"], bp["pI"], 1, 2)
+    check("oa_forbidden_skip", math.isclose(oracle.oa_align(op, d, 1, 2)["score"], want, abs_tol=1e-9))
+    core = np.array([0.05, 0.10, 0.2, 0.25, 0.099, 0.3, 0.24, 0.11, 0.09, 0.12, 0.2, 0.1, 0.5, 0.1])
+    check("regions", oracle.regions(core, 0.25, 0.10, lib) == [(2, 4), (6, 8), (10, 14)])
     return fails
 
 
