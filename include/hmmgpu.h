@@ -155,6 +155,74 @@ int hmm_db_free(hmm_db *db);
 int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t,
                const hmm_results *out, hmm_stream stream);
 
+/* ---------------------------------------------------------------- decoding
+ *
+ * The step after the filter cascade: for the targets that passed it, the
+ * posterior probability that each residue is emitted by the profile's core
+ * (match or insert) states, the regions of each target that hold a domain,
+ * and one alignment of the profile to each region -- the row that a hit
+ * contributes to the multiple sequence alignment, which is what the
+ * paper's MSA-construction stage (Background section) builds from its
+ * jackhmmer searches.  Definitions (fp64 statements; the GPU computes in
+ * fp32):
+ *   - Forward and Backward over the local multihit model above give, for
+ *     every residue i, P(M_k emits x_i), P(I_k emits x_i), and the core
+ *     posterior core(i) = sum_k of both; end(i) = P(a domain ends at i);
+ *   - a region is a maximal run of residues with core >= HMM_RT2 that
+ *     holds at least one residue with core >= HMM_RT1;
+ *   - in each region [s, e] the alignment is the single core path
+ *     B -> M_k1 ... M_k2 -> E over residues a..b (s <= a <= b <= e; zero-
+ *     probability transitions excluded) that maximises
+ *       sum_{i=a}^{b} P(its state emits x_i) + sum_{i in [s,e] \ [a,b]} (1 - core(i)),
+ *     the expected number of residues of the region it labels correctly. */
+#define HMM_RT1 0.25f     /* a region needs one residue with core posterior >= HMM_RT1 ... */
+#define HMM_RT2 0.10f     /* ... and spans a run of residues with core posterior >= HMM_RT2 */
+
+/* One region of a decoded target and its alignment (1-based residues). */
+typedef struct {
+  int32_t target;   /* caller index of the target */
+  int32_t s, e;     /* region: residues s..e */
+  int32_t a, b;     /* aligned residues a..b */
+  int32_t k1, k2;   /* first and last match node of the alignment */
+  float score;      /* the maximised objective above */
+  float nexp;       /* expected number of domain ends inside the region: sum of end(i), i = s..e */
+} hmm_domain;
+
+/* Caller-owned DEVICE outputs of hmm_decode.
+ *   dom       [max_dom] domain records, in no particular order
+ *   n_dom     int32[1]: number of regions found (records beyond max_dom are
+ *             counted but not written)
+ *   exp_dom   [n_seqs] caller order, or NULL: expected number of domains
+ *             (sum of end(i) over the target) of each decoded target;
+ *             other entries are left untouched
+ *   pp        [n_residues] float, laid out like the caller's residue
+ *             array, or NULL: core(i) of every residue of a decoded target
+ *   aln       [n_residues] int16, laid out like the caller's residue array,
+ *             or NULL: for every residue of a decoded target, +k if its
+ *             region's alignment puts it on M_k, -k on I_k, 0 otherwise. */
+typedef struct {
+  hmm_domain *dom;
+  int32_t max_dom;
+  int32_t *n_dom;
+  float *exp_dom;
+  float *pp;
+  int16_t *aln;
+} hmm_decode_out;
+
+/* Posterior decoding, domain regions and alignments of the targets whose
+ * flags (device uint8[n_seqs], caller order; e.g. the flags a search wrote)
+ * contain every bit of `mask`; flags = NULL decodes every target.  The
+ * profile must be the one the flags came from.  Enqueued on `stream`;
+ * serialised with the searches on `db`.  On its first call for a database
+ * (and when a longer profile needs more) the library allocates a scratch
+ * area on the device for the Forward/Backward matrices of the targets in
+ * flight -- one slot per resident wave, at most 16 GiB -- which the
+ * database keeps until hmm_db_free.  Errors: HMM_EINVAL (NULL profile, db
+ * or out; NULL dom or n_dom; max_dom < 0), HMM_ENOMEM (scratch),
+ * HMM_EDEVICE. */
+int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask,
+               const hmm_decode_out *out, hmm_stream stream);
+
 /* Profiling hook: record HIP events around each stage of the next searches
  * on this database, in a ring of `capacity` searches (0 turns it off).  The
  * events are recorded on the search stream, so they bracket exactly that

@@ -24,8 +24,10 @@ HMM_MAX_LEN = 100000
 HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, HMM_FWD_PASS = (
     0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40)
 
+HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float32 in the library)
+
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
-            "hmm_debug_length_params", "hmm_debug_tables", "hmm_last_error", "hmm_profile_free",
+            "hmm_debug_length_params", "hmm_debug_tables", "hmm_decode", "hmm_last_error", "hmm_profile_free",
             "hmm_profile_upload", "hmm_search", "hmm_strerror")
 
 
@@ -49,6 +51,14 @@ class hmm_results(C.Structure):
                 ("counts", C.c_void_p)]
 
 
+class hmm_decode_out(C.Structure):
+    _fields_ = [("dom", C.c_void_p), ("max_dom", C.c_int32), ("n_dom", C.c_void_p), ("exp_dom", C.c_void_p),
+                ("pp", C.c_void_p), ("aln", C.c_void_p)]
+
+
+# hmm_domain: 9 x 4 bytes (target, s, e, a, b, k1, k2 as int32; score, nexp as float32)
+DOMAIN_FIELDS = ("target", "s", "e", "a", "b", "k1", "k2", "score", "nexp")
+
 _lib = None
 
 
@@ -71,6 +81,8 @@ def lib():
         L.hmm_db_free.argtypes = [vp]
         L.hmm_search.restype = C.c_int
         L.hmm_search.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), vp]
+        L.hmm_decode.restype = C.c_int
+        L.hmm_decode.argtypes = [vp, vp, vp, C.c_uint8, C.POINTER(hmm_decode_out), vp]
         L.hmm_db_info.restype = C.c_int
         L.hmm_db_info.argtypes = [vp, C.POINTER(i64), C.POINTER(i64), C.POINTER(i32)]
         L.hmm_db_stage_timing.restype = C.c_int
@@ -174,6 +186,20 @@ def hmm_search(profile: int, db: int, F, out: dict, stream=None) -> None:
            "hmm_search")
 
 
+def hmm_decode(profile: int, db: int, flags, mask: int, out: dict, stream=None) -> None:
+    """Enqueue posterior decoding.  `flags`: device uint8 tensor (caller
+    order) or None (decode every target); `out` maps dom (int32 [max_dom, 9])
+    and n_dom (int32 [1]) and optionally exp_dom / pp / aln to device
+    tensors."""
+    def ptr(k):
+        v = out.get(k)
+        return v.data_ptr() if v is not None else None
+    o = hmm_decode_out(ptr("dom"), int(out["dom"].shape[0]), ptr("n_dom"), ptr("exp_dom"), ptr("pp"), ptr("aln"))
+    fp = C.c_void_p(flags.data_ptr()) if flags is not None else C.c_void_p(0)
+    _check(lib().hmm_decode(C.c_void_p(profile), C.c_void_p(db), fp, int(mask) & 0xff, C.byref(o),
+                            _stream_handle(stream)), "hmm_decode")
+
+
 def _desc(prof, mu_msv=0.0, mu_vit=0.0, tau=0.0):
     M = int(prof.M)
     keep = [np.ascontiguousarray(a, dtype=np.float64) for a in (prof.bg, prof.match, prof.insert, prof.trans)]
@@ -265,3 +291,43 @@ def search(profile: Profile, db: Database, F, out: dict | None = None, stream=No
         stream = torch.cuda.current_stream()
     hmm_search(profile.handle, db.handle, F, out, stream)
     return out
+
+
+def decode(profile: Profile, db: Database, flags=None, mask: int = HMM_FWD_PASS, max_dom: int | None = None,
+           pp: bool = False, aln: bool = False, stream=None) -> dict:
+    """Posterior decoding of the targets whose flags hold `mask` (all targets
+    when flags is None) on the current torch stream (or `stream`).  Returns
+    device tensors: dom int32 [max_dom, 9] (fields DOMAIN_FIELDS; score and
+    nexp are float32 bit patterns), n_dom int32 [1], exp_dom float32 [n]
+    (NaN where not decoded), and pp float32 / aln int16 [n_residues] when
+    asked for (caller residue layout)."""
+    import torch
+    if max_dom is None:
+        max_dom = max(16, 4 * db.n)
+    dev = "cuda"
+    out = dict(dom=torch.zeros((max_dom, 9), dtype=torch.int32, device=dev),
+               n_dom=torch.zeros(1, dtype=torch.int32, device=dev),
+               exp_dom=torch.full((db.n,), float("nan"), dtype=torch.float32, device=dev))
+    if pp:
+        out["pp"] = torch.full((db.n_residues,), float("nan"), dtype=torch.float32, device=dev)
+    if aln:
+        out["aln"] = torch.full((db.n_residues,), -32768, dtype=torch.int16, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    hmm_decode(profile.handle, db.handle, flags, mask, out, stream)
+    return out
+
+
+def domains_table(out: dict) -> list:
+    """Host list of domain dicts from decode()'s outputs (after the stream
+    synchronises), sorted by (target, s)."""
+    n = int(out["n_dom"].cpu()[0])
+    raw = out["dom"][:min(n, out["dom"].shape[0])].cpu().numpy()
+    recs = []
+    for row in raw:
+        d = {k: int(v) for k, v in zip(DOMAIN_FIELDS[:7], row[:7])}
+        d["score"] = float(row[7:8].view(np.float32)[0])
+        d["nexp"] = float(row[8:9].view(np.float32)[0])
+        recs.append(d)
+    recs.sort(key=lambda d: (d["target"], d["s"]))
+    return recs

@@ -1,0 +1,751 @@
+// HIP kernels (gfx950) of posterior decoding: for every selected target,
+// Forward with every row kept, Backward with the posterior probability of
+// each state at each residue, the target's domain regions, and one
+// optimal-accuracy alignment per region (the hit's row of the multiple
+// sequence alignment).
+//
+// One wavefront decodes one target at a time in a private scratch slot
+// (one slot per resident wave; the launch has exactly one wave per slot):
+//   1. Forward in fp32 probability space, as in the search's Forward
+//      kernel, storing M_k(i) and I_k(i) of every row and the row's special
+//      values (N, J-loop, C-loop and E parts).
+//   2. Backward from row L down to row 1.  The backward delete chain runs
+//      from cell k+1 to cell k, so this phase puts virtual lane v = 63 - l
+//      on physical lane l: the chain then crosses lanes in the same
+//      direction as the forward one (lane l-1 -> l) and reuses its DPP
+//      prefix scan.  Each row's posteriors are normalised by that row's
+//      total, sum over the states that can emit residue i
+//         Z_i = sum_k (fM bM + fI bI) + fN bN + fJl bJ + fCl bC,
+//      which is the same value P(x) in the row's scale, so no scale factor
+//      has to be tracked.  The posteriors overwrite the stored forward row.
+//   3. Regions from the core posteriors (ballots over 64 residues), then per
+//      region the optimal-accuracy recurrence in max-plus form, with a
+//      4-bit traceback code per cell, and the traceback.
+// Values are kept inside [2^-32, 2^32] by exact power-of-two rescaling in
+// both directions, so a product of a forward and a backward value stays far
+// from the fp32 range limits.
+//
+// Lane-divergent branches appear only around stores (predicated writes of
+// one lane's value); every cross-lane operation runs with all lanes active.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+
+#include "hmm_device.h"
+#include "hmm_internal.h"
+
+namespace hmmgpu {
+namespace {
+
+constexpr float kNegInf = -__builtin_inff();
+constexpr float kWinHi = 0x1p32f, kWinLo = 0x1p-32f;
+
+// Lane l receives lane l-1's value; lane 0 receives `fill`.
+__device__ __forceinline__ float lane_up_fill(float v, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, v), 0x138, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float wave_max_f(float v) {
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+  return __builtin_bit_cast(float, uni(__builtin_bit_cast(int, v)));
+}
+
+__device__ __forceinline__ int wave_min_i32(int v) {
+  for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off));
+  return uni(v);
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Memory written by other lanes of this wave becomes visible to its loads.
+__device__ __forceinline__ void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup"); }
+
+// Inclusive prefix scan across lanes (lane l-1 -> l) of the affine maps
+// x -> a + P x, with the P parts before each step precomputed (see pstep).
+__device__ __forceinline__ float affine_scan(float a, const float (&ps)[6]) {
+  a = fmaf(ps[0], dpp_f<kRowShr1, 0xf>(a, 0.0f), a);
+  a = fmaf(ps[1], dpp_f<kRowShr2, 0xf>(a, 0.0f), a);
+  a = fmaf(ps[2], dpp_f<kRowShr4, 0xf>(a, 0.0f), a);
+  a = fmaf(ps[3], dpp_f<kRowShr8, 0xf>(a, 0.0f), a);
+  a = fmaf(ps[4], dpp_f<kRowBcast15, 0xa>(a, 0.0f), a);
+  a = fmaf(ps[5], dpp_f<kRowBcast31, 0xc>(a, 0.0f), a);
+  return a;
+}
+// The P parts of affine_scan for a lane's own P.
+__device__ __forceinline__ void affine_steps(float p, float (&ps)[6]) {
+  ps[0] = p;
+  p = p * dpp_f<kRowShr1, 0xf>(p, 1.0f);
+  ps[1] = p;
+  p = p * dpp_f<kRowShr2, 0xf>(p, 1.0f);
+  ps[2] = p;
+  p = p * dpp_f<kRowShr4, 0xf>(p, 1.0f);
+  ps[3] = p;
+  p = p * dpp_f<kRowShr8, 0xf>(p, 1.0f);
+  ps[4] = p;
+  p = p * dpp_f<kRowBcast15, 0xa>(p, 1.0f);
+  ps[5] = p;
+}
+// The same scan in max-plus form: maps x -> max(a, x + b), b in {0, -inf}.
+__device__ __forceinline__ float maxplus_scan(float a, const float (&bs)[6]) {
+  a = fmaxf(a, dpp_f<kRowShr1, 0xf>(a, kNegInf) + bs[0]);
+  a = fmaxf(a, dpp_f<kRowShr2, 0xf>(a, kNegInf) + bs[1]);
+  a = fmaxf(a, dpp_f<kRowShr4, 0xf>(a, kNegInf) + bs[2]);
+  a = fmaxf(a, dpp_f<kRowShr8, 0xf>(a, kNegInf) + bs[3]);
+  a = fmaxf(a, dpp_f<kRowBcast15, 0xa>(a, kNegInf) + bs[4]);
+  a = fmaxf(a, dpp_f<kRowBcast31, 0xc>(a, kNegInf) + bs[5]);
+  return a;
+}
+__device__ __forceinline__ void maxplus_steps(float b, float (&bs)[6]) {
+  bs[0] = b;
+  b = b + dpp_f<kRowShr1, 0xf>(b, 0.0f);
+  bs[1] = b;
+  b = b + dpp_f<kRowShr2, 0xf>(b, 0.0f);
+  bs[2] = b;
+  b = b + dpp_f<kRowShr4, 0xf>(b, 0.0f);
+  bs[3] = b;
+  b = b + dpp_f<kRowShr8, 0xf>(b, 0.0f);
+  bs[4] = b;
+  b = b + dpp_f<kRowBcast15, 0xa>(b, 0.0f);
+  bs[5] = b;
+}
+
+// Gate of a transition in the alignment recurrence: 0 if allowed, -inf if
+// its probability is zero.
+__device__ __forceinline__ float gate(float p) { return p > 0.0f ? 0.0f : kNegInf; }
+
+constexpr int kDecThreads = 256;
+
+template <int Q, bool EMIT_LDS, bool TR_LDS>
+__global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb db, DevDecode d) {
+  extern __shared__ float ldsd[];
+  constexpr int kEmit = kAlpha * 2 * Q * kWave;
+  constexpr int kTr = (TR_N + 2) * Q * kWave;
+  constexpr int kRowF = 2 * Q * kWave;   // floats of one stored row
+  constexpr int NB = (Q + 7) / 8;        // traceback dwords per lane per row
+  constexpr int kR = TR_LDS ? 1 : Q;     // register copies of a transition plane
+  if (EMIT_LDS || TR_LDS) {
+    if (EMIT_LDS)
+      for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsd)[i] = ((const float4 *)P.f_emit)[i];
+    if (TR_LDS) {
+      float4 *dst = (float4 *)(ldsd + (EMIT_LDS ? kEmit : 0));
+      for (int i = threadIdx.x; i < kTr / 4; i += blockDim.x) dst[i] = ((const float4 *)P.f_tr)[i];
+    }
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int vl = 63 - lane;
+  const int slot = wave_id();
+  if (slot >= d.nslots) return;
+  const float *emit = EMIT_LDS ? (const float *)ldsd : P.f_emit;
+  const float *trp = TR_LDS ? (const float *)(ldsd + (EMIT_LDS ? kEmit : 0)) : P.f_tr;
+  const int maxL = db.max_len;
+  float *post = d.scratch + (size_t)slot * d.slot_dw;
+  float *spec = post + (size_t)maxL * kRowF;
+  float *pcv = spec + (size_t)maxL * 8;
+  float *pev = pcv + maxL;
+  uint32_t *tbv = (uint32_t *)(pev + maxL);
+  const float entry_p = P.entry_p;
+  // transitions read from LDS are re-read at every use (trofs, always 0,
+  // is hidden from the compiler once per row)
+  int trofs = 0;
+  auto trl = [&](int k, int q, int col) -> float { return trp[(k * Q + q) * kWave + col + trofs]; };
+
+  // scan steps of the three delete chains (profile constants)
+  float psF[6], psB[6], bsO[6];
+  affine_steps(trl(TR_PRE, Q - 1, lane), psF);
+  affine_steps(trl(TR_SUF, 0, vl), psB);
+  float dpre[Q];   // alignment: sum of D->D gates inside the lane up to q
+  {
+    float acc = 0.0f;
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+      acc += gate(trl(TR_DDIN, q, lane));
+      dpre[q] = acc;
+    }
+    maxplus_steps(acc, bsO);
+  }
+
+  const int count = uni(__atomic_load_n(&db.counters[CNT_DEC], __ATOMIC_RELAXED));
+  for (;;) {
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_DEC], 1);
+    if (idx >= count) break;
+    const int t = uni(db.list_vit[idx]);
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const float loop = lp.loop_p, move = lp.move_p;
+    const uint8_t *x = db.res + db.start[t];
+    const int c = uni(db.perm[t]);
+    const int64_t co = db.coff[t];
+
+    // ------------------------------------------------ 1. Forward, rows kept
+    {
+      float ft[TR_N + 1][kR];
+      asm volatile("" : "+v"(trofs));   // per-phase table registers: no hoisting across targets
+      if (!TR_LDS) {
+#pragma unroll
+        for (int k = 0; k <= TR_N; k++)
+#pragma unroll
+          for (int q = 0; q < kR; q++) ft[k][q] = trl(k, q, lane);
+      }
+      auto TF = [&](int k, int q) -> float { return TR_LDS ? trl(k, q, lane) : ft[k][TR_LDS ? 0 : q]; };
+      float M[Q], I[Q], D[Q];
+#pragma unroll
+      for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = 0.0f;
+      float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
+      int ri = 0;
+      auto load = [&](float(&e)[2 * Q], int a) {
+        const float *er = emit + a * (2 * Q * kWave) + lane;
+#pragma unroll
+        for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+      };
+      auto row = [&](const float(&em)[2 * Q]) -> bool {
+        if (TR_LDS) asm volatile("" : "+v"(trofs));
+        const float msh = lane_up_f(M[Q - 1]);
+        const float ish = lane_up_f(I[Q - 1]);
+        const float dsh = lane_up_f(D[Q - 1]);
+        const float bent = B * entry_p;
+#pragma unroll
+        for (int q = Q - 1; q >= 0; q--) {
+          const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+          const float sm = fmaf(pm, TF(TR_MMIN, q), fmaf(pi, TF(TR_IMIN, q), fmaf(pd, TF(TR_DMIN, q), bent)));
+          const float si = fmaf(M[q], TF(TR_MI, q), I[q] * TF(TR_II, q));
+          M[q] = em[q] * sm;
+          I[q] = em[Q + q] * si;
+        }
+        const float din = lane_up_f(M[Q - 1]);
+        float dc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          D[q] = fmaf(q ? M[q - 1] : din, TF(TR_MDIN, q), dc * TF(TR_DDIN, q));
+          dc = D[q];
+        }
+        const float carry = lane_up_f(affine_scan(D[Q - 1], psF));
+        float part = 0.0f;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          D[q] = fmaf(carry, TF(TR_PRE, q), D[q]);
+          part += M[q] + D[q];
+        }
+        float E = wave_sum_f(part);
+        float Jl = J * loop, Cl = C * loop;
+        J = fmaf(0.5f, E, Jl);
+        C = fmaf(0.5f, E, Cl);
+        N = N * loop;
+        B = (N + J) * move;
+        const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
+        if (big > kWinHi || big < kWinLo) {
+          int ex;
+          (void)frexpf(big, &ex);
+          ex = uni(ex);
+          const float s = ldexpf(1.0f, -ex);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            M[q] *= s;
+            I[q] *= s;
+            D[q] *= s;
+          }
+          J *= s;
+          C *= s;
+          N *= s;
+          B *= s;
+          E *= s;
+          Jl *= s;
+          Cl *= s;
+        }
+        float *pr = post + (size_t)ri * kRowF + lane;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          pr[q * kWave] = M[q];
+          pr[(Q + q) * kWave] = I[q];
+        }
+        if (lane < 4) spec[ri * 8 + lane] = lane == 0 ? N : (lane == 1 ? Jl : (lane == 2 ? Cl : E));
+        ri++;
+        return false;
+      };
+      float ea[2 * Q], eb[2 * Q];
+      int stop;
+      (void)drive_rows(x, L, 0, 0, stop, lane, ea, eb, load, row);
+    }
+    wave_fence();
+
+    // ------------------------------------------------ 2. Backward and posteriors
+    float sum_end = 0.0f;
+    {
+      float bt[TR_N + 1][kR];   // planes 0..TR_N-1, then TR_SUF in slot TR_N
+      asm volatile("" : "+v"(trofs));
+      if (!TR_LDS) {
+#pragma unroll
+        for (int k = 0; k <= TR_N; k++)
+#pragma unroll
+          for (int q = 0; q < kR; q++) bt[k][q] = trl(k < TR_N ? k : TR_SUF, q, vl);
+      }
+      auto TB = [&](int k, int q) -> float {
+        return TR_LDS ? trl(k, q, vl) : bt[k == TR_SUF ? TR_N : k][TR_LDS ? 0 : q];
+      };
+      auto loadE = [&](float(&e)[2 * Q], int a) {
+        const float *er = emit + a * (2 * Q * kWave) + vl;
+#pragma unroll
+        for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+      };
+      auto loadF = [&](float(&f)[2 * Q], int i) {   // stored row i (1-based)
+        const float *pr = post + (size_t)(i - 1) * kRowF + vl;
+#pragma unroll
+        for (int q = 0; q < 2 * Q; q++) f[q] = pr[q * kWave];
+      };
+      // residues, read backwards 256 at a time (lane j holds dword j)
+      uint32_t rch = 0;
+      int rblk = -1;
+      auto res_at = [&](int r) -> int {
+        const int blk = r >> 8;
+        if (blk != rblk) {
+          rblk = blk;
+          rch = ((const uint32_t *)(x + (size_t)blk * 256))[lane];
+        }
+        return (int)((((uint32_t)__builtin_amdgcn_readlane((int)rch, (r >> 2) & 63)) >> ((r & 3) * 8)) & 0xffu);
+      };
+      float bM[Q], bI[Q];
+#pragma unroll
+      for (int q = 0; q < Q; q++) bM[q] = bI[q] = 0.0f;
+      float bJ = 0.0f, bN = 0.0f, bC = 0.0f;
+      // One backward row i from row i+1.  ec / fc hold the emissions of
+      // x_{i+1} and the stored forward row i; en / fn receive those of row
+      // i-1 (loaded here, used by the next call).
+      auto brow = [&](int i, const float(&ec)[2 * Q], const float(&fc)[2 * Q], float(&en)[2 * Q],
+                      float(&fn)[2 * Q]) {
+        if (TR_LDS) asm volatile("" : "+v"(trofs));
+        const bool last = i == L;
+        if (i >= 2) {
+          loadE(en, res_at(i - 1));   // residue x_i, used by row i-1
+          loadF(fn, i - 1);
+        }
+        // u_k = e_k(x_{i+1}) bM_k(i+1), w_k = i_k(x_{i+1}) bI_k(i+1)
+        float u[Q], w[Q];
+        float part = 0.0f;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          u[q] = last ? 0.0f : ec[q] * bM[q];
+          w[q] = last ? 0.0f : ec[Q + q] * bI[q];
+          part += u[q];
+        }
+        const float bB = entry_p * wave_sum_f(part);
+        const float nJ = fmaf(loop, bJ, move * bB);
+        const float nN = fmaf(loop, bN, move * bB);
+        const float nC = last ? move : loop * bC;
+        const float bE = 0.5f * (nC + nJ);
+        // terms through cell k+1, formed there and moved down one cell
+        float mmu[Q], imu[Q], dmu[Q];
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          mmu[q] = TB(TR_MMIN, q) * u[q];
+          imu[q] = TB(TR_IMIN, q) * u[q];
+          dmu[q] = TB(TR_DMIN, q) * u[q];
+        }
+        const float mm0 = lane_up_f(mmu[0]), im0 = lane_up_f(imu[0]), dm0 = lane_up_f(dmu[0]);
+        // delete chain D_k = E + DM_k u_{k+1} + DD_k D_{k+1}, within the lane first
+        float dp[Q];
+#pragma unroll
+        for (int q = Q - 1; q >= 0; q--) {
+          const float dmn = q + 1 < Q ? dmu[q + 1] : dm0;
+          dp[q] = q + 1 < Q ? fmaf(TB(TR_DDIN, q + 1), dp[q + 1], bE + dmn) : bE + dmn;
+        }
+        const float carry = lane_up_f(affine_scan(dp[0], psB));
+        float mdb[Q];
+#pragma unroll
+        for (int q = 0; q < Q; q++) mdb[q] = TB(TR_MDIN, q) * fmaf(carry, TB(TR_SUF, q), dp[q]);
+        const float md0 = lane_up_f(mdb[0]);
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          const float mmn = q + 1 < Q ? mmu[q + 1] : mm0;
+          const float imn = q + 1 < Q ? imu[q + 1] : im0;
+          const float mdn = q + 1 < Q ? mdb[q + 1] : md0;
+          bM[q] = bE + mmn + fmaf(TB(TR_MI, q), w[q], mdn);
+          bI[q] = fmaf(TB(TR_II, q), w[q], imn);
+        }
+        bJ = nJ;
+        bN = nN;
+        bC = nC;
+        // posteriors of row i, normalised by the row total
+        float part2 = 0.0f;
+#pragma unroll
+        for (int q = 0; q < Q; q++) part2 += fmaf(fc[q], bM[q], fc[Q + q] * bI[q]);
+        const float sv = spec[(i - 1) * 8 + (lane & 7)];
+        const float fN = readlane_f(sv, 0), fJl = readlane_f(sv, 1), fCl = readlane_f(sv, 2), fE = readlane_f(sv, 3);
+        const float Zc = wave_sum_f(part2);
+        const float Z = fmaf(fN, bN, fmaf(fJl, bJ, fmaf(fCl, bC, Zc)));
+        const float inv = 1.0f / Z;
+        float *pw = post + (size_t)(i - 1) * kRowF + vl;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          pw[q * kWave] = fc[q] * bM[q] * inv;
+          pw[(Q + q) * kWave] = fc[Q + q] * bI[q] * inv;
+        }
+        const float core = Zc * inv, pend = fE * bE * inv;
+        if (lane == 0) {
+          pcv[i - 1] = core;
+          pev[i - 1] = pend;
+          if (d.pp) d.pp[co + i - 1] = core;
+        }
+        sum_end += pend;
+        // rescale the values carried to the next row
+        const float big = fmaxf(fmaxf(fmaxf(bB, bJ), fmaxf(bN, bC)), bE);
+        if (big > kWinHi || big < kWinLo) {
+          int ex;
+          (void)frexpf(big, &ex);
+          ex = uni(ex);
+          const float s = ldexpf(1.0f, -ex);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            bM[q] *= s;
+            bI[q] *= s;
+          }
+          bJ *= s;
+          bN *= s;
+          bC *= s;
+        }
+      };
+      float ea[2 * Q], fa[2 * Q], eb[2 * Q], fb[2 * Q];
+#pragma unroll
+      for (int q = 0; q < 2 * Q; q++) ea[q] = 0.0f;   // row L uses no emissions
+      loadF(fa, L);
+      for (int i = L;;) {
+        brow(i, ea, fa, eb, fb);
+        if (--i < 1) break;
+        brow(i, eb, fb, ea, fa);
+        if (--i < 1) break;
+      }
+    }
+    if (d.exp_dom && lane == 0) d.exp_dom[c] = sum_end;
+    wave_fence();
+
+    // ------------------------------------------------ 3. Regions and alignments
+    {
+      float og[TR_N][kR];   // gates of the "into" transitions (forward layout)
+      asm volatile("" : "+v"(trofs));
+      if (!TR_LDS) {
+#pragma unroll
+        for (int k = 0; k < TR_N; k++)
+#pragma unroll
+          for (int q = 0; q < kR; q++) og[k][q] = gate(trl(k, q, lane));
+      }
+      auto GT = [&](int k, int q) -> float { return TR_LDS ? gate(trl(k, q, lane)) : og[k][TR_LDS ? 0 : q]; };
+      auto zero_fill = [&](int from, int to) {   // alignment codes of residues from..to (0-based) = 0
+        if (d.aln)
+          for (int j = from + lane; j <= to; j += kWave) d.aln[co + j] = 0;
+      };
+      int scan = 0, zpos = 0;
+      for (;;) {
+        // next region [rs, re] (0-based residues) at or after `scan`
+        int rs = -1, re = -1;
+        {
+          int in_run = 0, hit = 0, st0 = 0;
+          for (int base = scan & ~63; base < L && re < 0; base += 64) {
+            const int j = base + lane;
+            const float v = j < L ? pcv[j] : 0.0f;
+            const bool ok = j >= scan && j < L;
+            const uint64_t b2 = __builtin_amdgcn_ballot_w64(ok && v >= d.rt2);
+            const uint64_t b1 = __builtin_amdgcn_ballot_w64(ok && v >= d.rt1);
+            for (int k = 0; k < 64; k++) {
+              const int jj = base + k;
+              if (jj < scan) continue;
+              if (jj >= L) break;
+              if ((b2 >> k) & 1) {
+                if (!in_run) {
+                  in_run = 1;
+                  st0 = jj;
+                  hit = 0;
+                }
+                if ((b1 >> k) & 1) hit = 1;
+              } else if (in_run) {
+                in_run = 0;
+                if (hit) {
+                  rs = st0;
+                  re = jj - 1;
+                  break;
+                }
+              }
+            }
+          }
+          if (re < 0 && in_run && hit) {
+            rs = st0;
+            re = L - 1;
+          }
+        }
+        if (re < 0) break;
+        zero_fill(zpos, rs - 1);
+        zpos = re + 1;
+        scan = re + 1;
+        const int s1 = rs + 1, e1 = re + 1, R = re - rs + 1;   // 1-based region, rows
+
+        // optimal-accuracy recurrence over rows r = 0..R-1 (residue s1 + r)
+        float OM[Q], OI[Q], OD[Q];
+#pragma unroll
+        for (int q = 0; q < Q; q++) OM[q] = OI[q] = OD[q] = kNegInf;
+        float Gp = 0.0f;                     // sum of (1 - core) over the residues before this row
+        float bestv = kNegInf;
+        int bestr = 0, bestq = 0;
+        float pch = 0.0f;
+        int pblk = -1;
+        for (int r = 0; r < R; r++) {
+          if (TR_LDS) asm volatile("" : "+v"(trofs));
+          const int i0 = rs + r;
+          if ((i0 >> 6) != pblk) {
+            pblk = i0 >> 6;
+            const int j = pblk * 64 + lane;
+            pch = j < L ? pcv[j] : 0.0f;
+          }
+          const float gi = 1.0f - readlane_f(pch, i0 & 63);
+          const float *pr = post + (size_t)i0 * kRowF + lane;
+          float pm[Q], pi[Q];
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            pm[q] = pr[q * kWave];
+            pi[q] = pr[(Q + q) * kWave];
+          }
+          const float omL = lane_up_fill(OM[Q - 1], kNegInf);
+          const float oiL = lane_up_fill(OI[Q - 1], kNegInf);
+          const float odL = lane_up_fill(OD[Q - 1], kNegInf);
+          float nOM[Q], nOI[Q];
+          uint32_t tw[NB];
+#pragma unroll
+          for (int j = 0; j < NB; j++) tw[j] = 0;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float cm = (q ? OM[q - 1] : omL) + GT(TR_MMIN, q);
+            const float ci = (q ? OI[q - 1] : oiL) + GT(TR_IMIN, q);
+            const float cd = (q ? OD[q - 1] : odL) + GT(TR_DMIN, q);
+            float best = Gp;
+            uint32_t sel = 0;
+            if (cm > best) { best = cm; sel = 1; }
+            if (ci > best) { best = ci; sel = 2; }
+            if (cd > best) { best = cd; sel = 3; }
+            nOM[q] = pm[q] + best;
+            const float jm = OM[q] + GT(TR_MI, q), ji = OI[q] + GT(TR_II, q);
+            const uint32_t seli = ji > jm ? 1u : 0u;
+            nOI[q] = pi[q] + fmaxf(jm, ji);
+            tw[q >> 3] |= (sel | (seli << 2)) << ((q & 7) * 4);
+          }
+          // delete chain of this row: within the lane, then across lanes
+          const float nomL = lane_up_fill(nOM[Q - 1], kNegInf);
+          float dpart[Q];
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float fm = (q ? nOM[q - 1] : nomL) + GT(TR_MDIN, q);
+            dpart[q] = q ? fmaxf(fm, dpart[q - 1] + GT(TR_DDIN, q)) : fm;
+          }
+          const float dcarry = lane_up_fill(maxplus_scan(dpart[Q - 1], bsO), kNegInf);
+#pragma unroll
+          for (int q = 0; q < Q; q++) OD[q] = fmaxf(dpart[q], dcarry + dpre[q]);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float fd = (q ? OD[q - 1] : dcarry) + GT(TR_DDIN, q);
+            const float fm = (q ? nOM[q - 1] : nomL) + GT(TR_MDIN, q);
+            tw[q >> 3] |= (fd > fm ? 8u : 0u) << ((q & 7) * 4);
+          }
+          uint32_t *tr = tbv + (size_t)r * NB * kWave + lane;
+#pragma unroll
+          for (int j = 0; j < NB; j++) tr[j * kWave] = tw[j];
+          const float Gn = Gp + gi;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float v = nOM[q] - Gn;
+            if (v > bestv) {
+              bestv = v;
+              bestr = r;
+              bestq = q;
+            }
+            OM[q] = nOM[q];
+            OI[q] = nOI[q];
+          }
+          Gp = Gn;
+        }
+        // the first best end cell in row-major order
+        const float vmax = wave_max_f(bestv);
+        const int key = wave_min_i32(bestv == vmax ? bestr * (kWave * Q) + lane * Q + bestq : INT_MAX);
+        const int br = key / (kWave * Q), bc = key % (kWave * Q);
+        const float score = vmax + Gp;
+        wave_fence();
+
+        // traceback from M at (br, bc); codes collected 64 residues at a time
+        int r = br, cc = bc, st = 0;   // st: 0 = M, 2 = I, 3 = D
+        int a1 = s1, k1 = 1;
+        int cw = re >> 6;
+        int code = 0;
+        auto flush = [&](int w) {
+          const int j = w * 64 + lane;
+          if (d.aln && j >= rs && j <= re) d.aln[co + j] = (int16_t)code;
+          code = 0;
+        };
+        auto put = [&](int i0, int v) {
+          const int w = i0 >> 6;
+          while (cw > w) {
+            flush(cw);
+            cw--;
+          }
+          if (lane == (i0 & 63)) code = v;
+        };
+        for (int guard = 0; guard <= R + kWave * Q; guard++) {
+          if (r < 0 || cc < 0) break;
+          const int cl = cc / Q, q = cc - cl * Q;
+          const uint32_t *tr = tbv + ((size_t)r * NB + (q >> 3)) * kWave;
+          const uint32_t word = (uint32_t)__builtin_amdgcn_readlane((int)tr[lane], cl);
+          const uint32_t nib = (word >> ((q & 7) * 4)) & 0xfu;
+          if (st == 0) {
+            put(rs + r, cc + 1);
+            const uint32_t f = nib & 3u;
+            if (f == 0) {
+              a1 = s1 + r;
+              k1 = cc + 1;
+              break;
+            }
+            r--;
+            cc--;
+            st = f == 1 ? 0 : (int)f;
+          } else if (st == 2) {
+            put(rs + r, -(cc + 1));
+            st = (nib >> 2) & 1u ? 2 : 0;
+            r--;
+          } else {
+            st = (nib >> 3) & 1u ? 3 : 0;
+            cc--;
+          }
+        }
+        while (cw >= (rs >> 6)) {
+          flush(cw);
+          cw--;
+        }
+        // expected domain ends in the region
+        float acc = 0.0f;
+        for (int j = rs + lane; j <= re; j += kWave) acc += pev[j];
+        const float nexp = wave_sum_f(acc);
+        const int di = wave_fetch_add(&db.counters[CNT_NDOM], 1);
+        if (di < d.max_dom && lane < 9) {
+          const int32_t v = lane == 0 ? c
+                          : lane == 1 ? s1
+                          : lane == 2 ? e1
+                          : lane == 3 ? a1
+                          : lane == 4 ? s1 + br
+                          : lane == 5 ? k1
+                          : lane == 6 ? bc + 1
+                          : lane == 7 ? __builtin_bit_cast(int32_t, score)
+                                      : __builtin_bit_cast(int32_t, nexp);
+          ((int32_t *)(d.dom + di))[lane] = v;
+        }
+        wave_fence();
+      }
+      zero_fill(zpos, L - 1);
+    }
+  }
+}
+
+// Targets to decode: those whose caller flags hold every bit of the mask.
+__global__ void decode_select(DevDb db, const uint8_t *flags, int mask) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= db.n) return;
+  const bool take = !flags || (flags[db.perm[t]] & mask) == mask;
+  if (take) db.list_vit[atomicAdd(&db.counters[CNT_DEC], 1)] = (int32_t)t;
+}
+
+__global__ void decode_clear(int32_t *c) {
+  if (threadIdx.x == 0) {
+    c[CNT_DEC] = 0;
+    c[CNT_WORK_DEC] = 0;
+    c[CNT_NDOM] = 0;
+  }
+}
+
+__global__ void decode_export(const int32_t *c, int32_t *n_dom) {
+  if (threadIdx.x == 0) *n_dom = c[CNT_NDOM];
+}
+
+// Tables of the decode kernel: emissions in LDS up to 12 vectors per lane,
+// transitions in registers up to 16, else in LDS.
+template <int Q>
+constexpr bool kDecEmitLds = Q <= 12;
+template <int Q>
+constexpr bool kDecTrLds = Q > 16;
+
+template <int Q>
+size_t decode_lds() {
+  return (kDecEmitLds<Q> ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) +
+         (kDecTrLds<Q> ? (size_t)(TR_N + 2) * Q * kWave * 4 : 0);
+}
+
+template <int Q>
+int decode_waves_q() {
+  auto k = decode_kernel<Q, kDecEmitLds<Q>, kDecTrLds<Q>>;
+  const size_t lds = decode_lds<Q>();
+  if (lds > 64 * 1024)
+    (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, kDecThreads, lds) != hipSuccess || nb < 1) nb = 1;
+  int dev = 0, ncu = 0;
+  (void)hipGetDevice(&dev);
+  (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (ncu <= 0) ncu = 256;
+  return nb * ncu * (kDecThreads / kWave);
+}
+
+template <int Q>
+hipError_t launch_decode_q(const DevDb &db, const DevProfile &P, const DevDecode &d, hipStream_t s) {
+  auto k = decode_kernel<Q, kDecEmitLds<Q>, kDecTrLds<Q>>;
+  const size_t lds = decode_lds<Q>();
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int blocks = d.nslots / (kDecThreads / kWave);
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(kDecThreads), lds, s, P, db, d);
+  return hipGetLastError();
+}
+
+#define HMM_DEC_CASES(X) \
+  X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12) X(14) X(16) X(20) X(24) X(28) X(32) X(40) X(48)
+
+}  // namespace
+
+int decode_max_waves(const DevProfile &p) {
+  switch (p.Q32) {
+#define HMM_CASE(q) \
+  case q:           \
+    return decode_waves_q<q>();
+    HMM_DEC_CASES(HMM_CASE)
+#undef HMM_CASE
+  }
+  return 0;
+}
+
+hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t s) {
+  hipLaunchKernelGGL(decode_clear, dim3(1), dim3(64), 0, s, db.counters);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || db.n <= 0) {
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(decode_export, dim3(1), dim3(64), 0, s, (const int32_t *)db.counters, d.n_dom);
+      e = hipGetLastError();
+    }
+    return e;
+  }
+  const int threads = 256;
+  hipLaunchKernelGGL(decode_select, dim3((unsigned)((db.n + threads - 1) / threads)), dim3(threads), 0, s, db,
+                     d.sel_flags, d.sel_mask);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  switch (p.Q32) {
+#define HMM_CASE(q)                          \
+  case q:                                    \
+    e = launch_decode_q<q>(db, p, d, s);     \
+    break;
+    HMM_DEC_CASES(HMM_CASE)
+#undef HMM_CASE
+    default:
+      e = hipErrorInvalidValue;
+  }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(decode_export, dim3(1), dim3(64), 0, s, (const int32_t *)db.counters, d.n_dom);
+  return hipGetLastError();
+}
+
+}  // namespace hmmgpu

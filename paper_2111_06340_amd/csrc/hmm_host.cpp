@@ -82,6 +82,9 @@ int instantiated_q32(int q) {
 
 std::atomic<uint64_t> g_profile_serial{1};
 
+// Device memory the decoding scratch of one database may take.
+constexpr size_t kDecodeScratchMax = (size_t)16 << 30;
+
 }  // namespace
 
 struct hmm_profile {
@@ -113,6 +116,9 @@ struct hmm_db {
   // join (recorded on aux).
   hipStream_t aux = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
+  // posterior-decoding scratch (allocated by the first hmm_decode)
+  void *dec_mem = nullptr;
+  size_t dec_bytes = 0;
   // stage timing ring (profiling hook)
   std::vector<hipEvent_t> tev;  // capacity * 5
   int32_t tcap = 0;
@@ -274,7 +280,7 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   const size_t n_vtr = (size_t)TR_N * Q8 * kWave;
   const size_t n_w32emit = (size_t)kAlpha * 2 * Q32 * kWave;
   const size_t n_w32tr = (size_t)TR_N * Q32 * kWave;
-  const size_t n_ftr = (size_t)(TR_N + 1) * Q32 * kWave;
+  const size_t n_ftr = (size_t)(TR_N + 2) * Q32 * kWave;
   const size_t total = n_msv + n_vemit + n_vtr + n_w32emit + n_w32tr + n_w32emit + n_ftr;
   std::vector<uint32_t> h(total, 0);
   uint32_t *h_msv = h.data();
@@ -370,12 +376,20 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
         h_w32tr[(size_t)tr * Q32 * kWave + pk_index(q, l)] = w32(tr_cell(tr, c));
         h_ftr[(size_t)tr * Q32 * kWave + pk_index(q, l)] = (float)tr_prob(tr, c);
       }
-  // D-chain prefix products inside each slot: prod_{j<=q} DDin(cell l*Q+j)
+  // D-chain products inside each slot.  Forward (cell k-1 -> k):
+  // prod_{j<=q} DDin(cell l*Q+j).  Backward (cell k+1 -> k):
+  // prod_{j=q+1}^{Q} DDin(cell l*Q+j), whose last factor is the next slot's
+  // first cell (0 past the last slot).
   for (int l = 0; l < kWave; l++) {
     double acc = 1.0;
     for (int q = 0; q < Q32; q++) {
       acc *= tr_prob(TR_DDIN, w_cell(Q32, q, l));
-      h_ftr[(size_t)TR_N * Q32 * kWave + pk_index(q, l)] = (float)acc;
+      h_ftr[(size_t)TR_PRE * Q32 * kWave + pk_index(q, l)] = (float)acc;
+    }
+    acc = l + 1 < kWave ? tr_prob(TR_DDIN, w_cell(Q32, 0, l + 1)) : 0.0;
+    for (int q = Q32 - 1; q >= 0; q--) {
+      h_ftr[(size_t)TR_SUF * Q32 * kWave + pk_index(q, l)] = (float)acc;
+      acc *= tr_prob(TR_DDIN, w_cell(Q32, q, l));
     }
   }
 
@@ -556,7 +570,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   const size_t sz_res = al((size_t)res_bytes);
   const size_t sz_start = al((size_t)n * 8 + 8), sz_i32 = al((size_t)n * 4 + 4), sz_u8 = al((size_t)n + 1);
   const size_t sz_lp = al(sizeof(LenParams) * ((size_t)max_len + 1));
-  const size_t total = sz_res + sz_start + sz_i32 * 2 + sz_u8 + sz_i32 * 3 + al(CNT_N * 4) + sz_lp;
+  const size_t total = sz_res + sz_start * 2 + sz_i32 * 2 + sz_u8 + sz_i32 * 3 + al(CNT_N * 4) + sz_lp;
 
   hmm_db *db = new (std::nothrow) hmm_db();
   if (!db) return fail(HMM_ENOMEM, "host allocation failed");
@@ -583,6 +597,9 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   const size_t o_perm = off;
   int32_t *s_perm = (int32_t *)(stage + off);
   off += sz_i32;
+  const size_t o_coff = off;
+  int64_t *s_coff = (int64_t *)(stage + off);
+  off += sz_start;
   const size_t o_flags = off;
   off += sz_u8;
   const size_t o_lv = off;
@@ -600,6 +617,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
     s_start[i] = start[i];
     s_len[i] = len[i];
     s_perm[i] = order[i];
+    s_coff[i] = offsets[order[i]];
   }
   e = hipMalloc(&db->dmem, total);
   if (e != hipSuccess) {
@@ -631,6 +649,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   dv.start = (const int64_t *)(b + o_start);
   dv.len = (const int32_t *)(b + o_len);
   dv.perm = (const int32_t *)(b + o_perm);
+  dv.coff = (const int64_t *)(b + o_coff);
   dv.flags_sorted = b + o_flags;
   dv.list_vit = (int32_t *)(b + o_lv);
   dv.list_ovf = (int32_t *)(b + o_lo);
@@ -704,6 +723,7 @@ int hmm_db_free(hmm_db *db) {
   drop_timing(db);
   release_sync(db);
   if (db->h_lp) (void)hipHostFree(db->h_lp);
+  if (db->dec_mem) (void)hipFree(db->dec_mem);
   hipError_t e2 = db->dmem ? hipFree(db->dmem) : hipSuccess;
   delete db;
   if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize(db)");
@@ -746,6 +766,67 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   hipEvent_t *ev = nullptr;
   if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
   HIP_TRY(launch_search(p->dev, db->dev, o, s, db->aux, db->fork, db->join, ev), "kernel launch");
+  HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
+  db->searched = true;
+  return HMM_OK;
+}
+
+int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask, const hmm_decode_out *out,
+               hmm_stream stream) {
+  if (!p || !db || !out) return fail(HMM_EINVAL, "NULL profile, db or out");
+  if (!out->dom || !out->n_dom) return fail(HMM_EINVAL, "NULL dom or n_dom");
+  if (out->max_dom < 0) return fail(HMM_EINVAL, "max_dom = %d", out->max_dom);
+  hipStream_t s = (hipStream_t)stream;
+  // serialise with the searches on this database (lists, counters, scratch)
+  if (db->searched) HIP_TRY(hipStreamWaitEvent(s, db->done, 0), "hipStreamWaitEvent");
+  DevDecode d{};
+  d.dom = out->dom;
+  d.max_dom = out->max_dom;
+  d.n_dom = out->n_dom;
+  d.exp_dom = out->exp_dom;
+  d.pp = out->pp;
+  d.aln = out->aln;
+  d.sel_flags = flags;
+  d.sel_mask = mask;
+  d.rt1 = HMM_RT1;
+  d.rt2 = HMM_RT2;
+  if (db->n > 0) {
+    // the loop and move probabilities of each length (profile-independent)
+    if (db->lp_serial == 0) {
+      if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+      const hmm_thresholds all{1.0, 1.0, 1.0};
+      for (int L = 0; L <= db->max_len; L++) length_params(p, &all, L < 1 ? 1 : L, &db->h_lp[L], nullptr);
+      HIP_TRY(hipMemcpyAsync(db->d_lp, db->h_lp, sizeof(LenParams) * ((size_t)db->max_len + 1),
+                             hipMemcpyHostToDevice, s),
+              "hipMemcpyAsync(length table)");
+      db->lp_serial = p->serial;
+      db->lp_F[0] = db->lp_F[1] = db->lp_F[2] = 1.0;
+    }
+    // one scratch slot per resident wave, within the scratch budget
+    const int64_t slot_dw = decode_slot_dw(p->dev.Q32, db->max_len);
+    const size_t slot_bytes = (size_t)slot_dw * 4;
+    int64_t nslots = decode_max_waves(p->dev);
+    nslots = std::min<int64_t>(nslots, (int64_t)(kDecodeScratchMax / slot_bytes));
+    nslots = std::min<int64_t>(nslots, (db->n + 3) / 4 * 4);
+    nslots = nslots / 4 * 4;
+    if (nslots < 4) return fail(HMM_ENOMEM, "decode scratch: %zu bytes per wave exceed the budget", slot_bytes);
+    const size_t need = (size_t)nslots * slot_bytes;
+    if (need > db->dec_bytes) {
+      if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+      if (db->dec_mem) HIP_TRY(hipFree(db->dec_mem), "hipFree(decode scratch)");
+      db->dec_mem = nullptr;
+      db->dec_bytes = 0;
+      hipError_t e = hipMalloc(&db->dec_mem, need);
+      if (e != hipSuccess)
+        return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "decode scratch of %zu bytes", need)
+                                        : fail_hip(e, "hipMalloc(decode scratch)");
+      db->dec_bytes = need;
+    }
+    d.scratch = (float *)db->dec_mem;
+    d.slot_dw = slot_dw;
+    d.nslots = (int32_t)nslots;
+  }
+  HIP_TRY(launch_decode(p->dev, db->dev, d, s), "kernel launch");
   HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
   db->searched = true;
   return HMM_OK;

@@ -53,11 +53,19 @@ struct DevProfile {
   const int32_t *v32_emit;      // [20][2][Q32][64]
   const int32_t *v32_tr;        // [TR_N][Q32][64]
   const float *f_emit;          // [20][2][Q32][64] odds e/f, i/f
-  const float *f_tr;            // [TR_N + 1][Q32][64]: probabilities, then D-chain prefix products
+  // [TR_N + 2][Q32][64]: probabilities; plane TR_PRE: D-chain products
+  // prod_{j<=q} DDIN(lane*Q + j); plane TR_SUF: prod_{j=q+1}^{Q} DDIN(lane*Q + j)
+  // (the last factor belongs to the next lane's first cell; 0 past the end)
+  const float *f_tr;
 };
+enum { TR_PRE = TR_N, TR_SUF = TR_N + 1 };
 
 // Counters in the database scratch (device int32).
-enum { CNT_VIT = 0, CNT_OVF, CNT_FWD, CNT_FWD_PASS, CNT_WORK_VIT, CNT_WORK_OVF, CNT_WORK_FWD, CNT_N = 8 };
+enum {
+  CNT_VIT = 0, CNT_OVF, CNT_FWD, CNT_FWD_PASS, CNT_WORK_VIT, CNT_WORK_OVF, CNT_WORK_FWD,
+  CNT_DEC, CNT_WORK_DEC, CNT_NDOM,   // posterior decoding: list size, work counter, domains found
+  CNT_N = 16
+};
 
 struct DevDb {
   int64_t n;
@@ -72,6 +80,7 @@ struct DevDb {
   int32_t *list_fwd;            // [n] Viterbi survivors
   int32_t *counters;            // [CNT_N]
   const LenParams *lp;          // [max_len + 1]
+  const int64_t *coff;          // [n] offset of each target in the caller's residue array
 };
 
 struct DevOut {
@@ -81,6 +90,37 @@ struct DevOut {
   uint8_t *flags;
   int64_t *counts;
 };
+
+// Posterior decoding (hmm_decode): outputs and per-wave scratch.
+struct DevDecode {
+  hmm_domain *dom;              // [max_dom] domain records
+  int32_t max_dom;
+  int32_t *n_dom;               // device int32: domains found (may exceed max_dom)
+  float *exp_dom;               // [n] caller order, or null
+  float *pp;                    // [n_residues] caller layout, or null
+  int16_t *aln;                 // [n_residues] caller layout, or null
+  const uint8_t *sel_flags;     // [n] caller order; null = decode every target
+  int32_t sel_mask;             // decode targets with (flags & mask) == mask
+  float rt1, rt2;               // region thresholds on the core posterior
+  float *scratch;               // nslots * slot_dw floats
+  int64_t slot_dw;              // dwords per wave slot
+  int32_t nslots;               // waves of the decode launch (one slot each)
+};
+
+// Dwords of one decode slot for vectors-per-lane Q and targets up to max_len:
+//   posteriors [max_len][2][Q][64], specials [max_len][8], core and end
+//   posteriors [max_len] each, traceback nibbles [max_len][ceil(Q/8)][64].
+inline int64_t decode_slot_dw(int Q, int max_len) {
+  const int64_t nb = (Q + 7) / 8;
+  const int64_t dw = (int64_t)max_len * (2 * Q * 64 + 8 + 2 + nb * 64);
+  return (dw + 63) / 64 * 64;
+}
+
+// Largest number of waves of the decode kernel of profile p resident at once.
+int decode_max_waves(const DevProfile &p);
+
+// Enqueue the decode of the selected targets on `stream` (d.nslots waves).
+hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t stream);
 
 // Enqueue the whole cascade on `stream`.  The int32 rescore runs on `aux`,
 // concurrently with Forward: it forks after the int16 Viterbi (event

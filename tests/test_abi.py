@@ -34,9 +34,16 @@ def test_library_exports_every_declared_symbol():
 
 def test_header_constants_match_binding():
     txt = open(HEADER).read()
-    consts = dict(re.findall(r"#define (HMM_[A-Z_0-9]+) \(?(-?(?:0x)?[0-9a-fA-F]+)\)?", txt))
+    floats = dict(re.findall(r"#define (HMM_[A-Z_0-9]+) ([0-9]+\.[0-9]+)f\b", txt))
+    consts = dict(re.findall(r"#define (HMM_[A-Z_0-9]+) \(?(-?(?:0x)?[0-9a-fA-F]+)\)?(?:\s|$)", txt))
+    assert set(floats) == {"HMM_RT1", "HMM_RT2"}
     for k, v in consts.items():
         assert getattr(hg, k) == int(v, 0), k
+    for k, v in floats.items():
+        assert getattr(hg, k) == float(v), k
+        assert np.float32(getattr(hg, k)) == np.float32(float(v))
+    # the library's region thresholds are the oracle's
+    assert (hg.HMM_RT1, hg.HMM_RT2) == (oracle.RT1, oracle.RT2)
 
 
 def test_strerror():
@@ -174,3 +181,17 @@ def test_length_params_equal_oracle(F):
         assert (lib["thr8"], lib["thr16"]) == (t8, t16)
         assert lib["loop"] == o["loop"] and lib["move"] == o["move"] and lib["null"] == o["null"]
         assert lib["fwd_thr"] == ft or (math.isinf(ft) and math.isinf(lib["fwd_thr"]))
+
+
+def test_decode_rejects_bad_arguments_on_the_host():
+    import ctypes as C
+    L = hg.lib()
+    out = hg.hmm_decode_out(None, 0, None, None, None, None)
+    # NULL profile / db / out, NULL dom or n_dom, negative max_dom: rejected before any GPU call
+    assert L.hmm_decode(None, None, None, 0, C.byref(out), None) == hg.HMM_EINVAL
+    assert L.hmm_decode(C.c_void_p(1), C.c_void_p(1), None, 0, None, None) == hg.HMM_EINVAL
+    assert L.hmm_decode(C.c_void_p(1), C.c_void_p(1), None, 0, C.byref(out), None) == hg.HMM_EINVAL
+    assert "dom" in hg.hmm_last_error()
+    bad = hg.hmm_decode_out(C.c_void_p(8).value, -1, C.c_void_p(8).value, None, None, None)
+    assert L.hmm_decode(C.c_void_p(1), C.c_void_p(1), None, 0, C.byref(bad), None) == hg.HMM_EINVAL
+    assert "max_dom" in hg.hmm_last_error()
