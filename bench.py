@@ -42,6 +42,8 @@ MSV_OPS_PER_CELL = 4
 VIT_OPS_PER_CELL = 18
 RESCORE_OPS_PER_CELL = 17
 FWD_FLOPS_PER_CELL = 18
+BWD_FLOPS_PER_CELL = 26
+OA_FLOPS_PER_CELL = 20
 
 
 def log(msg):
@@ -118,6 +120,10 @@ def main():
                     help="run one plain device copy of MB MiB first (scales rocprofv3 byte counters)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "msv_traffic_C3.json"),
                     help="HBM traffic per MSV launch measured by rocprofv3 counters (JSON), if present")
+    ap.add_argument("--decode", action="store_true",
+                    help="also time posterior decoding (hmm_decode) of the Forward survivors of the last "
+                         "search: Forward with rows kept, Backward, regions and alignments (reported "
+                         "under 'decode', not in value)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the search shards by database bins across GPUs "
@@ -248,6 +254,8 @@ def main():
     }
     if batched:
         rec["queries_per_hour"] = round(len(Ps) / (ms_step / 1e3) * 3600.0, 1)
+    if args.decode:
+        rec["decode"] = bench_decode(hg, Ps[-1], profs[-1], D, outs[-1], stream, args)
     for P in Ps:
         P.close()
     D.close()
@@ -257,6 +265,49 @@ def main():
         rec["cpu_baseline"] = cpu_baseline(profs[0], db, F, args.cpu_seconds, threads)
         log(f"CPU oracle: {rec['cpu_baseline']['value']} GCUPS")
     print(json.dumps(rec), flush=True)
+
+
+def bench_decode(hg, P, prof, D, out, stream, args) -> dict:
+    """Time hmm_decode of the Forward passes of the last search on the
+    search stream (HIP events on that stream bracket exactly its kernels)."""
+    import numpy as np
+    import torch
+    flags = out["flags"]
+    fl = flags.cpu().numpy()
+    lengths = np.asarray(D.lengths_caller())
+    sel = (fl & hg.HMM_FWD_PASS) != 0
+    n_dec = int(sel.sum())
+    cells = prof.M * int(lengths[sel].sum())
+    dec = None
+    for _ in range(max(1, args.warmup)):
+        dec = hg.decode(P, D, flags=flags, mask=hg.HMM_FWD_PASS, stream=stream)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(args.steps):
+        dec = hg.decode(P, D, flags=flags, mask=hg.HMM_FWD_PASS, stream=stream)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    doms = hg.domains_table(dec)
+    region_cells = prof.M * sum(d["e"] - d["s"] + 1 for d in doms)
+    # fp32 work of the three passes (FMA = 2 flops): Forward 18 and Backward
+    # 26 flops per cell of every decoded target, alignment 20 per cell of
+    # the regions (adds and maxima of its three states)
+    flops = (FWD_FLOPS_PER_CELL + BWD_FLOPS_PER_CELL) * cells + OA_FLOPS_PER_CELL * region_cells
+    # HBM traffic the design needs: every kept Forward row (M and I, 8 bytes
+    # per cell) written once and read back once by the Backward pass, plus
+    # the 0.5-byte traceback code of every region cell written (the
+    # traceback reads a few of them again)
+    traffic = 16 * cells + region_cells // 2
+    s = ms / 1e3
+    log(f"decode: {n_dec} targets, {len(doms)} regions, {ms:.3f} ms, {cells / s / 1e9:.1f} GCUPS")
+    return {"ms": round(ms, 4), "targets": n_dec, "regions": len(doms), "cells": cells,
+            "region_cells": region_cells, "gcups": round(cells / s / 1e9, 2),
+            "roofline": {"fp32": {"achieved": round(flops / s / 1e12, 3), "peak": PEAK_FP32_TFLOPS,
+                                  "unit": "TFLOP/s", "frac": round(flops / s / 1e12 / PEAK_FP32_TFLOPS, 4)},
+                         "hbm": {"achieved": round(traffic / s / 1e9, 1), "peak": 8000.0, "unit": "GB/s",
+                                 "frac": round(traffic / s / 8e12, 4)}}}
 
 
 def kernel_source_sha() -> str:

@@ -263,6 +263,11 @@ class Database:
     def __init__(self, residues, offsets, stream=None):
         self.handle = hmm_db_upload(residues, offsets, stream)
         self.n, self.n_residues, self.max_len = hmm_db_info(self.handle)
+        self._lengths = np.diff(np.asarray(offsets, dtype=np.int64))
+
+    def lengths_caller(self):
+        """Target lengths in the caller's order (host array)."""
+        return self._lengths
 
     def close(self):
         if getattr(self, "handle", None):

@@ -7,7 +7,7 @@
 // One wavefront decodes one target at a time in a private scratch slot
 // (one slot per resident wave; the launch has exactly one wave per slot):
 //   1. Forward in fp32 probability space, as in the search's Forward
-//      kernel, storing M_k(i) and I_k(i) of every row and the row's special
+//      kernel, keeping M_k(i) and I_k(i) of every row and the row's special
 //      values (N, J-loop, C-loop and E parts).
 //   2. Backward from row L down to row 1.  The backward delete chain runs
 //      from cell k+1 to cell k, so this phase puts virtual lane v = 63 - l
@@ -17,10 +17,11 @@
 //      total, sum over the states that can emit residue i
 //         Z_i = sum_k (fM bM + fI bI) + fN bN + fJl bJ + fCl bC,
 //      which is the same value P(x) in the row's scale, so no scale factor
-//      has to be tracked.  The posteriors overwrite the stored forward row.
-//   3. Regions from the core posteriors (ballots over 64 residues), then per
-//      region the optimal-accuracy recurrence in max-plus form, with a
-//      4-bit traceback code per cell, and the traceback.
+//      has to be tracked.  In the same pass, row by row in the same
+//      direction, the region rule and the optimal-accuracy recurrence
+//      (written from the end of the region, max-plus form, a 4-bit
+//      traceback code per cell) advance, so posteriors are never stored.
+//   3. Traceback of each region's alignment, from its start cell forwards.
 // Values are kept inside [2^-32, 2^32] by exact power-of-two rescaling in
 // both directions, so a product of a forward and a backward value stays far
 // from the fp32 range limits.
@@ -145,29 +146,21 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
   const int maxL = db.max_len;
   float *post = d.scratch + (size_t)slot * d.slot_dw;
   float *spec = post + (size_t)maxL * kRowF;
-  float *pcv = spec + (size_t)maxL * 8;
-  float *pev = pcv + maxL;
-  uint32_t *tbv = (uint32_t *)(pev + maxL);
+  int32_t *regs = (int32_t *)(spec + (size_t)maxL * 8);
+  uint32_t *tbv = (uint32_t *)(regs + (size_t)maxL * 4 + 8);
   const float entry_p = P.entry_p;
   // transitions read from LDS are re-read at every use (trofs, always 0,
   // is hidden from the compiler once per row)
   int trofs = 0;
   auto trl = [&](int k, int q, int col) -> float { return trp[(k * Q + q) * kWave + col + trofs]; };
 
-  // scan steps of the three delete chains (profile constants)
-  float psF[6], psB[6], bsO[6];
+  // scan steps of the delete chains (profile constants): Forward, Backward,
+  // and the alignment recurrence (max-plus form of the Backward chain)
+  float psF[6], psB[6], bsB[6];
   affine_steps(trl(TR_PRE, Q - 1, lane), psF);
   affine_steps(trl(TR_SUF, 0, vl), psB);
-  float dpre[Q];   // alignment: sum of D->D gates inside the lane up to q
-  {
-    float acc = 0.0f;
-#pragma unroll
-    for (int q = 0; q < Q; q++) {
-      acc += gate(trl(TR_DDIN, q, lane));
-      dpre[q] = acc;
-    }
-    maxplus_steps(acc, bsO);
-  }
+  maxplus_steps(gate(trl(TR_SUF, 0, vl)), bsB);
+  const int cbase = vl * Q;   // first cell of this lane in the Backward layout
 
   const int count = uni(__atomic_load_n(&db.counters[CNT_DEC], __ATOMIC_RELAXED));
   for (;;) {
@@ -272,11 +265,26 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
     }
     wave_fence();
 
-    // ------------------------------------------------ 2. Backward and posteriors
+    // ------------------------------------------------ 2. Backward, posteriors, regions, alignments
+    //
+    // Rows run from L down to 1.  After row i's posteriors, the region
+    // rule and the alignment recurrence advance by one row in the same
+    // direction: a run of rows with core >= rt2 is a candidate region, and
+    // inside it the recurrence is the optimal-accuracy one written from the
+    // end of the region (T(i) = sum_{j=i}^{e} (1 - core(j))):
+    //   OM_k(i) = pM_k(i) + max{ T(i+1) [end], OM_{k+1}(i+1) [MM_k],
+    //                            OI_k(i+1) [MI_k], OD_{k+1}(i) [MD_k] }
+    //   OI_k(i) = pI_k(i) + max{ OM_{k+1}(i+1) [IM_k], OI_k(i+1) [II_k] }
+    //   OD_k(i) = max{ OM_{k+1}(i+1) [DM_k], OD_{k+1}(i) [DD_k] }
+    // (a transition of probability zero is not allowed); the alignment
+    // starts at the match cell maximising OM_k(i) - T(i), and its value is
+    // that maximum plus T(s).  When the run ends it is kept (it held a
+    // residue with core >= rt1) or its residues get code 0.
     float sum_end = 0.0f;
+    int nreg = 0;
     {
       float bt[TR_N + 1][kR];   // planes 0..TR_N-1, then TR_SUF in slot TR_N
-      asm volatile("" : "+v"(trofs));
+      asm volatile("" : "+v"(trofs));   // per-phase table registers: no hoisting across targets
       if (!TR_LDS) {
 #pragma unroll
         for (int k = 0; k <= TR_N; k++)
@@ -286,6 +294,7 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
       auto TB = [&](int k, int q) -> float {
         return TR_LDS ? trl(k, q, vl) : bt[k == TR_SUF ? TR_N : k][TR_LDS ? 0 : q];
       };
+      auto GB = [&](int k, int q) -> float { return gate(TB(k, q)); };
       auto loadE = [&](float(&e)[2 * Q], int a) {
         const float *er = emit + a * (2 * Q * kWave) + vl;
 #pragma unroll
@@ -311,333 +320,315 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
 #pragma unroll
       for (int q = 0; q < Q; q++) bM[q] = bI[q] = 0.0f;
       float bJ = 0.0f, bN = 0.0f, bC = 0.0f;
-      // One backward row i from row i+1.  ec / fc hold the emissions of
-      // x_{i+1} and the stored forward row i; en / fn receive those of row
-      // i-1 (loaded here, used by the next call).
-      auto brow = [&](int i, const float(&ec)[2 * Q], const float(&fc)[2 * Q], float(&en)[2 * Q],
-                      float(&fn)[2 * Q]) {
+      // alignment recurrence: row i+1 values, run state, best start cell
+      float OMn[Q], OIn[Q];
+#pragma unroll
+      for (int q = 0; q < Q; q++) OMn[q] = OIn[q] = kNegInf;
+      int in_run = 0, run_e = 0, hit = 0, besti = 0, bestc = 0;
+      float T = 0.0f, nexp = 0.0f, bestv = kNegInf;
+      // Rows a row ahead in two more buffers, except for long profiles,
+      // where the registers are better spent on the row itself.
+      constexpr bool kPrefetch = Q <= 12;
+      float enx[kPrefetch ? 2 * Q : 1], fnx[kPrefetch ? 2 * Q : 1];
+      if constexpr (kPrefetch) {
+#pragma unroll
+        for (int q = 0; q < 2 * Q; q++) enx[q] = 0.0f;   // row L uses no emissions
+        loadF(fnx, L);
+      }
+      for (int i = L; i >= 0; i--) {
         if (TR_LDS) asm volatile("" : "+v"(trofs));
-        const bool last = i == L;
-        if (i >= 2) {
-          loadE(en, res_at(i - 1));   // residue x_i, used by row i-1
-          loadF(fn, i - 1);
-        }
-        // u_k = e_k(x_{i+1}) bM_k(i+1), w_k = i_k(x_{i+1}) bI_k(i+1)
-        float u[Q], w[Q];
-        float part = 0.0f;
+        float core = 0.0f, pend = 0.0f;
+        float pm[Q], pi[Q];
+        if (i >= 1) {
+          // ---- Backward row i from row i+1 (ec: emissions of x_{i+1}, fc: kept Forward row i)
+          const bool last = i == L;
+          float ec[2 * Q], fc[2 * Q];
+          if constexpr (kPrefetch) {
 #pragma unroll
-        for (int q = 0; q < Q; q++) {
-          u[q] = last ? 0.0f : ec[q] * bM[q];
-          w[q] = last ? 0.0f : ec[Q + q] * bI[q];
-          part += u[q];
-        }
-        const float bB = entry_p * wave_sum_f(part);
-        const float nJ = fmaf(loop, bJ, move * bB);
-        const float nN = fmaf(loop, bN, move * bB);
-        const float nC = last ? move : loop * bC;
-        const float bE = 0.5f * (nC + nJ);
-        // terms through cell k+1, formed there and moved down one cell
-        float mmu[Q], imu[Q], dmu[Q];
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          mmu[q] = TB(TR_MMIN, q) * u[q];
-          imu[q] = TB(TR_IMIN, q) * u[q];
-          dmu[q] = TB(TR_DMIN, q) * u[q];
-        }
-        const float mm0 = lane_up_f(mmu[0]), im0 = lane_up_f(imu[0]), dm0 = lane_up_f(dmu[0]);
-        // delete chain D_k = E + DM_k u_{k+1} + DD_k D_{k+1}, within the lane first
-        float dp[Q];
-#pragma unroll
-        for (int q = Q - 1; q >= 0; q--) {
-          const float dmn = q + 1 < Q ? dmu[q + 1] : dm0;
-          dp[q] = q + 1 < Q ? fmaf(TB(TR_DDIN, q + 1), dp[q + 1], bE + dmn) : bE + dmn;
-        }
-        const float carry = lane_up_f(affine_scan(dp[0], psB));
-        float mdb[Q];
-#pragma unroll
-        for (int q = 0; q < Q; q++) mdb[q] = TB(TR_MDIN, q) * fmaf(carry, TB(TR_SUF, q), dp[q]);
-        const float md0 = lane_up_f(mdb[0]);
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          const float mmn = q + 1 < Q ? mmu[q + 1] : mm0;
-          const float imn = q + 1 < Q ? imu[q + 1] : im0;
-          const float mdn = q + 1 < Q ? mdb[q + 1] : md0;
-          bM[q] = bE + mmn + fmaf(TB(TR_MI, q), w[q], mdn);
-          bI[q] = fmaf(TB(TR_II, q), w[q], imn);
-        }
-        bJ = nJ;
-        bN = nN;
-        bC = nC;
-        // posteriors of row i, normalised by the row total
-        float part2 = 0.0f;
-#pragma unroll
-        for (int q = 0; q < Q; q++) part2 += fmaf(fc[q], bM[q], fc[Q + q] * bI[q]);
-        const float sv = spec[(i - 1) * 8 + (lane & 7)];
-        const float fN = readlane_f(sv, 0), fJl = readlane_f(sv, 1), fCl = readlane_f(sv, 2), fE = readlane_f(sv, 3);
-        const float Zc = wave_sum_f(part2);
-        const float Z = fmaf(fN, bN, fmaf(fJl, bJ, fmaf(fCl, bC, Zc)));
-        const float inv = 1.0f / Z;
-        float *pw = post + (size_t)(i - 1) * kRowF + vl;
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          pw[q * kWave] = fc[q] * bM[q] * inv;
-          pw[(Q + q) * kWave] = fc[Q + q] * bI[q] * inv;
-        }
-        const float core = Zc * inv, pend = fE * bE * inv;
-        if (lane == 0) {
-          pcv[i - 1] = core;
-          pev[i - 1] = pend;
-          if (d.pp) d.pp[co + i - 1] = core;
-        }
-        sum_end += pend;
-        // rescale the values carried to the next row
-        const float big = fmaxf(fmaxf(fmaxf(bB, bJ), fmaxf(bN, bC)), bE);
-        if (big > kWinHi || big < kWinLo) {
-          int ex;
-          (void)frexpf(big, &ex);
-          ex = uni(ex);
-          const float s = ldexpf(1.0f, -ex);
+            for (int q = 0; q < 2 * Q; q++) {
+              ec[q] = enx[q];
+              fc[q] = fnx[q];
+            }
+            if (i >= 2) {
+              loadE(enx, res_at(i - 1));   // residue x_i, used by row i-1
+              loadF(fnx, i - 1);
+            }
+          } else {
+            if (!last) loadE(ec, res_at(i));
+            loadF(fc, i);
+          }
+          // u_k = e_k(x_{i+1}) bM_k(i+1), w_k = i_k(x_{i+1}) bI_k(i+1)
+          float u[Q], w[Q];
+          float part = 0.0f;
 #pragma unroll
           for (int q = 0; q < Q; q++) {
-            bM[q] *= s;
-            bI[q] *= s;
+            u[q] = last ? 0.0f : ec[q] * bM[q];
+            w[q] = last ? 0.0f : ec[Q + q] * bI[q];
+            part += u[q];
           }
-          bJ *= s;
-          bN *= s;
-          bC *= s;
-        }
-      };
-      float ea[2 * Q], fa[2 * Q], eb[2 * Q], fb[2 * Q];
+          const float bB = entry_p * wave_sum_f(part);
+          const float nJ = fmaf(loop, bJ, move * bB);
+          const float nN = fmaf(loop, bN, move * bB);
+          const float nC = last ? move : loop * bC;
+          const float bE = 0.5f * (nC + nJ);
+          // terms through cell k+1, formed there and moved down one cell
+          float mmu[Q], imu[Q], dmu[Q];
 #pragma unroll
-      for (int q = 0; q < 2 * Q; q++) ea[q] = 0.0f;   // row L uses no emissions
-      loadF(fa, L);
-      for (int i = L;;) {
-        brow(i, ea, fa, eb, fb);
-        if (--i < 1) break;
-        brow(i, eb, fb, ea, fa);
-        if (--i < 1) break;
+          for (int q = 0; q < Q; q++) {
+            mmu[q] = TB(TR_MMIN, q) * u[q];
+            imu[q] = TB(TR_IMIN, q) * u[q];
+            dmu[q] = TB(TR_DMIN, q) * u[q];
+          }
+          const float mm0 = lane_up_f(mmu[0]), im0 = lane_up_f(imu[0]), dm0 = lane_up_f(dmu[0]);
+          // delete chain D_k = E + DM_k u_{k+1} + DD_k D_{k+1}, within the lane first
+          float dp[Q];
+#pragma unroll
+          for (int q = Q - 1; q >= 0; q--) {
+            const float dmn = q + 1 < Q ? dmu[q + 1] : dm0;
+            dp[q] = q + 1 < Q ? fmaf(TB(TR_DDIN, q + 1), dp[q + 1], bE + dmn) : bE + dmn;
+          }
+          const float carry = lane_up_f(affine_scan(dp[0], psB));
+          float mdb[Q];
+#pragma unroll
+          for (int q = 0; q < Q; q++) mdb[q] = TB(TR_MDIN, q) * fmaf(carry, TB(TR_SUF, q), dp[q]);
+          const float md0 = lane_up_f(mdb[0]);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float mmn = q + 1 < Q ? mmu[q + 1] : mm0;
+            const float imn = q + 1 < Q ? imu[q + 1] : im0;
+            const float mdn = q + 1 < Q ? mdb[q + 1] : md0;
+            bM[q] = bE + mmn + fmaf(TB(TR_MI, q), w[q], mdn);
+            bI[q] = fmaf(TB(TR_II, q), w[q], imn);
+          }
+          bJ = nJ;
+          bN = nN;
+          bC = nC;
+          // ---- posteriors of row i, normalised by the row total
+          float part2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            pm[q] = fc[q] * bM[q];
+            pi[q] = fc[Q + q] * bI[q];
+            part2 += pm[q] + pi[q];
+          }
+          const float sv = spec[(i - 1) * 8 + (lane & 7)];
+          const float fN = readlane_f(sv, 0), fJl = readlane_f(sv, 1), fCl = readlane_f(sv, 2),
+                      fE = readlane_f(sv, 3);
+          const float Zc = wave_sum_f(part2);
+          const float Z = fmaf(fN, bN, fmaf(fJl, bJ, fmaf(fCl, bC, Zc)));
+          const float inv = 1.0f / Z;
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            pm[q] *= inv;
+            pi[q] *= inv;
+          }
+          core = Zc * inv;
+          pend = fE * bE * inv;
+          if (d.pp && lane == 0) d.pp[co + i - 1] = core;
+          sum_end += pend;
+          // rescale the values carried to the next row
+          const float big = fmaxf(fmaxf(fmaxf(bB, bJ), fmaxf(bN, bC)), bE);
+          if (big > kWinHi || big < kWinLo) {
+            int ex;
+            (void)frexpf(big, &ex);
+            ex = uni(ex);
+            const float sc = ldexpf(1.0f, -ex);
+#pragma unroll
+            for (int q = 0; q < Q; q++) {
+              bM[q] *= sc;
+              bI[q] *= sc;
+            }
+            bJ *= sc;
+            bN *= sc;
+            bC *= sc;
+          }
+        }
+        if (i >= 1 && core >= d.rt2) {
+          // ---- one row of the alignment recurrence
+          if (!in_run) {
+            in_run = 1;
+            run_e = i;
+            hit = 0;
+            T = 0.0f;
+            nexp = 0.0f;
+            bestv = kNegInf;
+#pragma unroll
+            for (int q = 0; q < Q; q++) OMn[q] = OIn[q] = kNegInf;
+          }
+          if (core >= d.rt1) hit = 1;
+          nexp += pend;
+          const float Tn = T;
+          float xm[Q], xi[Q], xd[Q];
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            xm[q] = OMn[q] + GB(TR_MMIN, q);
+            xi[q] = OMn[q] + GB(TR_IMIN, q);
+            xd[q] = OMn[q] + GB(TR_DMIN, q);
+          }
+          const float xm0 = lane_up_fill(xm[0], kNegInf), xi0 = lane_up_fill(xi[0], kNegInf),
+                      xd0 = lane_up_fill(xd[0], kNegInf);
+          float dpart[Q];
+#pragma unroll
+          for (int q = Q - 1; q >= 0; q--) {
+            const float fd = q + 1 < Q ? xd[q + 1] : xd0;
+            dpart[q] = q + 1 < Q ? fmaxf(fd, dpart[q + 1] + GB(TR_DDIN, q + 1)) : fd;
+          }
+          const float dcar = lane_up_fill(maxplus_scan(dpart[0], bsB), kNegInf);
+          float yd[Q], zd[Q];
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float od = fmaxf(dpart[q], dcar + GB(TR_SUF, q));
+            yd[q] = od + GB(TR_MDIN, q);   // M_{k-1} -> D_k, formed at cell k
+            zd[q] = od + GB(TR_DDIN, q);   // D_{k-1} -> D_k
+          }
+          const float yd0 = lane_up_fill(yd[0], kNegInf), zd0 = lane_up_fill(zd[0], kNegInf);
+          uint32_t tw[NB];
+#pragma unroll
+          for (int j = 0; j < NB; j++) tw[j] = 0;
+          T = Tn + (1.0f - core);
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const float cm = q + 1 < Q ? xm[q + 1] : xm0;
+            const float ci = OIn[q] + GB(TR_MI, q);
+            const float cd = q + 1 < Q ? yd[q + 1] : yd0;
+            float best = Tn;
+            uint32_t sel = 0;
+            if (cm > best) { best = cm; sel = 1; }
+            if (ci > best) { best = ci; sel = 2; }
+            if (cd > best) { best = cd; sel = 3; }
+            const float nm = pm[q] + best;
+            const float im = q + 1 < Q ? xi[q + 1] : xi0;
+            const float ii = OIn[q] + GB(TR_II, q);
+            const float ni = pi[q] + fmaxf(im, ii);
+            const float dd = q + 1 < Q ? zd[q + 1] : zd0;
+            const float dm = q + 1 < Q ? xd[q + 1] : xd0;
+            tw[q >> 3] |= (sel | (ii > im ? 4u : 0u) | (dd > dm ? 8u : 0u)) << ((q & 7) * 4);
+            OMn[q] = nm;
+            OIn[q] = ni;
+            const float v = nm - T;
+            if (v > bestv && cbase + q < P.M) {
+              bestv = v;
+              besti = i;
+              bestc = cbase + q;
+            }
+          }
+          uint32_t *tr = tbv + (size_t)(i - 1) * NB * kWave + lane;
+#pragma unroll
+          for (int j = 0; j < NB; j++) tr[j * kWave] = tw[j];
+        } else {
+          if (in_run) {
+            // the run [i+1, run_e] ends
+            const int s1 = i + 1, e1 = run_e;
+            if (hit) {
+              const float vmax = wave_max_f(bestv);
+              const int key = wave_min_i32(bestv == vmax ? (besti - 1) * (kWave * Q) + bestc : INT_MAX);
+              const int32_t score = __builtin_bit_cast(int32_t, vmax + T);
+              const int32_t nx = __builtin_bit_cast(int32_t, nexp);
+              if (lane < 6) {
+                const int32_t v = lane == 0 ? s1 : lane == 1 ? e1 : lane == 2 ? key / (kWave * Q) + 1
+                                : lane == 3 ? key % (kWave * Q) : lane == 4 ? score : nx;
+                regs[nreg * 8 + lane] = v;
+              }
+              nreg++;
+            } else if (d.aln) {
+              for (int j = s1 - 1 + lane; j <= e1 - 1; j += kWave) d.aln[co + j] = 0;
+            }
+            in_run = 0;
+          }
+          if (i >= 1 && d.aln && lane == 0) d.aln[co + i - 1] = 0;
+        }
       }
     }
     if (d.exp_dom && lane == 0) d.exp_dom[c] = sum_end;
     wave_fence();
 
-    // ------------------------------------------------ 3. Regions and alignments
-    {
-      float og[TR_N][kR];   // gates of the "into" transitions (forward layout)
-      asm volatile("" : "+v"(trofs));
-      if (!TR_LDS) {
-#pragma unroll
-        for (int k = 0; k < TR_N; k++)
-#pragma unroll
-          for (int q = 0; q < kR; q++) og[k][q] = gate(trl(k, q, lane));
-      }
-      auto GT = [&](int k, int q) -> float { return TR_LDS ? gate(trl(k, q, lane)) : og[k][TR_LDS ? 0 : q]; };
-      auto zero_fill = [&](int from, int to) {   // alignment codes of residues from..to (0-based) = 0
-        if (d.aln)
-          for (int j = from + lane; j <= to; j += kWave) d.aln[co + j] = 0;
+    // ------------------------------------------------ 3. Tracebacks of the regions
+    for (int rg = 0; rg < nreg; rg++) {
+      const int32_t rv = regs[rg * 8 + (lane & 7)];
+      const int s1 = __builtin_amdgcn_readlane(rv, 0), e1 = __builtin_amdgcn_readlane(rv, 1);
+      const int si = __builtin_amdgcn_readlane(rv, 2), sc = __builtin_amdgcn_readlane(rv, 3);
+      const int32_t score = __builtin_amdgcn_readlane(rv, 4), nx = __builtin_amdgcn_readlane(rv, 5);
+      // traceback codes of one diagonal, 64 cells at a time: lane j holds the
+      // word of (row i0 + j, cell c0 + j); a move off that diagonal reloads
+      int i0 = -(1 << 30), c0 = 0;
+      uint32_t pf = 0;
+      auto nib_at = [&](int i, int cc) -> uint32_t {
+        int j = i - i0;
+        if (!(j >= 0 && j < kWave && cc - c0 == j)) {
+          i0 = i;
+          c0 = cc;
+          j = 0;
+          const int il = min(i + lane, maxL);
+          const int cl = min(cc + lane, kWave * Q - 1);
+          const int vq = cl / Q, ql = cl - vq * Q;
+          pf = tbv[((size_t)(il - 1) * NB + (ql >> 3)) * kWave + (63 - vq)];
+        }
+        const uint32_t wd = (uint32_t)__builtin_amdgcn_readlane((int)pf, j);
+        return (wd >> (((cc % Q) & 7) * 4)) & 0xfu;
       };
-      int scan = 0, zpos = 0;
-      for (;;) {
-        // next region [rs, re] (0-based residues) at or after `scan`
-        int rs = -1, re = -1;
-        {
-          int in_run = 0, hit = 0, st0 = 0;
-          for (int base = scan & ~63; base < L && re < 0; base += 64) {
-            const int j = base + lane;
-            const float v = j < L ? pcv[j] : 0.0f;
-            const bool ok = j >= scan && j < L;
-            const uint64_t b2 = __builtin_amdgcn_ballot_w64(ok && v >= d.rt2);
-            const uint64_t b1 = __builtin_amdgcn_ballot_w64(ok && v >= d.rt1);
-            for (int k = 0; k < 64; k++) {
-              const int jj = base + k;
-              if (jj < scan) continue;
-              if (jj >= L) break;
-              if ((b2 >> k) & 1) {
-                if (!in_run) {
-                  in_run = 1;
-                  st0 = jj;
-                  hit = 0;
-                }
-                if ((b1 >> k) & 1) hit = 1;
-              } else if (in_run) {
-                in_run = 0;
-                if (hit) {
-                  rs = st0;
-                  re = jj - 1;
-                  break;
-                }
-              }
-            }
-          }
-          if (re < 0 && in_run && hit) {
-            rs = st0;
-            re = L - 1;
-          }
-        }
-        if (re < 0) break;
-        zero_fill(zpos, rs - 1);
-        zpos = re + 1;
-        scan = re + 1;
-        const int s1 = rs + 1, e1 = re + 1, R = re - rs + 1;   // 1-based region, rows
-
-        // optimal-accuracy recurrence over rows r = 0..R-1 (residue s1 + r)
-        float OM[Q], OI[Q], OD[Q];
-#pragma unroll
-        for (int q = 0; q < Q; q++) OM[q] = OI[q] = OD[q] = kNegInf;
-        float Gp = 0.0f;                     // sum of (1 - core) over the residues before this row
-        float bestv = kNegInf;
-        int bestr = 0, bestq = 0;
-        float pch = 0.0f;
-        int pblk = -1;
-        for (int r = 0; r < R; r++) {
-          if (TR_LDS) asm volatile("" : "+v"(trofs));
-          const int i0 = rs + r;
-          if ((i0 >> 6) != pblk) {
-            pblk = i0 >> 6;
-            const int j = pblk * 64 + lane;
-            pch = j < L ? pcv[j] : 0.0f;
-          }
-          const float gi = 1.0f - readlane_f(pch, i0 & 63);
-          const float *pr = post + (size_t)i0 * kRowF + lane;
-          float pm[Q], pi[Q];
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            pm[q] = pr[q * kWave];
-            pi[q] = pr[(Q + q) * kWave];
-          }
-          const float omL = lane_up_fill(OM[Q - 1], kNegInf);
-          const float oiL = lane_up_fill(OI[Q - 1], kNegInf);
-          const float odL = lane_up_fill(OD[Q - 1], kNegInf);
-          float nOM[Q], nOI[Q];
-          uint32_t tw[NB];
-#pragma unroll
-          for (int j = 0; j < NB; j++) tw[j] = 0;
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const float cm = (q ? OM[q - 1] : omL) + GT(TR_MMIN, q);
-            const float ci = (q ? OI[q - 1] : oiL) + GT(TR_IMIN, q);
-            const float cd = (q ? OD[q - 1] : odL) + GT(TR_DMIN, q);
-            float best = Gp;
-            uint32_t sel = 0;
-            if (cm > best) { best = cm; sel = 1; }
-            if (ci > best) { best = ci; sel = 2; }
-            if (cd > best) { best = cd; sel = 3; }
-            nOM[q] = pm[q] + best;
-            const float jm = OM[q] + GT(TR_MI, q), ji = OI[q] + GT(TR_II, q);
-            const uint32_t seli = ji > jm ? 1u : 0u;
-            nOI[q] = pi[q] + fmaxf(jm, ji);
-            tw[q >> 3] |= (sel | (seli << 2)) << ((q & 7) * 4);
-          }
-          // delete chain of this row: within the lane, then across lanes
-          const float nomL = lane_up_fill(nOM[Q - 1], kNegInf);
-          float dpart[Q];
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const float fm = (q ? nOM[q - 1] : nomL) + GT(TR_MDIN, q);
-            dpart[q] = q ? fmaxf(fm, dpart[q - 1] + GT(TR_DDIN, q)) : fm;
-          }
-          const float dcarry = lane_up_fill(maxplus_scan(dpart[Q - 1], bsO), kNegInf);
-#pragma unroll
-          for (int q = 0; q < Q; q++) OD[q] = fmaxf(dpart[q], dcarry + dpre[q]);
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const float fd = (q ? OD[q - 1] : dcarry) + GT(TR_DDIN, q);
-            const float fm = (q ? nOM[q - 1] : nomL) + GT(TR_MDIN, q);
-            tw[q >> 3] |= (fd > fm ? 8u : 0u) << ((q & 7) * 4);
-          }
-          uint32_t *tr = tbv + (size_t)r * NB * kWave + lane;
-#pragma unroll
-          for (int j = 0; j < NB; j++) tr[j * kWave] = tw[j];
-          const float Gn = Gp + gi;
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const float v = nOM[q] - Gn;
-            if (v > bestv) {
-              bestv = v;
-              bestr = r;
-              bestq = q;
-            }
-            OM[q] = nOM[q];
-            OI[q] = nOI[q];
-          }
-          Gp = Gn;
-        }
-        // the first best end cell in row-major order
-        const float vmax = wave_max_f(bestv);
-        const int key = wave_min_i32(bestv == vmax ? bestr * (kWave * Q) + lane * Q + bestq : INT_MAX);
-        const int br = key / (kWave * Q), bc = key % (kWave * Q);
-        const float score = vmax + Gp;
-        wave_fence();
-
-        // traceback from M at (br, bc); codes collected 64 residues at a time
-        int r = br, cc = bc, st = 0;   // st: 0 = M, 2 = I, 3 = D
-        int a1 = s1, k1 = 1;
-        int cw = re >> 6;
-        int code = 0;
-        auto flush = [&](int w) {
-          const int j = w * 64 + lane;
-          if (d.aln && j >= rs && j <= re) d.aln[co + j] = (int16_t)code;
-          code = 0;
-        };
-        auto put = [&](int i0, int v) {
-          const int w = i0 >> 6;
-          while (cw > w) {
-            flush(cw);
-            cw--;
-          }
-          if (lane == (i0 & 63)) code = v;
-        };
-        for (int guard = 0; guard <= R + kWave * Q; guard++) {
-          if (r < 0 || cc < 0) break;
-          const int cl = cc / Q, q = cc - cl * Q;
-          const uint32_t *tr = tbv + ((size_t)r * NB + (q >> 3)) * kWave;
-          const uint32_t word = (uint32_t)__builtin_amdgcn_readlane((int)tr[lane], cl);
-          const uint32_t nib = (word >> ((q & 7) * 4)) & 0xfu;
-          if (st == 0) {
-            put(rs + r, cc + 1);
-            const uint32_t f = nib & 3u;
-            if (f == 0) {
-              a1 = s1 + r;
-              k1 = cc + 1;
-              break;
-            }
-            r--;
-            cc--;
-            st = f == 1 ? 0 : (int)f;
-          } else if (st == 2) {
-            put(rs + r, -(cc + 1));
-            st = (nib >> 2) & 1u ? 2 : 0;
-            r--;
-          } else {
-            st = (nib >> 3) & 1u ? 3 : 0;
-            cc--;
-          }
-        }
-        while (cw >= (rs >> 6)) {
+      // codes collected 64 residues at a time, stored a window at a time
+      int cw = (s1 - 1) >> 6;
+      int code = 0;
+      auto flush = [&](int wnd) {
+        const int j = wnd * 64 + lane;
+        if (d.aln && j >= s1 - 1 && j <= e1 - 1) d.aln[co + j] = (int16_t)code;
+        code = 0;
+      };
+      auto put = [&](int r0, int v) {
+        const int wnd = r0 >> 6;
+        while (cw < wnd) {
           flush(cw);
-          cw--;
+          cw++;
         }
-        // expected domain ends in the region
-        float acc = 0.0f;
-        for (int j = rs + lane; j <= re; j += kWave) acc += pev[j];
-        const float nexp = wave_sum_f(acc);
-        const int di = wave_fetch_add(&db.counters[CNT_NDOM], 1);
-        if (di < d.max_dom && lane < 9) {
-          const int32_t v = lane == 0 ? c
-                          : lane == 1 ? s1
-                          : lane == 2 ? e1
-                          : lane == 3 ? a1
-                          : lane == 4 ? s1 + br
-                          : lane == 5 ? k1
-                          : lane == 6 ? bc + 1
-                          : lane == 7 ? __builtin_bit_cast(int32_t, score)
-                                      : __builtin_bit_cast(int32_t, nexp);
-          ((int32_t *)(d.dom + di))[lane] = v;
+        if (lane == (r0 & 63)) code = v;
+      };
+      int i = si, cc = sc, st = 0;   // st: 0 = M, 2 = I, 3 = D
+      int b1 = si, k2 = sc + 1;
+      for (int guard = 0; guard <= (e1 - s1 + 1) + kWave * Q; guard++) {
+        if (i > e1 || cc >= P.M) break;
+        const uint32_t nib = nib_at(i, cc);
+        if (st == 0) {
+          put(i - 1, cc + 1);
+          const uint32_t f = nib & 3u;
+          if (f == 0) {
+            b1 = i;
+            k2 = cc + 1;
+            break;
+          }
+          if (f != 3) i++;
+          if (f != 2) cc++;
+          st = f == 1 ? 0 : (int)f;
+        } else if (st == 2) {
+          put(i - 1, -(cc + 1));
+          if ((nib >> 2) & 1u) {
+            i++;
+          } else {
+            i++;
+            cc++;
+            st = 0;
+          }
+        } else {
+          if ((nib >> 3) & 1u) {
+            cc++;
+          } else {
+            i++;
+            cc++;
+            st = 0;
+          }
         }
-        wave_fence();
       }
-      zero_fill(zpos, L - 1);
+      while (cw <= ((e1 - 1) >> 6)) {
+        flush(cw);
+        cw++;
+      }
+      const int di = wave_fetch_add(&db.counters[CNT_NDOM], 1);
+      if (di < d.max_dom && lane < 9) {
+        const int32_t v = lane == 0 ? c : lane == 1 ? s1 : lane == 2 ? e1 : lane == 3 ? si : lane == 4 ? b1
+                        : lane == 5 ? sc + 1 : lane == 6 ? k2 : lane == 7 ? score : nx;
+        ((int32_t *)(d.dom + di))[lane] = v;
+      }
     }
+    wave_fence();
   }
 }
 

@@ -108,11 +108,11 @@ struct DevDecode {
 };
 
 // Dwords of one decode slot for vectors-per-lane Q and targets up to max_len:
-//   posteriors [max_len][2][Q][64], specials [max_len][8], core and end
-//   posteriors [max_len] each, traceback nibbles [max_len][ceil(Q/8)][64].
+//   kept Forward rows [max_len][2][Q][64], their specials [max_len][8],
+//   regions [max_len / 2 + 1][8], traceback codes [max_len][ceil(Q/8)][64].
 inline int64_t decode_slot_dw(int Q, int max_len) {
   const int64_t nb = (Q + 7) / 8;
-  const int64_t dw = (int64_t)max_len * (2 * Q * 64 + 8 + 2 + nb * 64);
+  const int64_t dw = (int64_t)max_len * (2 * Q * 64 + 8 + 4 + nb * 64) + 8;
   return (dw + 63) / 64 * 64;
 }
 
