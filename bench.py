@@ -307,12 +307,24 @@ def bench_decode(hg, P, prof, D, out, stream, args) -> dict:
             "roofline": {"fp32": {"achieved": round(flops / s / 1e12, 3), "peak": PEAK_FP32_TFLOPS,
                                   "unit": "TFLOP/s", "frac": round(flops / s / 1e12 / PEAK_FP32_TFLOPS, 4)},
                          "hbm": {"achieved": round(traffic / s / 1e9, 1), "peak": 8000.0, "unit": "GB/s",
-                                 "frac": round(traffic / s / 8e12, 4)}}}
+                                 "frac": round(traffic / s / 8e12, 4), "design_bytes": traffic,
+                                 "traffic": measured_traffic(args, "decode_traffic_C3.json", "hmm_decode.hip")}}}
 
 
-def kernel_source_sha() -> str:
+def measured_traffic(args, name: str, source: str):
+    """HBM bytes per launch from committed rocprofv3 counter passes, while
+    the kernel source is the one they were taken on (C3 only)."""
+    path = os.path.join(ROOT, "profiles", name)
+    if args.workload != "C3" or args.cutoffs or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        tr = json.load(f)
+    return tr.get("bytes_per_launch") if tr.get("kernel_source_sha") == kernel_source_sha(source) else None
+
+
+def kernel_source_sha(source: str = "hmm_kernels.hip") -> str:
     import hashlib
-    p = os.path.join(ROOT, "paper_2111_06340_amd", "csrc", "hmm_kernels.hip")
+    p = os.path.join(ROOT, "paper_2111_06340_amd", "csrc", source)
     with open(p, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
