@@ -266,3 +266,39 @@ def test_decode_selection_capacity_and_empty():
     assert len(t2) == 3 and t2 <= t3
     D.close()
     P.close()
+
+
+@pytest.mark.parametrize("ci", range(3))
+def test_search_and_decode_match_frozen_oracle_fixtures(ci):
+    """The GPU against the oracle outputs frozen in tests/golden (written by
+    tests/golden/make_golden.py from the oracle alone)."""
+    from test_golden import case_database, case_profile, load_cases
+    c = load_cases()[ci]
+    prof = case_profile(c)
+    res_, off = case_database(c)
+    res, g = run(prof, res_, off, tuple(c["calib"]), tuple(c["cutoffs"]), decode_all=True)
+    op = oracle.OracleProfile(prof)
+    by_t = {}
+    for d in g["doms"]:
+        by_t.setdefault(d["target"], []).append(d)
+    for t, want in enumerate(c["targets"]):
+        L = len(want["residues"])
+        assert int(res["msv"][t]) == want["msv"] and int(res["vit"][t]) == want["vit"]
+        assert int(res["flags"][t]) == want["flags"]
+        assert abs(float(res["fwd"][t]) - want["fwd"]) <= 1e-3 + 1e-5 * abs(want["fwd"])
+        pp = g["pp"][off[t]:off[t + 1]].astype(np.float64)
+        assert np.max(np.abs(pp - np.array(want["core"]))) <= tol_pp(L)
+        gd = by_t.get(t, [])
+        core = np.array(want["core"])
+        amb = np.any(np.abs(core - oracle.RT1) <= tol_pp(L)) or np.any(np.abs(core - oracle.RT2) <= tol_pp(L))
+        if not amb:
+            assert [(d["s"], d["e"]) for d in gd] == [(d["s"], d["e"]) for d in want["domains"]]
+            x = res_[off[t]:off[t + 1]]
+            dec = oracle.decode(op, x)
+            for d, w in zip(gd, want["domains"]):
+                code = g["aln"][off[t] + d["s"] - 1:off[t] + d["e"]].astype(np.int16)
+                sc, ok = oracle.oa_path_score(op, dec, d["s"], d["e"], code)
+                R = d["e"] - d["s"] + 1
+                assert ok and sc >= w["score"] - tol_pp(L) * R - 8 * U * R
+                assert abs(d["score"] - w["score"]) <= tol_pp(L) * R + 8 * U * R
+    announce(f"golden case {ci} M={c['M']}: {len(c['targets'])} targets ok")
