@@ -82,9 +82,12 @@ def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
             "seconds": round(t, 2)}
 
 
-def stage_roofline(M_list, res_total, ran_cells, st_ms):
+def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
     """Per-stage fractions of the relevant VALU peak: algorithmic ops of the
-    cells each stage processed, over its measured time (HIP events)."""
+    cells each stage processed, over its measured time (HIP events).  With
+    a pipelined search (chunks > 1) the later stages overlap the MSV of the
+    next chunk and only their exposed time is measured, so only MSV's
+    fraction is given (run with --pipeline 1 for the others)."""
     msv_ops = MSV_OPS_PER_CELL * sum(M * res_total for M in M_list)
     out = {}
 
@@ -93,6 +96,10 @@ def stage_roofline(M_list, res_total, ran_cells, st_ms):
         return {"achieved": round(ach, 3), "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
 
     out["msv"] = entry(msv_ops, st_ms[0], round(PEAK_PK16_TOPS, 2), "Tops/s packed 16-bit, 4 ops/cell")
+    if chunks > 1:
+        out["note"] = (f"{chunks} pipelined chunks: Viterbi, rescore and Forward overlap the next chunk's MSV; "
+                       f"stage_ms holds their exposed time after the last MSV")
+        return out
     out["viterbi"] = entry(VIT_OPS_PER_CELL * ran_cells["viterbi"], st_ms[1], round(PEAK_PK16_TOPS, 2),
                            "Tops/s packed 16-bit, 18 ops/cell")
     out["rescore"] = entry(RESCORE_OPS_PER_CELL * ran_cells["rescore"], st_ms[2], round(PEAK_I32_TOPS, 2),
@@ -120,6 +127,17 @@ def main():
                     help="run one plain device copy of MB MiB first (scales rocprofv3 byte counters)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "msv_traffic_C3.json"),
                     help="HBM traffic per MSV launch measured by rocprofv3 counters (JSON), if present")
+    ap.add_argument("--streams", type=int, default=0,
+                    help="spread the searches of a step over this many database handles (hmm_db_share) "
+                         "and streams, so that they run concurrently (0 = 4 for C4, else 1)")
+    ap.add_argument("--dbs", type=int, default=1,
+                    help="search this many databases of the workload's recipe (different seeds) per step; "
+                         "with --streams 2, one profile against two databases models the paper's "
+                         "side-by-side MSA searches")
+    ap.add_argument("--pipeline", type=int, default=-1,
+                    help="chunks a search is pipelined in (hmm_db_pipeline; 0 = the library's default, "
+                         "1 = sequential stages, whose per-stage times give per-stage roofline fractions; "
+                         "-1 = 1 for C4, whose 64 searches overlap through --streams, else the default)")
     ap.add_argument("--decode", action="store_true",
                     help="also time posterior decoding (hmm_decode) of the Forward survivors of the last "
                          "search: Forward with rows kept, Backward, regions and alignments (reported "
@@ -139,15 +157,20 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     batched = args.workload == "C4"
+    if args.streams <= 0:
+        args.streams = 4 if batched else 1
+    if args.pipeline < 0:
+        args.pipeline = 1 if batched else 0
     w = gen.WORKLOADS["C3" if batched else args.workload]
     F = tuple(float(v) for v in args.cutoffs.split(",")) if args.cutoffs else w.F
     t = time.perf_counter()
     dbprof = gen.workload_profile(w)
     profs = gen.c4_profiles() if batched else [dbprof]
-    db = gen.workload_database(w, prof=dbprof)
+    dbs = [gen.workload_database(w, prof=dbprof, seed_offset=j) for j in range(args.dbs)]
+    db = dbs[0]
     log(f"generated {args.workload}: {len(profs)} profile(s), M={[p.M for p in profs][:8]}"
-        f"{'...' if len(profs) > 8 else ''}, {db.n} targets, {db.residues.size} residues "
-        f"in {time.perf_counter() - t:.1f}s")
+        f"{'...' if len(profs) > 8 else ''}, {len(dbs)} database(s) of {db.n} targets, "
+        f"{sum(d.residues.size for d in dbs)} residues in {time.perf_counter() - t:.1f}s")
     t = time.perf_counter()
     if args.calib:
         assert not batched, "--calib gives one profile's calibration"
@@ -158,11 +181,22 @@ def main():
         f"{calibs[0]!r}{' ...' if batched else ''}")
     Ps = [hg.Profile(p, *c) for p, c in zip(profs, calibs)]
     t = time.perf_counter()
-    D = hg.Database(db.residues, db.offsets)
+    Ds = [hg.Database(d.residues, d.offsets) for d in dbs]
+    D = Ds[0]
+    chunks = [hg.hmm_db_pipeline(Dx.handle, args.pipeline) for Dx in Ds][0]
     upload_s = time.perf_counter() - t
-    log(f"database packed and uploaded in {upload_s:.2f}s (host buffers, PCIe included; not timed below)")
-    outs = [hg.alloc_results(D.n) for _ in Ps]
-    stream = torch.cuda.current_stream()
+    log(f"database(s) packed and uploaded in {upload_s:.2f}s (host buffers, PCIe included; not timed below)")
+    # search jobs (profile, database) spread round-robin over `streams` lanes;
+    # lane j searches through its own handle of every database, on its own stream
+    S = max(1, args.streams)
+    lanes = [[Dx if j == 0 else Dx.share() for Dx in Ds] for j in range(S)]
+    for lane in lanes[1:]:
+        for h in lane:
+            hg.hmm_db_pipeline(h.handle, chunks)
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(S - 1)]
+    jobs = [(pi, di) for pi in range(len(Ps)) for di in range(len(Ds))]
+    outs = [hg.alloc_results(Ds[di].n) for _, di in jobs]
+    stream = streams[0]
     if args.copy_probe:
         src = torch.ones(args.copy_probe << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -173,29 +207,36 @@ def main():
         del src, dst
 
     def step():
-        for P, out in zip(Ps, outs):
-            hg.search(P, D, F, out, stream=stream)
+        for i, ((pi, di), out) in enumerate(zip(jobs, outs)):
+            j = i % S
+            hg.search(Ps[pi], lanes[j][di], F, out, stream=streams[j])
 
+    timed_stages = S == 1 and len(Ds) == 1
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    hg.hmm_db_stage_timing(D.handle, args.steps * len(Ps))
+    if timed_stages:
+        hg.hmm_db_stage_timing(D.handle, args.steps * len(Ps))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     total = time.perf_counter() - t0
-    stages = hg.hmm_db_stage_times(D.handle, args.steps * len(Ps))
-    hg.hmm_db_stage_timing(D.handle, 0)
+    if timed_stages:
+        stages = hg.hmm_db_stage_times(D.handle, args.steps * len(Ps))
+        hg.hmm_db_stage_timing(D.handle, 0)
+    else:
+        stages = np.zeros((0, 4))
     ms_step = total / args.steps * 1e3
     M_list = [p.M for p in profs]
-    cells = sum(M_list) * D.n_residues
+    cells = sum(M_list) * sum(Dx.n_residues for Dx in Ds)
     gcups = cells / (ms_step / 1e3) / 1e9
-    lengths = np.diff(db.offsets)
     counts = np.zeros(4, np.int64)
     ran = {"viterbi": 0, "rescore": 0, "forward": 0}
-    for p, out in zip(profs, outs):
+    for (pi, di), out in zip(jobs, outs):
+        p = profs[pi]
+        lengths = np.diff(dbs[di].offsets)
         counts += out["counts"].cpu().numpy()
         fl = out["flags"].cpu().numpy()
         ran["viterbi"] += p.M * int(lengths[(fl & hg.HMM_VIT_RAN) != 0].sum())
@@ -206,7 +247,7 @@ def main():
     st_ms = [float(v) for v in
              (stages.reshape(-1, len(Ps), 4).sum(axis=1).mean(axis=0) if stages.size else np.zeros(4))]
     msv_ms = float(st_ms[0])
-    achieved = MSV_OPS_PER_CELL * cells / (msv_ms / 1e3) / 1e12
+    achieved = MSV_OPS_PER_CELL * cells / (msv_ms / 1e3) / 1e12 if msv_ms > 0 else 0.0
     log(f"{ms_step:.3f} ms/step, {gcups:.1f} GCUPS; stages ms: MSV {st_ms[0]:.3f} Viterbi {st_ms[1]:.3f} "
         f"rescore {st_ms[2]:.3f} (concurrent with) Forward {st_ms[3]:.3f}; counts {counts}")
     traffic = None
@@ -221,6 +262,11 @@ def main():
     else:
         wl = (f"{w.name}: Plan7 profile M={profs[0].M} vs {D.n} synthetic sequences ({D.n_residues} residues, "
               f"{w.planted * 100:g}% planted homologs)")
+    if len(Ds) > 1:
+        wl += (f", against {len(Ds)} databases of this recipe (different seeds; "
+               f"{sum(Dx.n_residues for Dx in Ds)} residues in all)")
+    if S > 1:
+        wl += f", searches spread over {S} concurrent streams and database handles"
     wl += f", MSV P<{F[0]:g} -> Viterbi P<{F[1]:g} -> Forward"
     rec = {
         "metric": "GCUPS (profile cols x DB residues /s), MSV+Viterbi+Forward, M=734 vs 1M seqs",
@@ -236,7 +282,7 @@ def main():
         "dtype": "u8/i16/i32/f32",
         "data": "synthetic",
         "config": {"workload": wl, "M": M_list if batched else M_list[0], "n_seqs": D.n,
-                   "residues": D.n_residues, "cutoffs": list(F)},
+                   "residues": D.n_residues, "cutoffs": list(F), "databases": len(Ds), "streams": S},
         # rescore and Forward run concurrently after Viterbi: both are timed
         # from Viterbi's end, Forward until both are done
         "stage_ms": {"msv": round(float(st_ms[0]), 4), "viterbi": round(float(st_ms[1]), 4),
@@ -247,19 +293,27 @@ def main():
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
                      "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic,
-                     "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_launch": cells // len(Ps)},
-        "stage_roofline": stage_roofline(M_list, D.n_residues, ran, st_ms),
+                     "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
+                     "msv_launches_per_search": chunks}
+        if timed_stages else None,
+        "stage_roofline": stage_roofline(M_list, D.n_residues, ran, st_ms, chunks) if timed_stages else None,
+        "pipeline_chunks": chunks,
         "upload_s": round(upload_s, 3),
         "calib": list(calibs[0]),
     }
     if batched:
         rec["queries_per_hour"] = round(len(Ps) / (ms_step / 1e3) * 3600.0, 1)
     if args.decode:
-        rec["decode"] = bench_decode(hg, Ps[-1], profs[-1], D, outs[-1], stream, args)
+        pi, di = jobs[-1]
+        rec["decode"] = bench_decode(hg, Ps[pi], profs[pi], Ds[di], outs[-1], stream, args)
     for P in Ps:
         P.close()
-    D.close()
-    if not args.no_cpu_baseline and not batched:
+    for lane in lanes[1:]:
+        for h in lane:
+            h.close()
+    for Dx in Ds:
+        Dx.close()
+    if not args.no_cpu_baseline and not batched and len(Ds) == 1:
         threads = min(16, len(os.sched_getaffinity(0)))
         log(f"CPU oracle baseline on {threads} threads ...")
         rec["cpu_baseline"] = cpu_baseline(profs[0], db, F, args.cpu_seconds, threads)

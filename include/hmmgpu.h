@@ -136,16 +136,29 @@ int hmm_profile_free(hmm_profile *p);
 int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n_seqs,
                   hmm_stream stream, hmm_db **out);
 
-/* Release a database (NULL is a no-op); waits for its last search. */
+/* Release a database handle (NULL is a no-op); waits for its last search.
+ * The packed residues are released with the last handle that uses them. */
 int hmm_db_free(hmm_db *db);
+
+/* A second handle on the same database, for concurrent searches (the paper,
+ * Design section, runs the MSA searches side by side instead of one after
+ * another).  The new handle shares the packed residues and index arrays of
+ * `db` (no copy, no host synchronisation) and owns its own search scratch,
+ * streams and events: searches on different handles are independent and
+ * run concurrently when enqueued on different streams, while searches on
+ * one handle stay serialised.  Free every handle with hmm_db_free, in any
+ * order.  Errors: HMM_EINVAL (NULL), HMM_ENOMEM, HMM_EDEVICE. */
+int hmm_db_share(const hmm_db *db, hmm_db **out);
 
 /* Search one profile against a database: MSV on every target, Viterbi on
  * MSV survivors, int32 rescore of int16-overflowed targets, Forward on
  * Viterbi survivors.  Enqueued on `stream` without host synchronisation
  * (except when the cutoffs change, see below); allocates nothing.  The
- * rescore runs on a stream owned by the database, forked from `stream`
- * after the int16 Viterbi and joined back before the search ends, so all
- * of the search's work is ordered on `stream`.
+ * search runs pipelined in chunks of the database (hmm_db_pipeline): the
+ * MSV kernels run on `stream`; Viterbi and Forward of each chunk on a
+ * stream owned by the database handle and the int32 rescore on another,
+ * forked from `stream` and joined back before the search ends, so all of
+ * the search's work is ordered on `stream`.
  * Searches on one database are serialised by the library (a search on a
  * second stream waits for the previous one on the GPU).  Changing the
  * cutoffs or the profile between searches on a database rebuilds a small
@@ -241,6 +254,18 @@ int hmm_db_stage_timing(hmm_db *db, int32_t capacity);
  * their number in *n.  Waits for the recorded searches to finish and
  * clears the record.  Errors: HMM_EINVAL, HMM_EDEVICE. */
 int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n);
+
+/* Tuning hook: the number of chunks (1..8) a search on this handle is
+ * pipelined in.  The length-sorted targets are split into that many
+ * contiguous ranges of about equal residue counts; the MSV kernels of the
+ * chunks run back to back on the search stream while the Viterbi, rescore
+ * and Forward of each finished chunk run on the handle's own streams beside
+ * them.  Results do not depend on it.  chunks = 0 changes nothing;
+ * *current (if non-NULL) receives the count in force.  The default is 2 for
+ * databases of at least 8 Mi residues, else 1 (plain sequential stages,
+ * which is what per-stage timing needs).
+ * Errors: HMM_EINVAL (NULL db, chunks outside 0..8). */
+int hmm_db_pipeline(hmm_db *db, int32_t chunks, int32_t *current);
 
 /* Database properties: number of targets, total residues, longest target. */
 int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t *max_len);

@@ -27,7 +27,8 @@ HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, 
 HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float32 in the library)
 
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
-            "hmm_debug_length_params", "hmm_debug_tables", "hmm_decode", "hmm_last_error", "hmm_profile_free",
+            "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables", "hmm_decode", "hmm_last_error",
+            "hmm_profile_free",
             "hmm_profile_upload", "hmm_search", "hmm_strerror")
 
 
@@ -79,6 +80,10 @@ def lib():
         L.hmm_db_upload.argtypes = [vp, vp, i64, vp, C.POINTER(vp)]
         L.hmm_db_free.restype = C.c_int
         L.hmm_db_free.argtypes = [vp]
+        L.hmm_db_pipeline.restype = C.c_int
+        L.hmm_db_pipeline.argtypes = [vp, i32, C.POINTER(i32)]
+        L.hmm_db_share.restype = C.c_int
+        L.hmm_db_share.argtypes = [vp, C.POINTER(vp)]
         L.hmm_search.restype = C.c_int
         L.hmm_search.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), vp]
         L.hmm_decode.restype = C.c_int
@@ -156,6 +161,20 @@ def hmm_db_upload(residues, offsets, stream=None) -> int:
 
 def hmm_db_free(handle: int) -> None:
     _check(lib().hmm_db_free(C.c_void_p(handle)), "hmm_db_free")
+
+
+def hmm_db_pipeline(handle: int, chunks: int = 0) -> int:
+    """Set (chunks > 0) and return the number of pipelined chunks of a search."""
+    cur = C.c_int32(0)
+    _check(lib().hmm_db_pipeline(C.c_void_p(handle), int(chunks), C.byref(cur)), "hmm_db_pipeline")
+    return cur.value
+
+
+def hmm_db_share(handle: int) -> int:
+    """A second handle on the same packed database, with its own scratch."""
+    h = C.c_void_p(0)
+    _check(lib().hmm_db_share(C.c_void_p(handle), C.byref(h)), "hmm_db_share")
+    return h.value
 
 
 def hmm_db_info(handle: int) -> tuple[int, int, int]:
@@ -260,10 +279,18 @@ class Profile:
 class Database:
     """Owning wrapper of a device database."""
 
-    def __init__(self, residues, offsets, stream=None):
-        self.handle = hmm_db_upload(residues, offsets, stream)
+    def __init__(self, residues, offsets, stream=None, _share_of=None):
+        if _share_of is not None:
+            self.handle = hmm_db_share(_share_of.handle)
+            self._lengths = _share_of._lengths
+        else:
+            self.handle = hmm_db_upload(residues, offsets, stream)
+            self._lengths = np.diff(np.asarray(offsets, dtype=np.int64))
         self.n, self.n_residues, self.max_len = hmm_db_info(self.handle)
-        self._lengths = np.diff(np.asarray(offsets, dtype=np.int64))
+
+    def share(self) -> "Database":
+        """Another handle on the same device database, for concurrent searches."""
+        return Database(None, None, _share_of=self)
 
     def lengths_caller(self):
         """Target lengths in the caller's order (host array)."""

@@ -99,10 +99,17 @@ struct hmm_profile {
   void *dmem = nullptr;  // one device allocation holding every table
 };
 
+// Packed residues and index arrays of a database, shared by its handles.
+struct hmm_db_data {
+  void *dmem = nullptr;
+  std::atomic<int> refs{1};
+};
+
 struct hmm_db {
   int64_t n = 0, n_res = 0;
   int32_t max_len = 0;
-  void *dmem = nullptr;  // packed residues + index arrays + scratch
+  hmm_db_data *data = nullptr;  // shared with the handles made by hmm_db_share
+  void *smem = nullptr;         // this handle's search scratch
   DevDb dev{};
   LenParams *h_lp = nullptr;  // pinned staging of the per-length table
   LenParams *d_lp = nullptr;
@@ -111,11 +118,12 @@ struct hmm_db {
   double lp_F[3] = {-1, -1, -1};
   hipEvent_t done = nullptr;   // completion of the latest search
   bool searched = false;
-  // The int32 rescore runs on `aux`, concurrently with Forward on the search
-  // stream, between the events fork (recorded on the search stream) and
-  // join (recorded on aux).
-  hipStream_t aux = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  // Streams and events of the pipelined cascade (see SearchSync), and the
+  // chunking: `chunks` contiguous ranges of the sorted targets, range k =
+  // [chunk_at[chunks][k], chunk_at[chunks][k+1]), of about equal residues.
+  SearchSync sync;
+  int chunks = 1;
+  int64_t chunk_at[kMaxChunks + 1][kMaxChunks + 1] = {};
   // posterior-decoding scratch (allocated by the first hmm_decode)
   void *dec_mem = nullptr;
   size_t dec_bytes = 0;
@@ -505,6 +513,48 @@ void length_params(const hmm_profile *p, const hmm_thresholds *t, int L, LenPara
 
 }  // namespace
 
+// The search scratch of one database handle (flags, survivor lists,
+// counters, per-length table), its pinned staging of that table, and the
+// streams and events that order its searches.
+static int attach_scratch(hmm_db *db) {
+  auto al = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t n = (size_t)db->n;
+  const size_t sz_u8 = al(n + 1), sz_i32 = al(n * 4 + 4);
+  const size_t sz_lp = al(sizeof(LenParams) * ((size_t)db->max_len + 1));
+  const size_t o_flags = 0, o_lv = o_flags + sz_u8, o_lo = o_lv + sz_i32, o_lf = o_lo + sz_i32;
+  const size_t o_cnt = o_lf + sz_i32, o_lp = o_cnt + al(kMaxChunks * CNT_N * 4), total = o_lp + sz_lp;
+  hipError_t e = hipMalloc(&db->smem, total);
+  if (e != hipSuccess) {
+    db->smem = nullptr;
+    return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "device allocation of %zu bytes failed", total)
+                                    : fail_hip(e, "hipMalloc(db scratch)");
+  }
+  e = hipMemset(db->smem, 0, total);
+  if (e == hipSuccess) e = hipHostMalloc((void **)&db->h_lp, sz_lp, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->done, hipEventDisableTiming);
+  SearchSync &y = db->sync;
+  for (int k = 0; k < kMaxChunks && e == hipSuccess; k++) {
+    e = hipEventCreateWithFlags(&y.msv_done[k], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&y.vit_done[k], hipEventDisableTiming);
+  }
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&y.aux_done, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&y.tail_done, hipEventDisableTiming);
+  // default priority, like every stream here
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&y.tail, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&y.aux, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail_hip(e, "database scratch");
+  uint8_t *b = (uint8_t *)db->smem;
+  DevDb &dv = db->dev;
+  dv.flags_sorted = b + o_flags;
+  dv.list_vit = (int32_t *)(b + o_lv);
+  dv.list_ovf = (int32_t *)(b + o_lo);
+  dv.list_fwd = (int32_t *)(b + o_lf);
+  dv.counters = (int32_t *)(b + o_cnt);
+  db->d_lp = (LenParams *)(b + o_lp);
+  dv.lp = db->d_lp;
+  return HMM_OK;
+}
+
 extern "C" {
 
 int hmm_debug_length_params(const hmm_profile_desc *d, const hmm_thresholds *t, int32_t L, int32_t *i32,
@@ -566,20 +616,43 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
     pos += ((int64_t)L + 15) / 16 * 16;
   }
   const int64_t res_bytes = pos + 1024;  // residue streams read up to 768 bytes past a target
+  // chunk boundaries for every chunk count: about equal residues per chunk
+  int64_t chunk_at[kMaxChunks + 1][kMaxChunks + 1] = {};
+  for (int K = 1; K <= kMaxChunks; K++) {
+    int64_t acc = 0, i = 0;
+    chunk_at[K][0] = 0;
+    for (int k = 1; k < K; k++) {
+      const int64_t goal = n_res * k / K;
+      while (i < n && acc + len[i] <= goal) acc += len[i++];
+      chunk_at[K][k] = std::max(i, chunk_at[K][k - 1]);
+    }
+    chunk_at[K][K] = n;
+  }
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   const size_t sz_res = al((size_t)res_bytes);
-  const size_t sz_start = al((size_t)n * 8 + 8), sz_i32 = al((size_t)n * 4 + 4), sz_u8 = al((size_t)n + 1);
-  const size_t sz_lp = al(sizeof(LenParams) * ((size_t)max_len + 1));
-  const size_t total = sz_res + sz_start * 2 + sz_i32 * 2 + sz_u8 + sz_i32 * 3 + al(CNT_N * 4) + sz_lp;
+  const size_t sz_start = al((size_t)n * 8 + 8), sz_i32 = al((size_t)n * 4 + 4);
+  const size_t total = sz_res + sz_start * 2 + sz_i32 * 2;
 
   hmm_db *db = new (std::nothrow) hmm_db();
   if (!db) return fail(HMM_ENOMEM, "host allocation failed");
   db->n = n;
   db->n_res = n_res;
   db->max_len = max_len;
+  memcpy(db->chunk_at, chunk_at, sizeof chunk_at);
+  // Pipelining pays once a chunk's MSV outlasts the tail it hides.  Two
+  // chunks measured best on a 348M-residue database: each MSV kernel fills
+  // every CU's LDS, so a chunk's Viterbi runs mostly after the next MSV and
+  // more chunks only add MSV launches.
+  db->chunks = n_res >= ((int64_t)8 << 20) ? 2 : 1;
+  db->data = new (std::nothrow) hmm_db_data();
+  if (!db->data) {
+    delete db;
+    return fail(HMM_ENOMEM, "host allocation failed");
+  }
   uint8_t *stage = nullptr;
   hipError_t e = hipHostMalloc((void **)&stage, total, hipHostMallocDefault);
   if (e != hipSuccess) {
+    delete db->data;
     delete db;
     return fail(HMM_ENOMEM, "pinned staging of %zu bytes failed: %s", total, hipGetErrorString(e));
   }
@@ -600,18 +673,6 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   const size_t o_coff = off;
   int64_t *s_coff = (int64_t *)(stage + off);
   off += sz_start;
-  const size_t o_flags = off;
-  off += sz_u8;
-  const size_t o_lv = off;
-  off += sz_i32;
-  const size_t o_lo = off;
-  off += sz_i32;
-  const size_t o_lf = off;
-  off += sz_i32;
-  const size_t o_cnt = off;
-  off += al(CNT_N * 4);
-  const size_t o_lp = off;
-  off += sz_lp;
   for (int64_t i = 0; i < n; i++) {
     memcpy(s_res + start[i], residues + offsets[order[i]], (size_t)len[i]);
     s_start[i] = start[i];
@@ -619,29 +680,24 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
     s_perm[i] = order[i];
     s_coff[i] = offsets[order[i]];
   }
-  e = hipMalloc(&db->dmem, total);
+  e = hipMalloc(&db->data->dmem, total);
   if (e != hipSuccess) {
     (void)hipHostFree(stage);
+    delete db->data;
     delete db;
     return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "device allocation of %zu bytes failed", total)
                                     : fail_hip(e, "hipMalloc(db)");
   }
-  e = hipMemcpyAsync(db->dmem, stage, o_flags, hipMemcpyHostToDevice, (hipStream_t)stream);
+  e = hipMemcpyAsync(db->data->dmem, stage, total, hipMemcpyHostToDevice, (hipStream_t)stream);
   if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
   (void)hipHostFree(stage);
-  if (e == hipSuccess) e = hipHostMalloc((void **)&db->h_lp, sz_lp, hipHostMallocDefault);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->done, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&db->join, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipStreamCreateWithFlags(&db->aux, hipStreamNonBlocking);
   if (e != hipSuccess) {
-    release_sync(db);
-    (void)hipFree(db->dmem);
-    if (db->h_lp) (void)hipHostFree(db->h_lp);
+    (void)hipFree(db->data->dmem);
+    delete db->data;
     delete db;
     return fail_hip(e, "database upload");
   }
-  uint8_t *b = (uint8_t *)db->dmem;
+  uint8_t *b = (uint8_t *)db->data->dmem;
   DevDb &dv = db->dev;
   dv.n = n;
   dv.max_len = max_len;
@@ -650,24 +706,50 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   dv.len = (const int32_t *)(b + o_len);
   dv.perm = (const int32_t *)(b + o_perm);
   dv.coff = (const int64_t *)(b + o_coff);
-  dv.flags_sorted = b + o_flags;
-  dv.list_vit = (int32_t *)(b + o_lv);
-  dv.list_ovf = (int32_t *)(b + o_lo);
-  dv.list_fwd = (int32_t *)(b + o_lf);
-  dv.counters = (int32_t *)(b + o_cnt);
-  db->d_lp = (LenParams *)(b + o_lp);
-  dv.lp = db->d_lp;
+  const int rc = attach_scratch(db);
+  if (rc != HMM_OK) {
+    (void)hmm_db_free(db);
+    return rc;
+  }
+  *out = db;
+  return HMM_OK;
+}
+
+int hmm_db_share(const hmm_db *src, hmm_db **out) {
+  if (!src || !out) return fail(HMM_EINVAL, "NULL db or out");
+  *out = nullptr;
+  hmm_db *db = new (std::nothrow) hmm_db();
+  if (!db) return fail(HMM_ENOMEM, "host allocation failed");
+  db->n = src->n;
+  db->n_res = src->n_res;
+  db->max_len = src->max_len;
+  db->data = src->data;
+  db->data->refs.fetch_add(1);
+  db->chunks = src->chunks;
+  memcpy(db->chunk_at, src->chunk_at, sizeof db->chunk_at);
+  db->dev = src->dev;   // shared residues and index arrays; attach_scratch replaces the rest
+  const int rc = attach_scratch(db);
+  if (rc != HMM_OK) {
+    (void)hmm_db_free(db);
+    return rc;
+  }
   *out = db;
   return HMM_OK;
 }
 
 static void release_sync(hmm_db *db) {
-  if (db->aux) (void)hipStreamDestroy(db->aux);
-  if (db->join) (void)hipEventDestroy(db->join);
-  if (db->fork) (void)hipEventDestroy(db->fork);
+  SearchSync &y = db->sync;
+  if (y.tail) (void)hipStreamDestroy(y.tail);
+  if (y.aux) (void)hipStreamDestroy(y.aux);
+  for (int k = 0; k < kMaxChunks; k++) {
+    if (y.msv_done[k]) (void)hipEventDestroy(y.msv_done[k]);
+    if (y.vit_done[k]) (void)hipEventDestroy(y.vit_done[k]);
+  }
+  if (y.aux_done) (void)hipEventDestroy(y.aux_done);
+  if (y.tail_done) (void)hipEventDestroy(y.tail_done);
   if (db->done) (void)hipEventDestroy(db->done);
-  db->aux = nullptr;
-  db->join = db->fork = db->done = nullptr;
+  db->sync = SearchSync{};
+  db->done = nullptr;
 }
 
 static void drop_timing(hmm_db *db) {
@@ -724,10 +806,23 @@ int hmm_db_free(hmm_db *db) {
   release_sync(db);
   if (db->h_lp) (void)hipHostFree(db->h_lp);
   if (db->dec_mem) (void)hipFree(db->dec_mem);
-  hipError_t e2 = db->dmem ? hipFree(db->dmem) : hipSuccess;
+  hipError_t e2 = db->smem ? hipFree(db->smem) : hipSuccess;
+  if (db->data && db->data->refs.fetch_sub(1) == 1) {
+    const hipError_t e3 = db->data->dmem ? hipFree(db->data->dmem) : hipSuccess;
+    if (e2 == hipSuccess) e2 = e3;
+    delete db->data;
+  }
   delete db;
   if (e != hipSuccess) return fail_hip(e, "hipEventSynchronize(db)");
   if (e2 != hipSuccess) return fail_hip(e2, "hipFree(db)");
+  return HMM_OK;
+}
+
+int hmm_db_pipeline(hmm_db *db, int32_t chunks, int32_t *current) {
+  if (!db) return fail(HMM_EINVAL, "db is NULL");
+  if (chunks < 0 || chunks > kMaxChunks) return fail(HMM_EINVAL, "chunks = %d; need 0..%d", chunks, kMaxChunks);
+  if (chunks > 0) db->chunks = chunks;   // searches on a handle are serialised on the GPU
+  if (current) *current = db->chunks;
   return HMM_OK;
 }
 
@@ -765,7 +860,10 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts};
   hipEvent_t *ev = nullptr;
   if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
-  HIP_TRY(launch_search(p->dev, db->dev, o, s, db->aux, db->fork, db->join, ev), "kernel launch");
+  DevDb chunk[kMaxChunks];
+  const int K = db->chunks;
+  for (int k = 0; k < K; k++) chunk[k] = chunk_of(db->dev, db->chunk_at[K][k], db->chunk_at[K][k + 1], k);
+  HIP_TRY(launch_search(p->dev, chunk, K, o, s, db->sync, ev), "kernel launch");
   HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
   db->searched = true;
   return HMM_OK;

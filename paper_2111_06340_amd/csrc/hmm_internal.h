@@ -122,14 +122,48 @@ int decode_max_waves(const DevProfile &p);
 // Enqueue the decode of the selected targets on `stream` (d.nslots waves).
 hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t stream);
 
-// Enqueue the whole cascade on `stream`.  The int32 rescore runs on `aux`,
-// concurrently with Forward: it forks after the int16 Viterbi (event
-// `fork`) and joins before the final counter export (event `join`), so all
-// work stays ordered on `stream`.  When `ev` is non-null, ev[0..4] are
-// recorded at the start, after MSV, after Viterbi (the fork), after the
-// rescore (on aux) and after the join.
-hipError_t launch_search(const DevProfile &p, const DevDb &db, const DevOut &out, hipStream_t stream,
-                         hipStream_t aux, hipEvent_t fork, hipEvent_t join, hipEvent_t *ev);
+// A search runs in up to kMaxChunks chunks of the length-sorted database
+// (contiguous ranges of about equal residue counts), pipelined: the MSV
+// kernels of the chunks run back to back on the search stream, and the rest
+// of each chunk's cascade (Viterbi, then Forward, with the int32 rescore
+// beside it) on a second stream as soon as the chunk's MSV is done, so it
+// overlaps the next chunk's MSV.  Each chunk has its own counter block and
+// keeps its survivor lists inside its own index range.
+constexpr int kMaxChunks = 8;
+
+// Streams and events that order one database handle's searches.
+struct SearchSync {
+  hipStream_t tail = nullptr;           // Viterbi and Forward of the chunks
+  hipStream_t aux = nullptr;            // int32 rescore, beside Forward
+  hipEvent_t msv_done[kMaxChunks] = {}; // recorded on the search stream
+  hipEvent_t vit_done[kMaxChunks] = {}; // recorded on tail
+  hipEvent_t aux_done = nullptr, tail_done = nullptr;
+};
+
+// The sorted targets [a, b) as a database of their own, with counter block k.
+inline DevDb chunk_of(const DevDb &d, int64_t a, int64_t b, int k) {
+  DevDb c = d;
+  c.n = b - a;
+  c.start += a;
+  c.len += a;
+  c.perm += a;
+  c.coff += a;
+  c.flags_sorted += a;
+  c.list_vit += a;
+  c.list_ovf += a;
+  c.list_fwd += a;
+  c.counters += (size_t)k * CNT_N;
+  return c;
+}
+
+// Enqueue the whole cascade of the chunks chunk[0..nchunks) on `stream`;
+// all of its work is joined back into `stream` before the final counter
+// export (the sum over the chunks' counter blocks, which start at
+// chunk[0].counters).  When `ev` is non-null, ev[0..4] are recorded at the
+// start and after the last MSV (search stream), after the last Viterbi
+// (tail), after the last rescore (aux) and at the end (search stream).
+hipError_t launch_search(const DevProfile &p, const DevDb *chunk, int nchunks, const DevOut &out,
+                         hipStream_t stream, const SearchSync &sync, hipEvent_t *ev);
 
 // Number of packed vectors per lane.
 inline int q8_of(int M) { return (M + 2 * kWave - 1) / (2 * kWave); }

@@ -642,16 +642,21 @@ __global__ void __launch_bounds__(kThreads32<Q>) fwd_kernel(DevProfile P, DevDb 
 
 // ============================================================================ small kernels
 
-__global__ void clear_counters(int32_t *c) {
-  if (threadIdx.x < CNT_N) c[threadIdx.x] = 0;
+__global__ void clear_counters(int32_t *c, int nblocks) {
+  for (int i = threadIdx.x; i < nblocks * CNT_N; i += blockDim.x) c[i] = 0;
 }
 
-__global__ void export_counts(const int32_t *c, int64_t *counts) {
+__global__ void export_counts(const int32_t *c, int nblocks, int64_t *counts) {
   if (threadIdx.x == 0) {
-    counts[0] = c[CNT_VIT];
-    counts[1] = c[CNT_OVF];
-    counts[2] = c[CNT_FWD];
-    counts[3] = c[CNT_FWD_PASS];
+    int64_t v[4] = {0, 0, 0, 0};
+    for (int k = 0; k < nblocks; k++) {
+      const int32_t *b = c + k * CNT_N;
+      v[0] += b[CNT_VIT];
+      v[1] += b[CNT_OVF];
+      v[2] += b[CNT_FWD];
+      v[3] += b[CNT_FWD_PASS];
+    }
+    for (int i = 0; i < 4; i++) counts[i] = v[i];
   }
 }
 
@@ -820,32 +825,46 @@ hipError_t dispatch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, h
 
 }  // namespace
 
-hipError_t launch_search(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s, hipStream_t aux,
-                         hipEvent_t fork, hipEvent_t join, hipEvent_t *ev) {
-  if (db.n <= 0) return hipSuccess;
+hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const DevOut &o, hipStream_t s,
+                         const SearchSync &y, hipEvent_t *ev) {
+  if (K < 1 || K > kMaxChunks) return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+    return e == hipSuccess;
+  };
   auto mark = [&](int i, hipStream_t st) {
-    if (ev && e == hipSuccess) e = hipEventRecord(ev[i], st);
+    if (ev) ok(hipEventRecord(ev[i], st));
   };
   mark(0, s);
-  hipLaunchKernelGGL(clear_counters, dim3(1), dim3(64), 0, s, db.counters);
-  e = hipGetLastError();
-  if (e == hipSuccess) e = dispatch_msv(P, db, o, s);
+  hipLaunchKernelGGL(clear_counters, dim3(1), dim3(256), 0, s, chunk[0].counters, K);
+  ok(hipGetLastError());
+  // MSV of every chunk, back to back on the search stream
+  for (int k = 0; k < K && e == hipSuccess; k++) {
+    if (chunk[k].n > 0) ok(dispatch_msv(P, chunk[k], o, s));
+    ok(hipEventRecord(y.msv_done[k], s));
+  }
   mark(1, s);
-  if (e == hipSuccess) e = dispatch_vit16(P, db, o, s);
-  mark(2, s);
-  // An int16 overflow passes the Viterbi filter whatever its exact score,
-  // so Forward needs nothing from the rescore: the two run side by side.
-  if (e == hipSuccess) e = hipEventRecord(fork, s);
-  if (e == hipSuccess) e = hipStreamWaitEvent(aux, fork, 0);
-  if (e == hipSuccess) e = dispatch_vit32(P, db, o, aux);
-  mark(3, aux);
-  if (e == hipSuccess) e = dispatch_fwd(P, db, o, s);
-  if (e == hipSuccess) e = hipEventRecord(join, aux);
-  if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+  // the rest of each chunk's cascade as soon as its MSV is done.  An int16
+  // overflow passes the Viterbi filter whatever its exact score, so Forward
+  // needs nothing from the rescore: the two run side by side.
+  for (int k = 0; k < K && e == hipSuccess; k++) {
+    const bool any = chunk[k].n > 0;
+    if (!ok(hipStreamWaitEvent(y.tail, y.msv_done[k], 0))) break;
+    if (any && !ok(dispatch_vit16(P, chunk[k], o, y.tail))) break;
+    if (!ok(hipEventRecord(y.vit_done[k], y.tail))) break;
+    if (k == K - 1) mark(2, y.tail);
+    if (!ok(hipStreamWaitEvent(y.aux, y.vit_done[k], 0))) break;
+    if (any && !ok(dispatch_vit32(P, chunk[k], o, y.aux))) break;
+    if (any && !ok(dispatch_fwd(P, chunk[k], o, y.tail))) break;
+  }
+  mark(3, y.aux);
+  if (ok(hipEventRecord(y.aux_done, y.aux)) && ok(hipStreamWaitEvent(y.tail, y.aux_done, 0)) &&
+      ok(hipEventRecord(y.tail_done, y.tail)))
+    ok(hipStreamWaitEvent(s, y.tail_done, 0));
   if (e == hipSuccess && o.counts) {
-    hipLaunchKernelGGL(export_counts, dim3(1), dim3(64), 0, s, db.counters, o.counts);
-    e = hipGetLastError();
+    hipLaunchKernelGGL(export_counts, dim3(1), dim3(64), 0, s, (const int32_t *)chunk[0].counters, K, o.counts);
+    ok(hipGetLastError());
   }
   mark(4, s);
   return e;

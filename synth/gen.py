@@ -332,11 +332,13 @@ def workload_profile(w: Workload) -> Profile:
     return make_profile(w.M, SEED_PROFILE + w.index)
 
 
-def workload_database(w: Workload, n: int | None = None, prof: Profile | None = None) -> Database:
+def workload_database(w: Workload, n: int | None = None, prof: Profile | None = None,
+                      seed_offset: int = 0) -> Database:
     """The workload's DB; n < w.n draws a smaller DB with the same recipe
-    (and a different stream of random numbers)."""
+    (and a different stream of random numbers); seed_offset > 0 draws
+    another database of the same recipe (a second database to search)."""
     prof = workload_profile(w) if prof is None else prof
-    return make_database(w.n if n is None else n, SEED_DB + w.index, prof, w.planted,
+    return make_database(w.n if n is None else n, SEED_DB + w.index + 1000 * seed_offset, prof, w.planted,
                          len_hi=w.len_hi, divergence=w.divergence)
 
 

@@ -404,3 +404,60 @@ def test_repeated_searches_streams_and_threshold_changes():
         announce(f"repeat F={F} ok {st} counts={counts.tolist()}")
     P.close()
     D.close()
+
+
+def test_concurrent_searches_on_shared_database_handles():
+    """hmm_db_share: four profiles searched at once on four streams through
+    four handles of one uploaded database; every result equals the oracle's,
+    and the shared residues outlive the handle that uploaded them."""
+    import torch
+    w = gen.WORKLOADS["C2"]
+    db = gen.workload_database(w, n=6000, prof=gen.workload_profile(w))
+    profs = [gen.make_profile(M, 900 + M) for M in (60, 200, 450, 801)]
+    calibs = [oracle.calibrate(oracle.OracleProfile(p), nthreads=NTHREADS) for p in profs]
+    Ps = [hg.Profile(p, *c) for p, c in zip(profs, calibs)]
+    D = hg.Database(db.residues, db.offsets)
+    handles = [D.share() for _ in range(4)]
+    D.close()                                   # the shares keep the data alive
+    streams = [torch.cuda.Stream() for _ in handles]
+    F = (0.05, 0.01, 1.0)
+    outs = [hg.alloc_results(db.n) for _ in handles]
+    for _ in range(2):                          # twice: the second round reuses every scratch
+        for P, H, s, o in zip(Ps, handles, streams, outs):
+            hg.search(P, H, F, o, stream=s)
+    torch.cuda.synchronize()
+    for p, c, o in zip(profs, calibs, outs):
+        g = {k: v.cpu().numpy() for k, v in o.items()}
+        ref = oracle_search(p, db.residues, db.offsets, c, F)
+        st = compare(g, ref, what=f"shared M={p.M}")
+        announce(f"shared handle M={p.M} ok {st}")
+    for H in handles:
+        H.close()
+    for P in Ps:
+        P.close()
+
+
+@pytest.mark.parametrize("chunks", [1, 3, 8])
+def test_pipelined_chunks_give_identical_results(chunks):
+    """The search is split into pipelined chunks of the sorted database;
+    results (and counts) do not depend on how many."""
+    import torch
+    w = gen.WORKLOADS["C2"]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=9000, prof=prof)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(db.residues, db.offsets)
+    assert hg.hmm_db_pipeline(D.handle, chunks) == chunks
+    F = (0.05, 0.01, 1.0)
+    out = hg.alloc_results(D.n)
+    hg.search(P, D, F, out)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    o = oracle_search(prof, db.residues, db.offsets, calib, F)
+    st = compare(g, o, what=f"chunks={chunks}")
+    fl = o["flags"]
+    assert list(g["counts"][:3]) == [np.sum((fl & m) != 0) for m in (hg.HMM_MSV_PASS, hg.HMM_VIT_OVF, hg.HMM_VIT_PASS)]
+    announce(f"pipelined chunks={chunks} ok {st}")
+    P.close()
+    D.close()
