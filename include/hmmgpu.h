@@ -236,6 +236,38 @@ typedef struct {
 int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask,
                const hmm_decode_out *out, hmm_stream stream);
 
+/* ---------------------------------------------------------------- iteration
+ *
+ * A jackhmmer search is iterated: the hits it accepts are aligned to the
+ * profile and a new profile is estimated from that alignment for the next
+ * search (the paper, Background section, names jackhmmer as the search tool
+ * of the MSA stage).  Counting runs on the GPU; the estimate is a small
+ * host computation:
+ *   - every aligned residue counts once for its state (M_k or I_k) and
+ *     residue; every step between consecutive states of an alignment's path
+ *     counts once for its transition, where M_k -> M_k' (k' > k + 1) passes
+ *     through D_{k+1} .. D_{k'-1} (MD_k, DD_{k+1} .. DD_{k'-2}, DM_{k'-1});
+ *   - the new profile takes the old one as a Dirichlet prior:
+ *       e'_k(a) = (c_k(a) + A e_k(a)) / (sum_b c_k(b) + A)   (match and insert rows)
+ *       t'_k    = (n_k + B t_k) / (sum of the group's n + B)  (MM MI MD | IM II | DM DD). */
+
+/* Add the counts of the alignments of dom[0 .. min(*n_dom, max_dom)) to
+ * `counts` (device uint32 [M][20] match, then [M-1][20] insert, then
+ * [M-1][7] transitions MM MI MD IM II DM DD; not cleared here).  dom, n_dom
+ * and aln are hmm_decode's outputs (device), on the same database and
+ * profile.  Enqueued on `stream` after the database's previous work.
+ * Errors: HMM_EINVAL (NULL argument, max_dom < 0), HMM_EDEVICE. */
+int hmm_count(const hmm_profile *p, hmm_db *db, const hmm_domain *dom, const int32_t *n_dom, int32_t max_dom,
+              const int16_t *aln, uint32_t *counts, hmm_stream stream);
+
+/* Host: the next iteration's probability profile from host counts (layout
+ * as hmm_count's) and the prior profile, with prior weights A (emissions)
+ * and B (transitions) > 0.  Writes match[M][20], insert[M-1][20],
+ * trans[M-1][7] (caller-owned, fp64).  Errors: HMM_EINVAL (invalid prior,
+ * NULL, A or B not > 0). */
+int hmm_rebuild(const hmm_profile_desc *prior, const uint32_t *counts, double A, double B, double *match,
+                double *insert, double *trans);
+
 /* Profiling hook: record HIP events around each stage of the next searches
  * on this database, in a ring of `capacity` searches (0 turns it off).  The
  * events are recorded on the search stream, so they bracket exactly that

@@ -331,3 +331,68 @@ def domains(p: OracleProfile, x, rt1: float = RT1, rt2: float = RT2) -> tuple[di
         d.update(s=s, e=e, nexp=float(dec["end"][s - 1:e].sum()))
         out.append(d)
     return dec, out
+
+
+# ------------------------------------------------------------ iteration: profile from hits
+
+def count_alignment(M: int, x, s: int, code) -> dict:
+    """Emission and transition counts of one region's alignment (codes as
+    oa_align: +k M_k, -k I_k, 0 not aligned; residue s + j has code[j]).
+
+    match[k-1][a]: residues a on M_k; insert[k-1][a]: on I_k; trans[k-1][t]
+    (MM MI MD IM II DM DD out of node k): the transitions between
+    consecutive states of the path, where M_k -> M_k' with k' > k + 1 passes
+    through D_{k+1} .. D_{k'-1} (MD_k, DD_{k+1} .. DD_{k'-2}, DM_{k'-1})."""
+    match = np.zeros((M, 20), np.int64)
+    insert = np.zeros((max(M - 1, 0), 20), np.int64)
+    trans = np.zeros((max(M - 1, 0), 7), np.int64)
+    code = [int(c) for c in code]
+    MM, MI, MD, IM, II, DM, DD = range(7)
+    prev = None
+    for j, c in enumerate(code):
+        if c == 0:
+            continue
+        a = int(x[s - 1 + j])
+        if c > 0:
+            match[c - 1, a] += 1
+        else:
+            insert[-c - 1, a] += 1
+        if prev is not None:
+            if prev > 0 and c > 0:           # M_k -> M_k'
+                k, k2 = prev, c
+                if k2 == k + 1:
+                    trans[k - 1, MM] += 1
+                else:
+                    trans[k - 1, MD] += 1
+                    for kk in range(k + 1, k2 - 1):
+                        trans[kk - 1, DD] += 1
+                    trans[k2 - 2, DM] += 1
+            elif prev > 0:                   # M_k -> I_k
+                trans[prev - 1, MI] += 1
+            elif c < 0:                      # I_k -> I_k
+                trans[-c - 1, II] += 1
+            else:                            # I_k -> M_{k+1}
+                trans[-prev - 1, IM] += 1
+        prev = c
+    return dict(match=match, insert=insert, trans=trans)
+
+
+def rebuild_profile(prof, counts: dict, A: float, B: float):
+    """The next iteration's profile: the counts of the accepted hits'
+    alignments with the previous profile as a Dirichlet prior (fp64):
+       e'_k(a) = (c_k(a) + A e_k(a)) / (sum_b c_k(b) + A)    (match and insert rows)
+       t'_k    = (n_k + B t_k) / (sum over the group n + B)   (groups MM MI MD | IM II | DM DD)"""
+    from synth import Profile
+    M = prof.M
+
+    def rows(c, p, w):
+        c = np.asarray(c, np.float64)
+        return (c + w * p) / (c.sum(axis=1, keepdims=True) + w)
+
+    match = rows(counts["match"], prof.match, A)
+    insert = rows(counts["insert"], prof.insert, A) if M > 1 else prof.insert.copy()
+    trans = np.zeros_like(prof.trans)
+    n = np.asarray(counts["trans"], np.float64)
+    for g in ((0, 3), (3, 5), (5, 7)):
+        trans[:, g[0]:g[1]] = rows(n[:, g[0]:g[1]], prof.trans[:, g[0]:g[1]], B)
+    return Profile(M, prof.bg.copy(), match, insert, trans)

@@ -27,8 +27,8 @@ HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, 
 HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float32 in the library)
 
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
-            "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables", "hmm_decode", "hmm_last_error",
-            "hmm_profile_free",
+            "hmm_count", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables",
+            "hmm_decode", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
             "hmm_profile_upload", "hmm_search", "hmm_strerror")
 
 
@@ -86,6 +86,10 @@ def lib():
         L.hmm_db_share.argtypes = [vp, C.POINTER(vp)]
         L.hmm_search.restype = C.c_int
         L.hmm_search.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), vp]
+        L.hmm_count.restype = C.c_int
+        L.hmm_count.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp]
+        L.hmm_rebuild.restype = C.c_int
+        L.hmm_rebuild.argtypes = [C.POINTER(hmm_profile_desc), vp, C.c_double, C.c_double, vp, vp, vp]
         L.hmm_decode.restype = C.c_int
         L.hmm_decode.argtypes = [vp, vp, vp, C.c_uint8, C.POINTER(hmm_decode_out), vp]
         L.hmm_db_info.restype = C.c_int
@@ -363,3 +367,33 @@ def domains_table(out: dict) -> list:
         recs.append(d)
     recs.sort(key=lambda d: (d["target"], d["s"]))
     return recs
+
+
+def hmm_count(profile: int, db: int, dec: dict, counts, stream=None) -> None:
+    """Enqueue the counts of decode()'s alignments into `counts` (device
+    uint32 tensor of M*20 + (M-1)*20 + (M-1)*7 entries, added to)."""
+    _check(lib().hmm_count(C.c_void_p(profile), C.c_void_p(db), C.c_void_p(dec["dom"].data_ptr()),
+                           C.c_void_p(dec["n_dom"].data_ptr()), int(dec["dom"].shape[0]),
+                           C.c_void_p(dec["aln"].data_ptr()), C.c_void_p(counts.data_ptr()),
+                           _stream_handle(stream)), "hmm_count")
+
+
+def count_size(M: int) -> int:
+    return M * HMM_K + max(M - 1, 0) * HMM_K + max(M - 1, 0) * 7
+
+
+def hmm_rebuild(prof, counts, A: float, B: float):
+    """Host estimate of the next iteration's profile (a synth.Profile-like
+    object with the prior's background) from host counts."""
+    from types import SimpleNamespace
+    M = int(prof.M)
+    d, keep = _desc(prof)
+    c = np.ascontiguousarray(counts, dtype=np.uint32)
+    assert c.size == count_size(M)
+    match = np.zeros((M, HMM_K))
+    insert = np.zeros((max(M - 1, 1), HMM_K))
+    trans = np.zeros((max(M - 1, 1), 7))
+    _check(lib().hmm_rebuild(C.byref(d), _ptr(c), float(A), float(B), _ptr(match), _ptr(insert), _ptr(trans)),
+           "hmm_rebuild")
+    return SimpleNamespace(M=M, bg=np.array(prof.bg, np.float64), match=match, insert=insert[:M - 1],
+                           trans=trans[:M - 1])

@@ -30,6 +30,7 @@
 // one lane's value); every cross-lane operation runs with all lanes active.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 
@@ -632,6 +633,54 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
   }
 }
 
+// Counts of the decoded alignments, one wave per domain record: every
+// aligned residue for its state and residue, every step between consecutive
+// states for its transition (a match-to-match step that skips nodes goes
+// through their delete states).  Integer atomics, so the counts are exact.
+// Records and codes are checked against the database and the profile, so
+// a mismatched buffer cannot send a write out of the count table.
+__global__ void __launch_bounds__(256) count_kernel(DevDb db, int M, const hmm_domain *dom, const int32_t *n_dom,
+                                                    int32_t max_dom, const int16_t *aln, uint32_t *counts) {
+  const int lane = threadIdx.x & 63;
+  const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
+  const int n = min(uni(*n_dom), max_dom);
+  uint32_t *cm = counts, *ci = counts + (size_t)M * kAlpha, *ct = ci + (size_t)(M - 1) * kAlpha;
+  enum { MM = 0, MI, MD, IM, II, DM, DD };
+  for (int r = wave_id(); r < n; r += nw) {
+    const int c = uni(dom[r].target);
+    if (c < 0 || c >= db.n) continue;
+    const int t = uni(db.iperm[c]);
+    const int L = uni(db.len[t]);
+    const int a1 = max(uni(dom[r].a), 1), b1 = min(uni(dom[r].b), L);
+    const uint8_t *x = db.res + db.start[t];
+    const int16_t *cod = aln + db.coff[t];
+    for (int j = a1 - 1 + lane; j <= b1 - 1; j += kWave) {
+      const int k = cod[j];
+      if (k > M || k < -(M - 1) || k == 0) continue;
+      const int a = x[j];
+      atomicAdd(k > 0 ? &cm[(k - 1) * kAlpha + a] : &ci[(-k - 1) * kAlpha + a], 1u);
+      if (j >= b1 - 1) continue;
+      const int k2 = cod[j + 1];
+      if (k2 > M || k2 < -(M - 1) || k2 == 0) continue;
+      if (k > 0 && k2 > 0) {
+        if (k2 == k + 1) {
+          atomicAdd(&ct[(k - 1) * 7 + MM], 1u);
+        } else if (k2 > k + 1) {
+          atomicAdd(&ct[(k - 1) * 7 + MD], 1u);
+          for (int kk = k + 1; kk < k2 - 1; kk++) atomicAdd(&ct[(kk - 1) * 7 + DD], 1u);
+          atomicAdd(&ct[(k2 - 2) * 7 + DM], 1u);
+        }
+      } else if (k > 0) {
+        if (-k2 == k) atomicAdd(&ct[(k - 1) * 7 + MI], 1u);
+      } else if (k2 < 0) {
+        if (k2 == k) atomicAdd(&ct[(-k - 1) * 7 + II], 1u);
+      } else if (k2 == -k + 1) {
+        atomicAdd(&ct[(-k - 1) * 7 + IM], 1u);
+      }
+    }
+  }
+}
+
 // Targets to decode: those whose caller flags hold every bit of the mask.
 __global__ void decode_select(DevDb db, const uint8_t *flags, int mask) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -707,6 +756,14 @@ int decode_max_waves(const DevProfile &p) {
 #undef HMM_CASE
   }
   return 0;
+}
+
+hipError_t launch_count(const DevProfile &p, const DevDb &db, const hmm_domain *dom, const int32_t *n_dom,
+                        int32_t max_dom, const int16_t *aln, uint32_t *counts, hipStream_t s) {
+  const int blocks = (int)std::min<int64_t>(((int64_t)max_dom + 3) / 4, 2048);
+  hipLaunchKernelGGL(count_kernel, dim3((unsigned)std::max(blocks, 1)), dim3(256), 0, s, db, p.M, dom, n_dom, max_dom,
+                     aln, counts);
+  return hipGetLastError();
 }
 
 hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t s) {

@@ -631,7 +631,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   const size_t sz_res = al((size_t)res_bytes);
   const size_t sz_start = al((size_t)n * 8 + 8), sz_i32 = al((size_t)n * 4 + 4);
-  const size_t total = sz_res + sz_start * 2 + sz_i32 * 2;
+  const size_t total = sz_res + sz_start * 2 + sz_i32 * 3;
 
   hmm_db *db = new (std::nothrow) hmm_db();
   if (!db) return fail(HMM_ENOMEM, "host allocation failed");
@@ -673,12 +673,16 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   const size_t o_coff = off;
   int64_t *s_coff = (int64_t *)(stage + off);
   off += sz_start;
+  const size_t o_iperm = off;
+  int32_t *s_iperm = (int32_t *)(stage + off);
+  off += sz_i32;
   for (int64_t i = 0; i < n; i++) {
     memcpy(s_res + start[i], residues + offsets[order[i]], (size_t)len[i]);
     s_start[i] = start[i];
     s_len[i] = len[i];
     s_perm[i] = order[i];
     s_coff[i] = offsets[order[i]];
+    s_iperm[order[i]] = (int32_t)i;
   }
   e = hipMalloc(&db->data->dmem, total);
   if (e != hipSuccess) {
@@ -706,6 +710,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   dv.len = (const int32_t *)(b + o_len);
   dv.perm = (const int32_t *)(b + o_perm);
   dv.coff = (const int64_t *)(b + o_coff);
+  dv.iperm = (const int32_t *)(b + o_iperm);
   const int rc = attach_scratch(db);
   if (rc != HMM_OK) {
     (void)hmm_db_free(db);
@@ -866,6 +871,45 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   HIP_TRY(launch_search(p->dev, chunk, K, o, s, db->sync, ev), "kernel launch");
   HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
   db->searched = true;
+  return HMM_OK;
+}
+
+int hmm_count(const hmm_profile *p, hmm_db *db, const hmm_domain *dom, const int32_t *n_dom, int32_t max_dom,
+              const int16_t *aln, uint32_t *counts, hmm_stream stream) {
+  if (!p || !db || !dom || !n_dom || !aln || !counts) return fail(HMM_EINVAL, "NULL argument");
+  if (max_dom < 0) return fail(HMM_EINVAL, "max_dom = %d", max_dom);
+  hipStream_t s = (hipStream_t)stream;
+  if (db->searched) HIP_TRY(hipStreamWaitEvent(s, db->done, 0), "hipStreamWaitEvent");
+  if (max_dom > 0 && db->n > 0) HIP_TRY(launch_count(p->dev, db->dev, dom, n_dom, max_dom, aln, counts, s), "kernel launch");
+  return HMM_OK;
+}
+
+int hmm_rebuild(const hmm_profile_desc *prior, const uint32_t *counts, double A, double B, double *match,
+                double *insert, double *trans) {
+  int rc = validate_desc(prior);
+  if (rc) return rc;
+  if (!counts || !match || (prior->M > 1 && (!insert || !trans))) return fail(HMM_EINVAL, "NULL argument");
+  if (!(A > 0.0) || !(B > 0.0) || !std::isfinite(A) || !std::isfinite(B))
+    return fail(HMM_EINVAL, "prior weights must be finite and > 0");
+  const int M = prior->M;
+  const uint32_t *cm = counts, *ci = counts + (size_t)M * kAlpha, *ct = ci + (size_t)(M - 1) * kAlpha;
+  // e'(a) = (c(a) + w p(a)) / (sum c + w) over each row (or transition group)
+  auto row = [](const uint32_t *c, const double *prev, int n, double w, double *out) {
+    double tot = 0.0;
+    for (int a = 0; a < n; a++) tot += (double)c[a];
+    for (int a = 0; a < n; a++) out[a] = ((double)c[a] + w * prev[a]) / (tot + w);
+  };
+  for (int k = 0; k < M; k++) row(cm + (size_t)k * kAlpha, prior->match + (size_t)k * kAlpha, kAlpha, A,
+                                  match + (size_t)k * kAlpha);
+  for (int k = 0; k + 1 < M; k++) {
+    row(ci + (size_t)k * kAlpha, prior->insert + (size_t)k * kAlpha, kAlpha, A, insert + (size_t)k * kAlpha);
+    const uint32_t *c = ct + (size_t)k * 7;
+    const double *t = prior->trans + (size_t)k * 7;
+    double *o = trans + (size_t)k * 7;
+    row(c, t, 3, B, o);           // MM MI MD
+    row(c + 3, t + 3, 2, B, o + 3);   // IM II
+    row(c + 5, t + 5, 2, B, o + 5);   // DM DD
+  }
   return HMM_OK;
 }
 

@@ -81,6 +81,7 @@ struct DevDb {
   int32_t *counters;            // [CNT_N]
   const LenParams *lp;          // [max_len + 1]
   const int64_t *coff;          // [n] offset of each target in the caller's residue array
+  const int32_t *iperm;         // [n] caller index -> sorted index
 };
 
 struct DevOut {
@@ -164,6 +165,12 @@ inline DevDb chunk_of(const DevDb &d, int64_t a, int64_t b, int k) {
 // (tail), after the last rescore (aux) and at the end (search stream).
 hipError_t launch_search(const DevProfile &p, const DevDb *chunk, int nchunks, const DevOut &out,
                          hipStream_t stream, const SearchSync &sync, hipEvent_t *ev);
+
+// Enqueue the emission and transition counts of the alignments of
+// dom[0 .. min(*n_dom, max_dom)) (codes in aln, caller residue layout) into
+// counts: uint32 [M][20] match, [M-1][20] insert, [M-1][7] transitions.
+hipError_t launch_count(const DevProfile &p, const DevDb &db, const hmm_domain *dom, const int32_t *n_dom,
+                        int32_t max_dom, const int16_t *aln, uint32_t *counts, hipStream_t stream);
 
 // Number of packed vectors per lane.
 inline int q8_of(int M) { return (M + 2 * kWave - 1) / (2 * kWave); }

@@ -195,3 +195,28 @@ def test_decode_rejects_bad_arguments_on_the_host():
     bad = hg.hmm_decode_out(C.c_void_p(8).value, -1, C.c_void_p(8).value, None, None, None)
     assert L.hmm_decode(C.c_void_p(1), C.c_void_p(1), None, 0, C.byref(bad), None) == hg.HMM_EINVAL
     assert "max_dom" in hg.hmm_last_error()
+
+
+@pytest.mark.parametrize("M,seed", [(1, 0), (2, 1), (30, 2), (257, 3)])
+def test_rebuild_equals_oracle_estimate(M, seed):
+    """hmm_rebuild (library host code) against the oracle's numpy estimate,
+    written independently; both fp64."""
+    prof = random_profile(M, seed)
+    rng = np.random.default_rng(seed)
+    c = dict(match=rng.integers(0, 50, (M, 20)), insert=rng.integers(0, 5, (max(M - 1, 0), 20)),
+             trans=rng.integers(0, 80, (max(M - 1, 0), 7)))
+    flat = np.concatenate([c["match"].ravel(), c["insert"].ravel(), c["trans"].ravel()]).astype(np.uint32)
+    got = hg.hmm_rebuild(prof, flat, 20.0, 10.0)
+    want = oracle.rebuild_profile(prof, c, 20.0, 10.0)
+    np.testing.assert_allclose(got.match, want.match, rtol=0, atol=1e-15)
+    np.testing.assert_allclose(got.insert, want.insert, rtol=0, atol=1e-15)
+    np.testing.assert_allclose(got.trans, want.trans, rtol=0, atol=1e-15)
+
+
+def test_rebuild_rejects_bad_arguments():
+    prof = random_profile(5, 1)
+    z = np.zeros(hg.count_size(5), np.uint32)
+    for A, B in ((0.0, 1.0), (1.0, -1.0), (float("nan"), 1.0)):
+        with pytest.raises(hg.HmmError) as e:
+            hg.hmm_rebuild(prof, z, A, B)
+        assert e.value.status == hg.HMM_EINVAL

@@ -302,3 +302,81 @@ def test_search_and_decode_match_frozen_oracle_fixtures(ci):
                 assert ok and sc >= w["score"] - tol_pp(L) * R - 8 * U * R
                 assert abs(d["score"] - w["score"]) <= tol_pp(L) * R + 8 * U * R
     announce(f"golden case {ci} M={c['M']}: {len(c['targets'])} targets ok")
+
+
+def _oracle_counts(M, residues, offsets, g):
+    tot = dict(match=np.zeros((M, 20), np.int64), insert=np.zeros((max(M - 1, 0), 20), np.int64),
+               trans=np.zeros((max(M - 1, 0), 7), np.int64))
+    for d in g["doms"]:
+        t = d["target"]
+        x = residues[offsets[t]:offsets[t + 1]]
+        code = g["aln"][offsets[t] + d["s"] - 1:offsets[t] + d["e"]]
+        c = oracle.count_alignment(M, x, d["s"], code)
+        for k in tot:
+            tot[k] += c[k]
+    return np.concatenate([tot["match"].ravel(), tot["insert"].ravel(), tot["trans"].ravel()])
+
+
+@pytest.mark.parametrize("M,n", [(1, 50), (90, 400), (734, 300), (2500, 40)])
+def test_counts_of_the_decoded_alignments(M, n):
+    """hmm_count on the GPU's own alignments equals the oracle's counting
+    of those alignments, exactly (integer counts)."""
+    import torch
+    prof = gen.make_profile(M, 40 + M)
+    db = gen.make_database(n, 77 + M, prof, 0.3, len_hi=3000 if M > 1000 else 1000)
+    P = hg.Profile(prof, 0.0, 0.0, 0.0)
+    D = hg.Database(db.residues, db.offsets)
+    dec = hg.decode(P, D, flags=None, aln=True)
+    counts = torch.zeros(hg.count_size(M), dtype=torch.int32, device="cuda")
+    hg.hmm_count(P.handle, D.handle, dec, counts)
+    hg.hmm_count(P.handle, D.handle, dec, counts)       # accumulates: twice the counts
+    torch.cuda.synchronize()
+    g = dict(doms=hg.domains_table(dec), aln=dec["aln"].cpu().numpy())
+    want = _oracle_counts(M, db.residues, db.offsets, g)
+    got = counts.cpu().numpy().astype(np.int64)
+    assert np.array_equal(got, 2 * want)
+    announce(f"counts M={M}: {len(g['doms'])} domains, {int(want.sum())} events ok")
+    P.close()
+    D.close()
+
+
+def test_one_search_iteration_end_to_end():
+    """search -> decode -> count -> rebuild -> search with the new profile:
+    the rebuilt profile equals the oracle's estimate from the same counts,
+    and the second search matches the oracle searching with it."""
+    import torch
+    from paper_2111_06340_amd.calibrate import calibrate
+    w = gen.WORKLOADS["C2"]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=4000, prof=prof)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    F = (0.02, 1e-3, 1.0)
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(db.residues, db.offsets)
+    out = hg.search(P, D, F)
+    dec = hg.decode(P, D, flags=out["flags"], mask=hg.HMM_FWD_PASS, aln=True)
+    counts = torch.zeros(hg.count_size(prof.M), dtype=torch.int32, device="cuda")
+    hg.hmm_count(P.handle, D.handle, dec, counts)
+    torch.cuda.synchronize()
+    c = counts.cpu().numpy().astype(np.uint32)
+    g = dict(doms=hg.domains_table(dec), aln=dec["aln"].cpu().numpy())
+    assert np.array_equal(c.astype(np.int64), _oracle_counts(prof.M, db.residues, db.offsets, g))
+    new = hg.hmm_rebuild(prof, c, 20.0, 10.0)
+    M = prof.M
+    cd = dict(match=c[:M * 20].reshape(M, 20), insert=c[M * 20:M * 40 - 20].reshape(M - 1, 20),
+              trans=c[M * 40 - 20:].reshape(M - 1, 7))
+    ref = oracle.rebuild_profile(prof, cd, 20.0, 10.0)
+    np.testing.assert_allclose(new.match, ref.match, atol=1e-15)
+    np.testing.assert_allclose(new.trans, ref.trans, atol=1e-15)
+    calib2 = calibrate(new)
+    P2 = hg.Profile(new, *calib2)
+    out2 = hg.search(P2, D, F)
+    torch.cuda.synchronize()
+    g2 = {k: v.cpu().numpy() for k, v in out2.items()}
+    o2 = oracle.search(oracle.OracleProfile(ref), db.residues, db.offsets, calib2, F, nthreads=NTHREADS)
+    from test_gpu_parity import compare
+    st = compare(g2, o2, what="iteration 2")
+    announce(f"iteration: {len(g['doms'])} domains counted; second search ok {st}")
+    P.close()
+    P2.close()
+    D.close()
