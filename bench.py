@@ -138,6 +138,10 @@ def main():
                     help="chunks a search is pipelined in (hmm_db_pipeline; 0 = the library's default, "
                          "1 = sequential stages, whose per-stage times give per-stage roofline fractions; "
                          "-1 = 1 for C4, whose 64 searches overlap through --streams, else the default)")
+    ap.add_argument("--iterations", type=int, default=1,
+                    help="iterate the search this many times (search, decode the Forward passes, count their "
+                         "alignments, re-estimate the profile, calibrate it, search again); reported under "
+                         "'iterations', never in value")
     ap.add_argument("--decode", action="store_true",
                     help="also time posterior decoding (hmm_decode) of the Forward survivors of the last "
                          "search: Forward with rows kept, Backward, regions and alignments (reported "
@@ -306,6 +310,8 @@ def main():
     if args.decode:
         pi, di = jobs[-1]
         rec["decode"] = bench_decode(hg, Ps[pi], profs[pi], Ds[di], outs[-1], stream, args)
+    if args.iterations > 1 and not batched:
+        rec["iterations"] = bench_iterations(hg, profs[0], calibs[0], D, F, stream, args)
     for P in Ps:
         P.close()
     for lane in lanes[1:]:
@@ -363,6 +369,47 @@ def bench_decode(hg, P, prof, D, out, stream, args) -> dict:
                          "hbm": {"achieved": round(traffic / s / 1e9, 1), "peak": 8000.0, "unit": "GB/s",
                                  "frac": round(traffic / s / 8e12, 4), "design_bytes": traffic,
                                  "traffic": measured_traffic(args, "decode_traffic_C3.json", "hmm_decode.hip")}}}
+
+
+def bench_iterations(hg, prof, calib, D, F, stream, args) -> list:
+    """jackhmmer-style iterations on the GPU: each one searches with the
+    current profile, decodes its Forward passes, counts their alignments
+    and re-estimates the profile (prior weights 20 and 10) for the next.
+    Times: the GPU part (search + decode + count, HIP events on the search
+    stream) and the host part (re-estimate, upload, calibration searches)."""
+    import numpy as np
+    import torch
+    from paper_2111_06340_amd.calibrate import calibrate
+    out = []
+    cur, cal = prof, calib
+    for it in range(args.iterations):
+        P = hg.Profile(cur, *cal)
+        res = hg.alloc_results(D.n)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        hg.search(P, D, F, res, stream=stream)
+        ev[1].record(stream)
+        dec = hg.decode(P, D, flags=res["flags"], mask=hg.HMM_FWD_PASS, aln=True, stream=stream)
+        ev[2].record(stream)
+        counts = torch.zeros(hg.count_size(cur.M), dtype=torch.int32, device="cuda")
+        hg.hmm_count(P.handle, D.handle, dec, counts, stream=stream)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        c = counts.cpu().numpy().astype(np.uint32)
+        nxt = hg.hmm_rebuild(cur, c, 20.0, 10.0)
+        ncal = calibrate(nxt)
+        host_s = time.perf_counter() - t
+        n_pass = int(res["counts"].cpu()[2])
+        rec = {"iteration": it + 1, "vit_pass": n_pass, "regions": int(dec["n_dom"].cpu()[0]),
+               "search_ms": round(ev[0].elapsed_time(ev[1]), 3), "decode_ms": round(ev[1].elapsed_time(ev[2]), 3),
+               "count_ms": round(ev[2].elapsed_time(ev[3]), 3), "host_rebuild_and_calibrate_s": round(host_s, 3)}
+        log(f"iteration {it + 1}: {rec}")
+        out.append(rec)
+        P.close()
+        cur, cal = nxt, ncal
+    return out
 
 
 def measured_traffic(args, name: str, source: str):
