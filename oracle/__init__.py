@@ -28,8 +28,9 @@ S16 = 500.0 / math.log(2.0)
 BASE8 = 190
 LN2 = math.log(2.0)
 
-F_MSV_PASS, F_MSV_OVF, F_VIT_RAN, F_VIT_PASS, F_VIT_OVF, F_FWD_RAN, F_FWD_PASS = (
-    0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40)
+F_MSV_PASS, F_MSV_OVF, F_VIT_RAN, F_VIT_PASS, F_VIT_OVF, F_FWD_RAN, F_FWD_PASS, F_BIAS_PASS = (
+    0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40, 0x80)
+BIAS_SWITCH = 1.0 / 64.0
 
 
 def build(force: bool = True) -> str:
@@ -87,6 +88,11 @@ def load(path: str):
         getattr(L, f).argtypes = [vp, vp, ip]
     L.orc_search.restype = ip
     L.orc_search.argtypes = [vp, vp, vp, C.c_int64, vp, vp, ip, ip, vp, vp, vp, vp, vp]
+    if hasattr(L, "orc_search_bias"):
+        L.orc_search_bias.restype = ip
+        L.orc_search_bias.argtypes = [vp, vp, vp, C.c_int64, vp, vp, ip, ip, ip, vp, vp, vp, vp, vp, vp]
+        L.orc_bias.restype = dp
+        L.orc_bias.argtypes = [vp, vp, ip]
     if hasattr(L, "orc_decode"):
         L.orc_decode.restype = ip
         L.orc_decode.argtypes = [vp, vp, ip, vp, vp, vp, vp, vp, vp, vp]
@@ -244,21 +250,28 @@ def calibrate(p: OracleProfile, nthreads: int = 8, n: int = 200) -> tuple[float,
     return mu_msv, mu_vit, tau
 
 
+def bias(p: OracleProfile, x) -> float:
+    """Composition-bias score (nats) of one target (see orc_bias)."""
+    x = _seq(x)
+    return float(p.lib.orc_bias(p.h, _ptr(x), x.size))
+
+
 def search(p: OracleProfile, residues, offsets, calib, F, nthreads: int = 8,
-           fwd_scaled: bool = False) -> dict:
-    """Filter pipeline over a whole database, caller order."""
+           fwd_scaled: bool = False, bias_filter: bool = False) -> dict:
+    """Filter pipeline over a whole database, caller order (with the
+    composition-bias filter between MSV and Viterbi when bias_filter)."""
     res = np.ascontiguousarray(residues, np.uint8)
     off = np.ascontiguousarray(offsets, np.int64)
     n = off.size - 1
     out = dict(msv=np.zeros(n, np.int16), vit=np.zeros(n, np.int32),
                fwd=np.zeros(n, np.float64), flags=np.zeros(n, np.uint8),
-               stage_s=np.zeros(3, np.float64))
+               beta=np.zeros(n, np.float64), stage_s=np.zeros(3, np.float64))
     c = np.asarray(calib, np.float64)
     f = np.asarray(F, np.float64)
-    rc = p.lib.orc_search(p.h, _ptr(res if res.size else np.zeros(1, np.uint8)), _ptr(off),
-                          n, _ptr(c), _ptr(f), int(nthreads), int(fwd_scaled),
-                          _ptr(out["msv"]), _ptr(out["vit"]), _ptr(out["fwd"]),
-                          _ptr(out["flags"]), _ptr(out["stage_s"]))
+    rc = p.lib.orc_search_bias(p.h, _ptr(res if res.size else np.zeros(1, np.uint8)), _ptr(off),
+                               n, _ptr(c), _ptr(f), int(nthreads), int(fwd_scaled), int(bias_filter),
+                               _ptr(out["msv"]), _ptr(out["vit"]), _ptr(out["fwd"]),
+                               _ptr(out["flags"]), _ptr(out["beta"]), _ptr(out["stage_s"]))
     if rc != 0:
         raise ValueError("oracle search rejected its input")
     return out

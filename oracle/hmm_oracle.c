@@ -60,6 +60,10 @@
 #define F_VIT_OVF 0x10
 #define F_FWD_RAN 0x20
 #define F_FWD_PASS 0x40
+#define F_BIAS_PASS 0x80             /* passed the composition-bias filter (only when it is on) */
+
+/* Composition-bias null model: switch probability between its two states */
+#define ORC_BIAS_SWITCH (1.0 / 64.0)
 
 typedef struct orc_profile {
   int M;
@@ -73,6 +77,8 @@ typedef struct orc_profile {
   /* Viterbi tables */
   int entry16, ej16;
   int16_t *msc16, *isc16, *t16;     /* [M][KA], [M-1][KA], [M-1][7] */
+  /* composition-bias filter: ln of (mean match emission / background) */
+  double bias_lr[KA];
 } orc_profile;
 
 /* Rounding used for every quantised score: q(x) = floor(x + 1/2), fp64. */
@@ -148,6 +154,12 @@ orc_profile *orc_profile_new(int M, const double *bg, const double *match,
                                : (int16_t)ORC_NEG16;
   p->entry16 = (int)clampl(qround(ORC_S16 * p->entry), -32768, 32767);
   p->ej16 = (int)clampl(qround(ORC_S16 * log(0.5)), -32768, 32767);
+  /* mean match composition over the nodes, as odds against the background */
+  for (int a = 0; a < KA; a++) {
+    double m = 0.0;
+    for (int k = 0; k < M; k++) m += match[k * KA + a];
+    p->bias_lr[a] = log(m / (double)M / bg[a]);
+  }
   return p;
 }
 
@@ -485,6 +497,33 @@ double orc_fwd_f64_scaled(const orc_profile *p, const uint8_t *x, int L) {
   return res;
 }
 
+/* ---------------------------------------------------------------- composition bias
+ *
+ * Composition-bias filter (reading): a null model with two states, R
+ * emitting the background f and S emitting the profile's mean match
+ * composition m(a) = (1/M) sum_k e_k(a); it starts in R or S with
+ * probability 1 - w, w and switches state with probability w at every
+ * further residue (w = 1/64).  The bias score is its log-likelihood ratio
+ * against the background (nats):
+ *    beta(x) = ln sum over state paths of P(path) prod_i r_{s_i}(x_i),
+ *    r_R = 1, r_S(a) = m(a)/f(a).
+ * With the filter on, a target that passes MSV goes on to Viterbi only if
+ * MSV overflowed or  msv_raw - S8 * max(beta, 0) >= THR8(L)  (the MSV
+ * score, less the bias in MSV units, still reaches the MSV cutoff).
+ * Forward recursion in log space over the two states.
+ */
+double orc_bias(const orc_profile *p, const uint8_t *x, int L) {
+  const double ls = log(ORC_BIAS_SWITCH), lt = log1p(-ORC_BIAS_SWITCH);
+  double aR = lt, aS = ls + p->bias_lr[x[0]];
+  for (int i = 1; i < L; i++) {
+    const double r = lse(aR + lt, aS + ls);
+    const double q = lse(aR + ls, aS + lt) + p->bias_lr[x[i]];
+    aR = r;
+    aS = q;
+  }
+  return lse(aR, aS);
+}
+
 /* ---------------------------------------------------------------- search */
 
 typedef struct {
@@ -496,6 +535,8 @@ typedef struct {
   const double *fthr;
   int all_f3;
   int fwd_scaled;
+  int bias;
+  double *beta;
   int16_t *msv;
   int32_t *vit;
   double *fwd;
@@ -531,9 +572,16 @@ static void *search_worker(void *arg) {
       j->msv[t] = (int16_t)raw;
       j->vit[t] = INT32_MIN;
       j->fwd[t] = NAN;
+      int go = (fl & F_MSV_PASS) != 0;
+      if (go && j->bias) {
+        double b = orc_bias(j->p, x, L);
+        if (j->beta) j->beta[t] = b;
+        if (ovf8 || (double)raw - ORC_S8 * (b > 0.0 ? b : 0.0) >= (double)j->thr8[L]) fl |= F_BIAS_PASS;
+        else go = 0;
+      }
       double t1 = now_s();
       st[0] += t1 - t0;
-      if (fl & F_MSV_PASS) {
+      if (go) {
         int ovf16 = 0;
         int32_t v = orc_vit16(j->p, x, L, &ovf16);
         fl |= F_VIT_RAN;
@@ -572,9 +620,9 @@ static void *search_worker(void *arg) {
  *   summed per-thread seconds of each stage.  fwd_scaled selects the
  *   probability-space Forward formulation.  Returns 0, or -1 on bad input.
  */
-int orc_search(const orc_profile *p, const uint8_t *res, const int64_t *off, int64_t n,
-               const double *calib, const double *F, int nthreads, int fwd_scaled,
-               int16_t *msv, int32_t *vit, double *fwd, uint8_t *flags, double *stage_s) {
+int orc_search_bias(const orc_profile *p, const uint8_t *res, const int64_t *off, int64_t n,
+                    const double *calib, const double *F, int nthreads, int fwd_scaled, int bias,
+                    int16_t *msv, int32_t *vit, double *fwd, uint8_t *flags, double *beta, double *stage_s) {
   if (!p || n < 0 || nthreads < 1) return -1;
   int maxL = 1;
   for (int64_t t = 0; t < n; t++) {
@@ -591,6 +639,9 @@ int orc_search(const orc_profile *p, const uint8_t *res, const int64_t *off, int
   j.p = p; j.res = res; j.off = off; j.n = n;
   j.thr8 = thr8; j.thr16 = thr16; j.fthr = fthr; j.all_f3 = F[2] >= 1.0;
   j.fwd_scaled = fwd_scaled;
+  j.bias = bias;
+  j.beta = beta;
+  if (beta) for (int64_t t = 0; t < n; t++) beta[t] = NAN;
   j.msv = msv; j.vit = vit; j.fwd = fwd; j.flags = flags;
   pthread_mutex_init(&j.mu, NULL);
   pthread_t *th = malloc(sizeof(pthread_t) * nthreads);
@@ -948,4 +999,11 @@ double orc_oa_path_score(const orc_profile *p, int L, const double *pcore, const
   }
   *valid = 1;
   return sc;
+}
+
+/* The pipeline without the composition-bias filter. */
+int orc_search(const orc_profile *p, const uint8_t *res, const int64_t *off, int64_t n,
+               const double *calib, const double *F, int nthreads, int fwd_scaled,
+               int16_t *msv, int32_t *vit, double *fwd, uint8_t *flags, double *stage_s) {
+  return orc_search_bias(p, res, off, n, calib, F, nthreads, fwd_scaled, 0, msv, vit, fwd, flags, NULL, stage_s);
 }

@@ -50,6 +50,9 @@ MUTANTS = {
                                      "pnjc[3 * (i - 1) + 1] = exp(FJ(i) + bJ - Z);"),
     "oa_flank_earns_core": ("G[r + 1] = G[r] + (1.0 - pcore[s - 1 + r]);", "G[r + 1] = G[r] + pcore[s - 1 + r];"),
     "oa_ignores_zero_dd": ("if (tr[6] > -INFINITY && ODc[k - 1] > u)", "if (ODc[k - 1] > u)"),
+    "bias_mean_not_divided": ("p->bias_lr[a] = log(m / (double)M / bg[a]);", "p->bias_lr[a] = log(m / bg[a]);"),
+    "bias_switch_swapped": ("const double q = lse(aR + ls, aS + lt) + p->bias_lr[x[i]];",
+                            "const double q = lse(aR + lt, aS + ls) + p->bias_lr[x[i]];"),
     "regions_strict_rt2": ("if (!(pcore[i] >= rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
                            "    while (j < L && pcore[j] >= rt2)",
                            "if (!(pcore[i] > rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
@@ -121,6 +124,11 @@ def _battery(lib) -> list:
     bp = brute.posteriors(brute.float_scores(prof, 2), x)
     want = brute.oa_best(4, _allowed(prof), bp["core"], bp["pM"], bp["pI"], 1, 2)
     check("oa_forbidden_skip", math.isclose(oracle.oa_align(op, d, 1, 2)["score"], want, abs_tol=1e-9))
+    from test_oracle_bias import _brute as bias_brute
+    for L, seed in ((1, 0), (4, 1), (7, 2)):
+        prof = random_profile(7, seed, alpha=0.3)
+        x = np.random.default_rng(seed + 10).integers(0, 20, L).astype(np.uint8)
+        check("bias", math.isclose(oracle.bias(oracle.OracleProfile(prof, lib), x), bias_brute(prof, x), abs_tol=1e-9))
     core = np.array([0.05, 0.10, 0.2, 0.25, 0.099, 0.3, 0.24, 0.11, 0.09, 0.12, 0.2, 0.1, 0.5, 0.1])
     check("regions", oracle.regions(core, 0.25, 0.10, lib) == [(2, 4), (6, 8), (10, 14)])
     return fails
