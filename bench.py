@@ -138,6 +138,8 @@ def main():
                     help="chunks a search is pipelined in (hmm_db_pipeline; 0 = the library's default, "
                          "1 = sequential stages, whose per-stage times give per-stage roofline fractions; "
                          "-1 = 1 for C4, whose 64 searches overlap through --streams, else the default)")
+    ap.add_argument("--bias", action="store_true",
+                    help="run the cascade with the composition-bias filter between MSV and Viterbi")
     ap.add_argument("--iterations", type=int, default=1,
                     help="iterate the search this many times (search, decode the Forward passes, count their "
                          "alignments, re-estimate the profile, calibrate it, search again); reported under "
@@ -213,7 +215,7 @@ def main():
     def step():
         for i, ((pi, di), out) in enumerate(zip(jobs, outs)):
             j = i % S
-            hg.search(Ps[pi], lanes[j][di], F, out, stream=streams[j])
+            hg.search(Ps[pi], lanes[j][di], F, out, stream=streams[j], bias_filter=args.bias)
 
     timed_stages = S == 1 and len(Ds) == 1
     for _ in range(args.warmup):
@@ -271,7 +273,7 @@ def main():
                f"{sum(Dx.n_residues for Dx in Ds)} residues in all)")
     if S > 1:
         wl += f", searches spread over {S} concurrent streams and database handles"
-    wl += f", MSV P<{F[0]:g} -> Viterbi P<{F[1]:g} -> Forward"
+    wl += f", MSV P<{F[0]:g}{' -> composition-bias filter' if args.bias else ''} -> Viterbi P<{F[1]:g} -> Forward"
     rec = {
         "metric": "GCUPS (profile cols x DB residues /s), MSV+Viterbi+Forward, M=734 vs 1M seqs",
         "value": round(gcups, 2),
@@ -291,7 +293,10 @@ def main():
         # from Viterbi's end, Forward until both are done
         "stage_ms": {"msv": round(float(st_ms[0]), 4), "viterbi": round(float(st_ms[1]), 4),
                      "rescore": round(float(st_ms[2]), 4), "forward_and_rescore": round(float(st_ms[3]), 4)},
-        "survivors": {"msv_pass": counts[0], "vit_overflow": counts[1], "vit_pass": counts[2],
+        "survivors": {"msv_pass": counts[0],
+                      "bias_pass": (int(sum(int(((o["flags"].cpu().numpy() & hg.HMM_BIAS_PASS) != 0).sum())
+                                            for o in outs)) if args.bias else None),
+                      "vit_overflow": counts[1], "vit_pass": counts[2],
                       "fwd_pass": counts[3], "viterbi_cells": ran["viterbi"], "rescore_cells": ran["rescore"],
                       "forward_cells": ran["forward"]},
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),

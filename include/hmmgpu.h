@@ -62,6 +62,7 @@ extern "C" {
 #define HMM_VIT_OVF 0x10  /* Viterbi saturated int16; vit holds the exact int32 rescore */
 #define HMM_FWD_RAN 0x20  /* Forward was computed */
 #define HMM_FWD_PASS 0x40 /* Forward score passed the F3 cutoff (set for every Forward target when F3 >= 1) */
+#define HMM_BIAS_PASS 0x80 /* passed the composition-bias filter (only set when the filter is on) */
 
 typedef struct hmm_profile hmm_profile; /* opaque; library-owned; immutable after upload */
 typedef struct hmm_db hmm_db;           /* opaque; library-owned; holds the packed database and search scratch */
@@ -86,9 +87,18 @@ typedef struct {
   double mu_msv, mu_vit, tau;
 } hmm_profile_desc;
 
-/* P-value cutoffs of the three stages; a value >= 1 passes every target. */
+/* P-value cutoffs of the three stages; a value >= 1 passes every target.
+ * bias_filter = 1 adds the composition-bias filter between MSV and Viterbi
+ * (0 = off, the plain cascade): a null model with two states, one emitting
+ * the background and one the profile's mean match composition
+ * m(a) = (1/M) sum_k e_k(a), starting in them with probability 63/64 and
+ * 1/64 and switching at each further residue with probability 1/64, gives
+ * the bias score beta = ln P(x | that model) / P(x | background) (nats); a
+ * target that passed MSV goes on only if MSV overflowed or
+ * msv - (3/ln 2) max(beta, 0) >= the MSV cutoff of its length. */
 typedef struct {
   double F1, F2, F3;
+  int32_t bias_filter;
 } hmm_thresholds;
 
 /* Caller-owned DEVICE buffers of n_seqs elements each, in the caller's
@@ -101,13 +111,17 @@ typedef struct {
  *             NaN when Forward did not run
  *   flags[i]  HMM_* flag bits
  *   counts    optional device int64[4] (may be NULL): number of MSV passes,
- *             Viterbi overflows, Viterbi passes, Forward passes. */
+ *             Viterbi overflows, Viterbi passes, Forward passes
+ *   bias      optional (may be NULL): the bias score beta (nats) of every
+ *             MSV pass when the bias filter is on; other entries are left
+ *             untouched. */
 typedef struct {
   int16_t *msv;
   int32_t *vit;
   float *fwd;
   uint8_t *flags;
   int64_t *counts;
+  float *bias;
 } hmm_results;
 
 /* Quantise a profile and upload its tables to the current device.  Profile

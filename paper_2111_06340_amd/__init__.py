@@ -21,8 +21,8 @@ HMM_OK, HMM_EINVAL, HMM_ERANGE, HMM_ENOMEM, HMM_EDEVICE = 0, -1, -2, -3, -4
 HMM_K = 20
 HMM_MAX_M = 3072
 HMM_MAX_LEN = 100000
-HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, HMM_FWD_PASS = (
-    0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40)
+HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, HMM_FWD_PASS, HMM_BIAS_PASS = (
+    0x01, 0x02, 0x04, 0x08, 0x10, 0x20, 0x40, 0x80)
 
 HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float32 in the library)
 
@@ -44,12 +44,12 @@ class hmm_profile_desc(C.Structure):
 
 
 class hmm_thresholds(C.Structure):
-    _fields_ = [("F1", C.c_double), ("F2", C.c_double), ("F3", C.c_double)]
+    _fields_ = [("F1", C.c_double), ("F2", C.c_double), ("F3", C.c_double), ("bias_filter", C.c_int32)]
 
 
 class hmm_results(C.Structure):
     _fields_ = [("msv", C.c_void_p), ("vit", C.c_void_p), ("fwd", C.c_void_p), ("flags", C.c_void_p),
-                ("counts", C.c_void_p)]
+                ("counts", C.c_void_p), ("bias", C.c_void_p)]
 
 
 class hmm_decode_out(C.Structure):
@@ -199,12 +199,14 @@ def hmm_db_stage_times(handle: int, cap: int) -> np.ndarray:
     return out[:n.value]
 
 
-def hmm_search(profile: int, db: int, F, out: dict, stream=None) -> None:
+def hmm_search(profile: int, db: int, F, out: dict, stream=None, bias_filter: bool = False) -> None:
     """Enqueue a search.  `out` maps msv/vit/fwd/flags (and optionally
-    counts) to device tensors of int16/int32/float32/uint8 (int64[4])."""
-    t = hmm_thresholds(*[float(v) for v in F])
+    counts, bias) to device tensors of int16/int32/float32/uint8 (int64[4],
+    float32)."""
+    t = hmm_thresholds(*[float(v) for v in F[:3]], int(bool(bias_filter)))
     r = hmm_results(out["msv"].data_ptr(), out["vit"].data_ptr(), out["fwd"].data_ptr(),
-                    out["flags"].data_ptr(), out["counts"].data_ptr() if out.get("counts") is not None else None)
+                    out["flags"].data_ptr(), out["counts"].data_ptr() if out.get("counts") is not None else None,
+                    out["bias"].data_ptr() if out.get("bias") is not None else None)
     _check(lib().hmm_search(C.c_void_p(profile), C.c_void_p(db), C.byref(t), C.byref(r), _stream_handle(stream)),
            "hmm_search")
 
@@ -253,7 +255,7 @@ def hmm_debug_length_params(prof, calib, F, L: int) -> dict:
     d, keep = _desc(prof, *calib)
     i32 = np.zeros(6, np.int32)
     f64 = np.zeros(4, np.float64)
-    t = hmm_thresholds(*[float(v) for v in F])
+    t = hmm_thresholds(*[float(v) for v in F[:3]], 0)
     _check(lib().hmm_debug_length_params(C.byref(d), C.byref(t), int(L), _ptr(i32), _ptr(f64)),
            "hmm_debug_length_params")
     return dict(move8=int(i32[0]), thr8=int(i32[1]), move16=int(i32[2]), thr16=int(i32[3]),
@@ -314,10 +316,12 @@ def alloc_results(n: int, device="cuda"):
                 vit=torch.empty(n, dtype=torch.int32, device=device),
                 fwd=torch.empty(n, dtype=torch.float32, device=device),
                 flags=torch.empty(n, dtype=torch.uint8, device=device),
-                counts=torch.zeros(4, dtype=torch.int64, device=device))
+                counts=torch.zeros(4, dtype=torch.int64, device=device),
+                bias=torch.full((n,), float("nan"), dtype=torch.float32, device=device))
 
 
-def search(profile: Profile, db: Database, F, out: dict | None = None, stream=None) -> dict:
+def search(profile: Profile, db: Database, F, out: dict | None = None, stream=None,
+           bias_filter: bool = False) -> dict:
     """Run one search on the current torch stream (or `stream`); returns the
     device result tensors (valid once the stream synchronises)."""
     import torch
@@ -325,7 +329,7 @@ def search(profile: Profile, db: Database, F, out: dict | None = None, stream=No
         out = alloc_results(db.n)
     if stream is None:
         stream = torch.cuda.current_stream()
-    hmm_search(profile.handle, db.handle, F, out, stream)
+    hmm_search(profile.handle, db.handle, F, out, stream, bias_filter)
     return out
 
 

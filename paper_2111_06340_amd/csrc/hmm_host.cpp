@@ -427,6 +427,11 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   dv.entry16 = p->entry16;
   dv.ej16 = p->ej16;
   dv.entry_p = (float)(2.0 / ((double)M * ((double)M + 1.0)));
+  for (int a = 0; a < kAlpha; a++) {
+    double m = 0.0;
+    for (int k = 0; k < M; k++) m += d->match[(size_t)k * kAlpha + a];
+    dv.bias_r[a] = (float)(m / (double)M / d->bg[a]);
+  }
   dv.msv = base;
   dv.vit_emit = base + n_msv;
   dv.vit_tr = dv.vit_emit + n_vemit;
@@ -845,6 +850,7 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   if (std::isnan(t->F1) || std::isnan(t->F2) || std::isnan(t->F3) || !(t->F1 > 0) || !(t->F2 > 0) ||
       !(t->F3 > 0))
     return fail(HMM_EINVAL, "P-value cutoffs must be > 0");
+  if (t->bias_filter != 0 && t->bias_filter != 1) return fail(HMM_EINVAL, "bias_filter = %d; need 0 or 1", t->bias_filter);
   if (db->n > 0 && (!out->msv || !out->vit || !out->fwd || !out->flags))
     return fail(HMM_EINVAL, "NULL output buffer");
   hipStream_t s = (hipStream_t)stream;
@@ -862,7 +868,7 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
     db->lp_F[1] = t->F2;
     db->lp_F[2] = t->F3;
   }
-  DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts};
+  DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts, out->bias, t->bias_filter};
   hipEvent_t *ev = nullptr;
   if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
   DevDb chunk[kMaxChunks];
@@ -936,7 +942,7 @@ int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t m
     // the loop and move probabilities of each length (profile-independent)
     if (db->lp_serial == 0) {
       if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
-      const hmm_thresholds all{1.0, 1.0, 1.0};
+      const hmm_thresholds all{1.0, 1.0, 1.0, 0};
       for (int L = 0; L <= db->max_len; L++) length_params(p, &all, L < 1 ? 1 : L, &db->h_lp[L], nullptr);
       HIP_TRY(hipMemcpyAsync(db->d_lp, db->h_lp, sizeof(LenParams) * ((size_t)db->max_len + 1),
                              hipMemcpyHostToDevice, s),

@@ -44,6 +44,7 @@ struct DevProfile {
   int32_t bias8, entry8, exit8;
   int32_t entry16, ej16;
   float entry_p;                // 2/(M(M+1))
+  float bias_r[kAlpha];         // composition-bias filter: mean match emission / background
   // MSV table, packed fp16 scores E = BIAS8 - COST8 (padding cells -1024).
   // msv_diag = 1: [20][P], P = 128 Qm, dword c = (E_c, E_{(c + P/2) mod P});
   // msv_diag = 0: [20][Qm][64] in the striped packed layout.
@@ -90,6 +91,8 @@ struct DevOut {
   float *fwd;
   uint8_t *flags;
   int64_t *counts;
+  float *bias;                  // optional bias scores
+  int32_t bias_filter;          // 1: composition-bias filter between MSV and Viterbi
 };
 
 // Posterior decoding (hmm_decode): outputs and per-wave scratch.

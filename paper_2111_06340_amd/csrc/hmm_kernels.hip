@@ -86,6 +86,68 @@ __device__ __forceinline__ h16x2 h2_max3(h16x2 a, h16x2 b, h16x2 c) {
 }
 __device__ __forceinline__ int h2_hmax(h16x2 v) { return (int)(float)__builtin_elementwise_maximum(v.x, v.y); }
 
+// Composition-bias score of one target (nats; result in every lane): the
+// forward probability ratio of a two-state null model (background, or the
+// profile's mean match composition with odds r(a) = P.bias_r[a]; start
+// 63/64 : 1/64, switch 1/64 per residue) against the background,
+//   beta = ln (pi G_0 G_1 ... G_{L-1} 1),  G_0 = diag(1, r(x_0)),
+//   G_i = [[63/64, r(x_i)/64], [1/64, 63/64 r(x_i)]].
+// Each lane multiplies the 2x2 matrices of one contiguous segment of the
+// target, then the segments are multiplied in order by a tree over the
+// lanes; products are kept in [2^-20, 2^20] by exact power-of-two scaling
+// with the exponents summed.
+constexpr float kS8f = (float)(3.0 / M_LN2);
+
+struct Mat2 {
+  float a, b, c, d;   // [[a, b], [c, d]]
+  int e;              // the product is this matrix times 2^e
+};
+
+__device__ __forceinline__ void mat2_mul(Mat2 &p, float ga, float gb, float gc, float gd, int ge) {
+  const float a = fmaf(p.a, ga, p.b * gc), b = fmaf(p.a, gb, p.b * gd);
+  const float c = fmaf(p.c, ga, p.d * gc), d = fmaf(p.c, gb, p.d * gd);
+  p.a = a;
+  p.b = b;
+  p.c = c;
+  p.d = d;
+  p.e += ge;
+  const float mx = fmaxf(fmaxf(a, b), fmaxf(c, d));
+  if (mx > 0x1p20f || mx < 0x1p-20f) {
+    int ex;
+    (void)frexpf(mx, &ex);
+    if (mx == 0.0f) ex = 0;
+    const float s = ldexpf(1.0f, -ex);
+    p.a *= s;
+    p.b *= s;
+    p.c *= s;
+    p.d *= s;
+    p.e += ex;
+  }
+}
+
+__device__ float bias_score(const DevProfile &P, const uint8_t *x, int L, int lane) {
+  constexpr float w = 1.0f / 64.0f, st = 63.0f / 64.0f;
+  const int seg = (L + kWave - 1) / kWave;
+  const int i0 = lane * seg, i1 = min(L, i0 + seg);
+  Mat2 m{1.0f, 0.0f, 0.0f, 1.0f, 0};
+  for (int i = i0; i < i1; i++) {   // lane-divergent, no cross-lane operation inside
+    const float r = P.bias_r[x[i]];
+    if (i == 0)
+      mat2_mul(m, 1.0f, 0.0f, 0.0f, r, 0);
+    else
+      mat2_mul(m, st, w * r, w, st * r, 0);
+  }
+  for (int dd = 1; dd < kWave; dd <<= 1) {
+    const float qa = __shfl_down(m.a, dd), qb = __shfl_down(m.b, dd), qc = __shfl_down(m.c, dd);
+    const float qd = __shfl_down(m.d, dd);
+    const int qe = __shfl_down(m.e, dd);
+    if ((lane & (2 * dd - 1)) == 0 && lane + dd < kWave) mat2_mul(m, qa, qb, qc, qd, qe);
+  }
+  const float s0 = fmaf(st, m.a, w * m.c), s1 = fmaf(st, m.b, w * m.d);
+  const float beta = logf(s0 + s1) + (float)m.e * (float)M_LN2;
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, beta), 0));
+}
+
 template <int Q, bool DIAG>
 __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOut out) {
   constexpr int kHalf = Q * kWave;                 // P/2 in DIAG, dwords per table row otherwise
@@ -224,7 +286,45 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     out.msv[c] = (int16_t)raw;
     out.vit[c] = INT32_MIN;
     out.fwd[c] = __builtin_nanf("");
-    if (pass) db.list_vit[wave_fetch_add(&db.counters[CNT_VIT], 1)] = t;
+    // with the composition-bias filter on, MSV passes go to the filter's
+    // list (the overflow list, unused until Viterbi) instead of Viterbi's
+    if (pass) {
+      const bool bf = out.bias_filter != 0;
+      (bf ? db.list_ovf : db.list_vit)[wave_fetch_add(&db.counters[bf ? CNT_OVF : CNT_VIT], 1)] = t;
+    }
+  }
+}
+
+// Composition-bias filter on the MSV passes (list_ovf, count CNT_OVF): the
+// bias score of each, and the ones whose MSV score less the bias still
+// reaches the cutoff (or that overflowed MSV) go on to Viterbi's list.
+__global__ void __launch_bounds__(256) bias_kernel(DevProfile P, DevDb db, DevOut out) {
+  const int lane = threadIdx.x & 63;
+  const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
+  for (;;) {
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
+    if (idx >= count) break;
+    const int t = uni(db.list_ovf[idx]);
+    const int L = uni(db.len[t]);
+    const LenParams lp = db.lp[L];
+    const float beta = bias_score(P, db.res + db.start[t], L, lane);
+    uint8_t fl = (uint8_t)uni(db.flags_sorted[t]);
+    const int c = uni(db.perm[t]);
+    const int raw = (int)out.msv[c];
+    const bool go = (fl & HMM_MSV_OVF) || (float)raw - kS8f * fmaxf(beta, 0.0f) >= (float)lp.thr8;
+    if (go) fl |= HMM_BIAS_PASS;
+    db.flags_sorted[t] = fl;
+    out.flags[c] = fl;
+    if (out.bias) out.bias[c] = beta;
+    if (go) db.list_vit[wave_fetch_add(&db.counters[CNT_VIT], 1)] = t;
+  }
+}
+
+// The overflow list and its counters start empty for Viterbi.
+__global__ void reset_ovf(int32_t *c) {
+  if (threadIdx.x == 0) {
+    c[CNT_OVF] = 0;
+    c[CNT_WORK_OVF] = 0;
   }
 }
 
@@ -769,6 +869,20 @@ hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hip
 #define HMM_MSV_DIAG_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14)
 #define HMM_MSV_STRIPED_CASES(X) X(14) X(16) X(20) X(24)
 
+hipError_t launch_bias(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(bias_kernel, 256, 0);
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (db.n + 3) / 4;
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(bias_kernel, dim3((unsigned)blocks), dim3(256), 0, s, P, db, o);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(reset_ovf, dim3(1), dim3(64), 0, s, db.counters);
+  return hipGetLastError();
+}
+
 hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   if (P.msv_diag) {
     switch (P.Qm) {
@@ -841,7 +955,10 @@ hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const D
   ok(hipGetLastError());
   // MSV of every chunk, back to back on the search stream
   for (int k = 0; k < K && e == hipSuccess; k++) {
-    if (chunk[k].n > 0) ok(dispatch_msv(P, chunk[k], o, s));
+    if (chunk[k].n > 0) {
+      ok(dispatch_msv(P, chunk[k], o, s));
+      if (o.bias_filter) ok(launch_bias(P, chunk[k], o, s));
+    }
     ok(hipEventRecord(y.msv_done[k], s));
   }
   mark(1, s);

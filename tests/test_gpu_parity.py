@@ -461,3 +461,65 @@ def test_pipelined_chunks_give_identical_results(chunks):
     announce(f"pipelined chunks={chunks} ok {st}")
     P.close()
     D.close()
+
+
+def _low_complexity_db(prof, base, seed):
+    """A reduced workload database plus targets made of the residues the
+    profile's mean composition favours most (they pass raw MSV but carry
+    a large composition bias)."""
+    rng = np.random.default_rng(seed)
+    odds = prof.match.mean(axis=0) / prof.bg
+    top = np.argsort(odds)[-3:]
+    seqs = [base.seq(i) for i in range(base.n)]
+    for L in (30, 60, 120, 250, 400, 800):
+        seqs.append(rng.choice(top, size=L).astype(np.uint8))
+        mix = gen.background_residues(rng, L)
+        mix[rng.random(L) < 0.5] = top[0]
+        seqs.append(mix)
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    return np.concatenate(seqs), off
+
+
+@pytest.mark.parametrize("name,n", [("C2", 8000), ("C3", 2000), ("C5", 300)])
+def test_bias_filter(name, n):
+    """The composition-bias filter between MSV and Viterbi: bias scores
+    within their fp32 tolerance; the filter decision, and everything after
+    it, exact except where the corrected MSV score lies within that
+    tolerance of the cutoff (there the GPU's decision must follow its own
+    bias score)."""
+    import torch
+    w = gen.WORKLOADS[name]
+    prof = gen.workload_profile(w)
+    base = gen.workload_database(w, n=n, prof=prof)
+    res, off = _low_complexity_db(prof, base, 5)
+    op = oracle.OracleProfile(prof)
+    calib = oracle.calibrate(op, nthreads=NTHREADS)
+    F = (0.05, 0.01, 1.0)
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(res, off)
+    out = hg.alloc_results(D.n)
+    hg.search(P, D, F, out, bias_filter=True)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items()}
+    o = oracle.search(op, res, off, calib, F, nthreads=NTHREADS, bias_filter=True)
+    lengths = np.diff(off)
+    ran = ~np.isnan(o["beta"])
+    assert np.array_equal(ran, ~np.isnan(g["bias"]))
+    tol = 1e-5 + 4 * 2.0 ** -24 * lengths
+    assert np.all(np.abs(g["bias"][ran] - o["beta"][ran]) <= tol[ran])
+    thr8 = np.array([oracle.thresholds(calib, F, int(L))[0] for L in lengths])
+    margin = o["msv"] - oracle.S8 * np.maximum(o["beta"], 0.0) - thr8
+    amb = ran & (np.abs(margin) <= oracle.S8 * tol) & ((o["flags"] & oracle.F_MSV_OVF) == 0)
+    for t in np.nonzero(amb)[0]:      # the GPU follows its own bias score
+        keep = float(g["msv"][t]) - np.float32(oracle.S8) * max(float(g["bias"][t]), 0.0) >= thr8[t]
+        assert bool(g["flags"][t] & hg.HMM_BIAS_PASS) == keep
+    idx = np.nonzero(~amb)[0]
+    sub = {k: v[idx] for k, v in o.items() if k in ("msv", "vit", "fwd", "flags")}
+    st = compare(g, sub, idx, what=f"bias {name}")
+    dropped = int(np.sum(((o["flags"] & oracle.F_MSV_PASS) != 0) & ((o["flags"] & oracle.F_BIAS_PASS) == 0)))
+    assert dropped >= 6
+    announce(f"bias filter {name} n={D.n}: {int(ran.sum())} scored, {dropped} dropped, {int(amb.sum())} near the "
+             f"cutoff, max bias error {np.max(np.abs(g['bias'][ran] - o['beta'][ran])):.2e} ok {st}")
+    P.close()
+    D.close()
