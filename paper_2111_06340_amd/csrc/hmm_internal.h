@@ -126,6 +126,13 @@ int decode_max_waves(const DevProfile &p);
 // Enqueue the decode of the selected targets on `stream` (d.nslots waves).
 hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t stream);
 
+// Forward and int32 rescore of long profiles with one workgroup of several
+// waves per target (hmm_coop.hip): coop_instance(Q) tells whether vectors
+// per lane Q have such an instance.
+bool coop_instance(int Q);
+hipError_t launch_fwd_coop(const DevProfile &p, const DevDb &db, const DevOut &o, hipStream_t stream);
+hipError_t launch_vit32_coop(const DevProfile &p, const DevDb &db, const DevOut &o, hipStream_t stream);
+
 // A search runs in up to kMaxChunks chunks of the length-sorted database
 // (contiguous ranges of about equal residue counts), pipelined: the MSV
 // kernels of the chunks run back to back on the search stream, and the rest

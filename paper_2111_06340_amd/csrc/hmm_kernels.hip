@@ -341,14 +341,14 @@ __global__ void reset_ovf(int32_t *c) {
 // would raise it.  The delete chain is computed inside each slot, then
 // propagated across slots until no lane changes (exact: sat is monotone).
 
-// Threads per block of the Viterbi, rescore and Forward kernels.  Large
-// instances run one wave per SIMD (4 waves per block): each wave may then
-// use the whole register file, architectural and accumulation registers,
-// and spills go to accumulation registers rather than to scratch memory.
+// Threads per block of the Viterbi kernel.  Large instances run one wave per
+// SIMD (4 waves per block): each wave may then use the whole register file,
+// architectural and accumulation registers, and spills go to accumulation
+// registers rather than to scratch memory.
 template <int Q>
-constexpr int kThreads16 = Q >= 16 ? 256 : 512;   // packed int16 Viterbi
-template <int Q>
-constexpr int kThreads32 = Q >= 14 ? 256 : 512;   // int32 rescore and Forward
+constexpr int kThreads16 = Q >= 16 ? 256 : 512;
+// Threads per block of the one-wave rescore and Forward kernels.
+constexpr int kThreads32 = 512;
 
 struct VitResult {
   int raw;
@@ -479,40 +479,27 @@ __global__ void __launch_bounds__(kThreads16<Q>) vit16_kernel(DevProfile P, DevD
 // ============================================================================ Viterbi int32 rescore
 //
 // The int16 recurrence in int32 with every add floored at -2^30 and no upper
-// clamp; run on the targets that overflowed int16.  Emission rows come from
-// LDS when the table fits (else global memory), prefetched a row ahead;
-// transitions stay in registers up to 16 vectors per lane, else in LDS.
+// clamp; run on the targets that overflowed int16.  One wave per target, for
+// profiles up to 12 vectors per lane (longer ones: hmm_coop.hip): emission
+// rows come from LDS, prefetched a row ahead; transitions stay in registers.
 
 __device__ __forceinline__ int fl32(int v) { return max(v, kNeg32); }
 
-template <int Q, bool EMIT_LDS, bool TR_LDS>
-__global__ void __launch_bounds__(kThreads32<Q>) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
+template <int Q>
+__global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ int32_t lds32[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;   // dwords
-  constexpr int kTr = TR_N * Q * kWave;
-  if (EMIT_LDS || TR_LDS) {
-    if (EMIT_LDS)
-      for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_emit)[i];
-    if (TR_LDS)
-      for (int i = threadIdx.x; i < kTr / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_tr)[i];
-    __syncthreads();
-  }
-  const int *emit = (EMIT_LDS ? (const int *)lds32 : P.v32_emit) + lane;
-  const int *trp = (TR_LDS ? (const int *)lds32 : P.v32_tr) + lane;
-  constexpr int kTrRegs = TR_LDS ? 1 : Q;
-  int tr[TR_N][kTrRegs];
-  if (!TR_LDS) {
+  for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_emit)[i];
+  __syncthreads();
+  const int *emit = (const int *)lds32 + lane;
+  const int *trp = P.v32_tr + lane;
+  int tr[TR_N][Q];
 #pragma unroll
-    for (int k = 0; k < TR_N; k++)
+  for (int k = 0; k < TR_N; k++)
 #pragma unroll
-      for (int q = 0; q < kTrRegs; q++) tr[k][q] = trp[(k * Q + q) * kWave];
-  }
-  // Transitions read from LDS are re-read on every row: `trofs` (always 0)
-  // is hidden from the compiler once per row, so the reads cannot be hoisted
-  // out of the row loop into registers (which would spill).
-  int trofs = 0;
-  auto TR = [&](int k, int q) -> int { return TR_LDS ? trp[(k * Q + q) * kWave + trofs] : tr[k][TR_LDS ? 0 : q]; };
+    for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
+  auto TR = [&](int k, int q) -> int { return tr[k][q]; };
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
@@ -535,7 +522,6 @@ __global__ void __launch_bounds__(kThreads32<Q>) vit32_kernel(DevProfile P, DevD
       for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
     };
     auto row = [&](const int(&em)[2 * Q]) -> bool {
-      if (TR_LDS) asm volatile("" : "+v"(trofs));
       const int msh = lane_up_i(M[Q - 1]);
       const int ish = lane_up_i(I[Q - 1]);
       const int dsh = lane_up_i(D[Q - 1]);
@@ -607,32 +593,21 @@ __global__ void __launch_bounds__(kThreads32<Q>) vit32_kernel(DevProfile P, DevD
 // of two whenever the largest special value leaves [2^-40, 2^40]; the removed
 // exponents are summed.  Result: ln(C move) + (sum of exponents) ln 2, nats.
 
-template <int Q, bool EMIT_LDS, bool TR_LDS>
-__global__ void __launch_bounds__(kThreads32<Q>) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
+template <int Q>
+__global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ float ldsf[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;
-  constexpr int kTr = (TR_N + 1) * Q * kWave;
-  if (EMIT_LDS || TR_LDS) {
-    if (EMIT_LDS)
-      for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_emit)[i];
-    if (TR_LDS)
-      for (int i = threadIdx.x; i < kTr / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_tr)[i];
-    __syncthreads();
-  }
-  const float *emit = (EMIT_LDS ? (const float *)ldsf : P.f_emit) + lane;
-  const float *trp = (TR_LDS ? (const float *)ldsf : P.f_tr) + lane;
-  constexpr int kR = TR_LDS ? 1 : Q;
-  float tr[TR_N + 1][kR];
-  if (!TR_LDS) {
+  for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_emit)[i];
+  __syncthreads();
+  const float *emit = (const float *)ldsf + lane;
+  const float *trp = P.f_tr + lane;
+  float tr[TR_N + 1][Q];
 #pragma unroll
-    for (int k = 0; k <= TR_N; k++)
+  for (int k = 0; k <= TR_N; k++)
 #pragma unroll
-      for (int q = 0; q < kR; q++) tr[k][q] = trp[(k * Q + q) * kWave];
-  }
-  // Transitions read from LDS are re-read on every row (see the rescore).
-  int trofs = 0;
-  auto TR = [&](int k, int q) -> float { return TR_LDS ? trp[(k * Q + q) * kWave + trofs] : tr[k][TR_LDS ? 0 : q]; };
+    for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
+  auto TR = [&](int k, int q) -> float { return tr[k][q]; };
   // P part of the delete-chain scan: the lane's P before each of the six steps
   float pstep[6];
   {
@@ -668,7 +643,6 @@ __global__ void __launch_bounds__(kThreads32<Q>) fwd_kernel(DevProfile P, DevDb 
       for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
     };
     auto row = [&](const float(&em)[2 * Q]) -> bool {
-      if (TR_LDS) asm volatile("" : "+v"(trofs));
       const float msh = lane_up_f(M[Q - 1]);
       const float ish = lane_up_f(I[Q - 1]);
       const float dsh = lane_up_f(D[Q - 1]);
@@ -836,33 +810,28 @@ hipError_t launch_list_kernel(K k, int threads, int &bpc, size_t lds, const DevP
   return hipGetLastError();
 }
 
-// Tables of the 32-bit kernels: emissions in LDS up to 12 vectors per lane
-// (120 KB), transitions in registers up to 16, else in LDS.
-template <int Q>
-constexpr bool kEmitLds32 = Q <= 12;
-template <int Q>
-constexpr bool kTrLds32 = Q > 16;
-static_assert(!(kEmitLds32<16> && kTrLds32<16>), "the two LDS tables share offset 0");
-
+// One-wave 32-bit kernels: the emission table in LDS (at most 120 KB, for
+// 12 vectors per lane), transitions in registers.
 template <int Q>
 hipError_t launch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
-  const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)TR_N * Q * kWave * 4 : 0);
+  static_assert(Q <= 12, "longer profiles take the cooperative kernels");
+  const size_t lds = (size_t)kAlpha * 2 * Q * kWave * 4;
   static int bpc = 0;
-  return launch_list_kernel(vit32_kernel<Q, E, T>, kThreads32<Q>, bpc, lds, P, db, o, s);
+  return launch_list_kernel(vit32_kernel<Q>, kThreads32, bpc, lds, P, db, o, s);
 }
 
 template <int Q>
 hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
-  constexpr bool E = kEmitLds32<Q>, T = kTrLds32<Q>;
-  const size_t lds = (E ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0) + (T ? (size_t)(TR_N + 1) * Q * kWave * 4 : 0);
+  static_assert(Q <= 12, "longer profiles take the cooperative kernels");
+  const size_t lds = (size_t)kAlpha * 2 * Q * kWave * 4;
   static int bpc = 0;
-  return launch_list_kernel(fwd_kernel<Q, E, T>, kThreads32<Q>, bpc, lds, P, db, o, s);
+  return launch_list_kernel(fwd_kernel<Q>, kThreads32, bpc, lds, P, db, o, s);
 }
 
 #define HMM_Q8_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14) X(16) X(20) X(24)
-#define HMM_Q32_CASES(X) \
-  X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12) X(14) X(16) X(20) X(24) X(28) X(32) X(40) X(48)
+// One-wave instances of the 32-bit kernels; 14 and more vectors per lane
+// (14, 16, 20, 24, 28, 32, 40, 48) run the cooperative ones.
+#define HMM_Q32_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(8) X(10) X(12)
 
 // MSV instances: diagonal layout up to 14 vectors per lane (table 10 KB per
 // vector in LDS), striped above.
@@ -916,6 +885,7 @@ hipError_t dispatch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o,
 }
 
 hipError_t dispatch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  if (coop_instance(P.Q32)) return launch_vit32_coop(P, db, o, s);
   switch (P.Q32) {
 #define HMM_CASE(q) \
   case q:           \
@@ -927,6 +897,7 @@ hipError_t dispatch_vit32(const DevProfile &P, const DevDb &db, const DevOut &o,
 }
 
 hipError_t dispatch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  if (coop_instance(P.Q32)) return launch_fwd_coop(P, db, o, s);
   switch (P.Q32) {
 #define HMM_CASE(q) \
   case q:           \

@@ -213,7 +213,8 @@ def _ragged_db(prof, seed, lengths=EDGE_LENGTHS, homolog_every=3):
     return np.concatenate(seqs), off
 
 
-@pytest.mark.parametrize("M", [1, 2, 3, 77, 127, 128, 129, 255, 256, 257, 733, 734, 1000, 1281])
+@pytest.mark.parametrize("M", [1, 2, 3, 77, 127, 128, 129, 255, 256, 257, 733, 734, 800, 1000, 1100, 1281,
+                               1700, 2000])
 def test_edge_lengths_and_profile_sizes(M):
     prof = gen.make_profile(M, 500 + M)
     res, off = _ragged_db(prof, M)
@@ -255,7 +256,7 @@ def _peaked(M, seed, p_top=0.81):
     return gen.Profile(M, bg, match, insert, trans), c.astype(np.uint8)
 
 
-@pytest.mark.parametrize("M", [40, 200, 700])
+@pytest.mark.parametrize("M", [40, 200, 700, 800, 1000, 2500])
 def test_overflow_and_rescore(M):
     prof, c = _peaked(M, M)
     rng = np.random.default_rng(M)
@@ -277,6 +278,36 @@ def test_overflow_and_rescore(M):
         st = compare(g, o, what=f"peaked M={M}")
         assert st["vit_ovf"] >= 1 and st["msv_ovf"] >= 1
         announce(f"overflow M={M} F={F} ok {st}")
+
+
+@pytest.mark.parametrize("M", [700, 900, 1500, 2600])
+def test_long_delete_runs(M):
+    """A peaked profile whose middle half is skipped by a cheap delete run,
+    searched with the consensus minus that block: the best path (and much
+    of the Forward mass) runs through hundreds of consecutive delete
+    states, across many lanes of the profile layout and, for long
+    profiles, across the waves that share one target."""
+    prof, c = _peaked(M, 7 * M)
+    a, b = M // 4, 3 * M // 4
+    tr = prof.trans.copy()
+    tr[a - 1] = [0.6, 0.05, 0.35, 0.6, 0.4, 0.5, 0.5]      # M_a -> D_{a+1} likely
+    tr[a:b, 5], tr[a:b, 6] = 0.01, 0.99                    # D -> D runs cheap
+    prof = gen.Profile(M, prof.bg, prof.match, prof.insert, tr)
+    rng = np.random.default_rng(M)
+    seqs = [np.concatenate([c[:a], c[b:]]),
+            np.concatenate([gen.background_residues(rng, 40), c[:a], c[b + M // 8:],
+                            gen.background_residues(rng, 25)]),
+            np.concatenate([c[:a // 2], c[b:]]),
+            gen.background_residues(rng, 300)]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    res = np.concatenate(seqs)
+    calib = (-8.0, -9.0, -4.0)
+    F = (1.0, 1.0, 1.0)
+    g = run_gpu(prof, res, off, calib, F)
+    o = oracle_search(prof, res, off, calib, F)
+    st = compare(g, o, what=f"delete runs M={M}")
+    announce(f"delete runs M={M} ok {st}")
 
 
 def _high_bias_profiles():
