@@ -148,6 +148,255 @@ __device__ float bias_score(const DevProfile &P, const uint8_t *x, int L, int la
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, beta), 0));
 }
 
+// ---------------------------------------------------------------- MSV table reads
+// The diagonal layout's table rows are read with ds_read_addtid_b32, whose
+// address is M0 + offset + 4 * lane: the wave-uniform part (residue row and
+// diagonal offset) goes into M0 with one scalar move, so a row's reads cost
+// no vector instruction.  The compiler does not see these loads in its
+// wait-count tracking, so they are confined to straight-line code: the
+// reads of row r+1 are issued before row r's arithmetic and waited for
+// (s_waitcnt lgkmcnt(0)) right after it, before any branch.  No read is in
+// flight at a branch, a merge or a loop edge, so no copy or reuse of a
+// register can race with a read into it.  M0 is otherwise only written by
+// the compiler right before its own uses (lane writes of the atomic-add
+// scan), never carried across this code.
+// A scalar write of M0 needs one wait state before an add-TID LDS
+// instruction reads it (the s_nop).
+template <int Q>
+__device__ __forceinline__ void lds_load_tid(uint32_t (&c)[Q], int m0) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(m0));
+#pragma unroll
+  for (int q = 0; q < Q; q++) asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[q]) : "i"(q * kWave * 4));
+}
+template <int Q>
+__device__ __forceinline__ void lds_wait(uint32_t (&c)[Q]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::);
+#pragma unroll
+  for (int q = 0; q < Q; q++) asm volatile("" : "+v"(c[q]));
+}
+
+// Row driver of the diagonal MSV: residues four to a dword as in drive_rows,
+// table buffers in alternation, the rows of a dword taken in pairs.
+// row(cur, next, kind) computes a row from `cur`, waits for the reads into
+// `next` (issued just before), then tests: kind 0 = first row of a pair (no
+// test), 1 = second row of a pair (tests both), 2 = a row on its own (start
+// or end of a run; tested).  Returns true if a row stopped the driver
+// (`stop` = the last row computed) or the limit was reached (`stop` =
+// limit - 1).
+template <int Q, typename Load, typename Row>
+__device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int limit, int &stop, int lane,
+                                            uint32_t (&ba)[Q], uint32_t (&bb)[Q], Load load, Row row) {
+  auto code = [](uint32_t w, int r) { return (int)((w >> (8 * r)) & 0xffu); };
+  int r = r0;
+  for (; (r & 3) != 0; r++) {
+    if (r >= L) return false;
+    load(ba, uni((int)x[r]));
+    lds_wait(ba);
+    if (row(ba, ba, 2)) {
+      stop = r;
+      return true;
+    }
+  }
+  if (r >= L) return false;
+  const int cs = r & ~255;
+  const uint32_t *p = (const uint32_t *)(x + cs);
+  uint32_t cur = __builtin_nontemporal_load(p + lane);
+  uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
+  int j0 = (r & 255) >> 2;
+  uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, j0);
+  load(ba, code(w, 0));
+  lds_wait(ba);
+  for (int c0 = cs;; c0 += 256) {
+    const int nfull = min(kWave, (L - c0) >> 2);
+    for (int j = j0; j < nfull; j++) {
+      const int rr = c0 + 4 * j;
+      if (rr >= limit) {
+        stop = rr - 1;
+        return true;
+      }
+      uint32_t wn;
+      if (j == kWave - 1)
+        wn = (uint32_t)__builtin_amdgcn_readlane((int)nxt, 0);
+      else
+        wn = (uint32_t)__builtin_amdgcn_readlane((int)cur, j + 1);
+      load(bb, code(w, 1));
+      row(ba, bb, 0);
+      load(ba, code(w, 2));
+      if (row(bb, ba, 1)) {
+        stop = rr + 1;
+        return true;
+      }
+      load(bb, code(w, 3));
+      row(ba, bb, 0);
+      load(ba, code(wn, 0));
+      if (row(bb, ba, 1)) {
+        stop = rr + 3;
+        return true;
+      }
+      w = wn;
+    }
+    if (nfull < kWave) {  // the target's last 0..3 rows (row 0's table already in ba)
+      const int rt = c0 + 4 * nfull;
+      if (rt >= L) return false;
+      if (rt >= limit) {
+        stop = rt - 1;
+        return true;
+      }
+      for (int k = 0; rt + k < L; k++) {
+        if (k) {
+          load(ba, code(w, k));
+          lds_wait(ba);
+        }
+        if (row(ba, ba, 2)) {
+          stop = rt + k;
+          return true;
+        }
+      }
+      return false;
+    }
+    if (c0 + 256 >= L) return false;
+    j0 = 0;
+    cur = nxt;
+    nxt = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 2) * kWave + lane);
+  }
+}
+
+struct MsvResult {
+  int raw;
+  bool ovf;
+};
+
+// Diagonal-layout MSV of one target.  Rows come in pairs and the trigger
+// test runs once per pair, on two running maxima (even rows, odd rows).
+// When a pair fires and its first row already reached the trigger, the
+// second row was computed with the old Bx; since xB only grows and
+//   v'_k = max(v_{k-1} + E, Bx' + E, 0) = max(v_k, Bx' + E)   (Bx' >= Bx),
+// that row is corrected in place from its own table entries: in units of
+// the new Bx, w' = max(w + Bx - Bx', E).  Then the second row is tested
+// again against the new trigger value.
+template <int Q>
+__device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const uint8_t *x, int L, const LenParams &lp,
+                                                     int lane, uint32_t (&ca)[Q], uint32_t (&cb)[Q]) {
+  constexpr int kHalf = Q * kWave;   // P/2: dwords per half table row
+  constexpr int kRowB = 2 * kHalf * 4;  // bytes per residue in the table
+  const int entry8 = P.entry8, exit8 = P.exit8;
+  const int ovf_line = 255 - P.bias8;
+  auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
+  const int mv = lp.move8;
+  const int base = max(kBase8 - mv, 0);
+  int xJt = 0;
+  int Bx = min(max(base - entry8, 0), max(ovf_line, 0));
+  bool ovf = ovf_line <= 0;
+  h16x2 acc_e = as_h2(splat(-Bx)), acc_o = acc_e;
+  if (!ovf) {
+    h16x2 w[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) w[q] = acc_e;
+    uint32_t nbx = splat(-Bx);
+    auto trigger_thr = [&]() { return splat(min(ovf_line, max(xJt, kBase8) + 4) - Bx - 1); };
+    uint32_t thr = trigger_thr();
+    // xJ from the largest cell m so far, and the Bx it gives the next row
+    auto settle = [&](int m) {
+      xJt = max(xJt, max(m - exit8, 0));
+      return min(max(max(base, max(xJt - mv, 0)) - entry8, 0), ovf_line);
+    };
+    auto fold = [&](h16x2 &acc) {
+#pragma unroll
+      for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
+      if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
+    };
+    auto fired = [&]() { return any_lane(as_u(h2_max3(acc_o, as_h2(thr), acc_e)) != thr); };
+    // byte offset of the next load's row inside the residue's table row:
+    // 4 (row mod P/2); the driver stops at every multiple of P/2 rows, so at
+    // most one (discarded) read lies one dword row past P/2, still inside
+    // the residue's table row of P dwords
+    int lofs = 0;
+    // Empty asm statements that "modify" the row state order the code: the
+    // next row's reads are issued before this row's arithmetic, and the wait
+    // for them comes after it, so the read latency hides behind the row.
+    auto pin = [&]() {
+#pragma unroll
+      for (int q = 0; q < Q; q++) asm volatile("" : "+v"(w[q]));
+    };
+    auto load = [&](uint32_t(&c)[Q], int a) {
+      lds_load_tid(c, a * kRowB + lofs);
+      lofs += 4;
+      pin();
+    };
+    auto row = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int kind) -> bool {
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        const h16x2 e = as_h2(c[q]);
+        w[q] = h2_max3(w[q] + e, e, as_h2(nbx));
+      }
+      fold(kind == 1 ? acc_o : acc_e);
+      pin();
+      lds_wait(next);
+      if (kind == 0 || !fired()) return false;
+      if (kind == 2 || !any_lane(as_u(__builtin_elementwise_maximum(acc_e, as_h2(thr))) != thr)) return true;
+      // the pair's first row reached the trigger: settle it, correct the second row
+      const int m = wave_max_i32(h2_hmax(acc_e)) + Bx;
+      if (m >= ovf_line) {
+        ovf = true;
+        return true;
+      }
+      const int nBx = settle(m);
+      if (nBx != Bx) {
+        const h16x2 d = as_h2(splat(Bx - nBx));
+#pragma unroll
+        for (int q = 0; q < Q; q++) w[q] = __builtin_elementwise_maximum(w[q] + d, as_h2(c[q]));
+        acc_e += d;
+        acc_o += d;
+        fold(acc_o);
+        Bx = nBx;
+        nbx = splat(-Bx);
+      }
+      thr = trigger_thr();
+      return fired();
+    };
+    int r = 0;
+    for (;;) {
+      int stop = 0;
+      const int limit = (r / kHalf + 1) * kHalf;   // end of the current phase
+      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
+      if (ovf) break;
+      const int m = wave_max_i32(h2_hmax(__builtin_elementwise_maximum(acc_e, acc_o))) + Bx;
+      if (m >= ovf_line) {
+        ovf = true;
+        break;
+      }
+      const int nBx = settle(m);
+      if (nBx != Bx) {  // re-base w and the running maxima to the new Bx
+        const h16x2 d = as_h2(splat(Bx - nBx));
+#pragma unroll
+        for (int q = 0; q < Q; q++) w[q] += d;
+        acc_e += d;
+        acc_o += d;
+        Bx = nBx;
+        nbx = splat(-Bx);
+      }
+      thr = trigger_thr();
+      r = stop + 1;
+      if (r >= L) break;
+      lofs = 4 * (r % kHalf);
+      if (lofs == 0) {  // the halves of every state dword swap diagonals
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          const uint32_t u = as_u(w[q]);
+          w[q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
+        }
+      }
+    }
+  }
+  MsvResult res{255, ovf};
+  if (!ovf) {
+    const int m = wave_max_i32(h2_hmax(__builtin_elementwise_maximum(acc_e, acc_o))) + Bx;
+    const int xJ = max(m - exit8, 0);
+    res.raw = max(xJ - mv, 0);
+  }
+  return res;
+}
+
 template <int Q, bool DIAG>
 __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOut out) {
   constexpr int kHalf = Q * kWave;                 // P/2 in DIAG, dwords per table row otherwise
@@ -165,6 +414,10 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   const int ovf_line = 255 - P.bias8;
   const uint32_t *tab = lds + lane;
   const int n = (int)db.n;
+  // table buffers of the diagonal path (kept defined: its driver's exits use them)
+  uint32_t da[Q], dbuf[Q];
+#pragma unroll
+  for (int q = 0; q < Q; q++) da[q] = dbuf[q] = 0;
   // packed fp16 pair (v, v) as a wave-uniform dword
   auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
   // The next target's length and start are read during the current
@@ -182,101 +435,83 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     const uint8_t *x = db.res + snext;
     const int cperm = db.perm[t];  // read now, used at the end
     const LenParams lp = db.lp[L];
-    const int mv = lp.move8;
-    const int base = max(kBase8 - mv, 0);
-    int xJt = 0;
-    int Bx = min(max(base - entry8, 0), max(ovf_line, 0));
-    bool ovf = ovf_line <= 0;
-    h16x2 acc = as_h2(splat(-Bx));
-    if (!ovf) {
-      h16x2 w[Q];
+    MsvResult res;
+    if constexpr (DIAG) {
+      res = msv_target_diag<Q>(P, x, L, lp, lane, da, dbuf);
+    } else {  // striped layout
+      const int mv = lp.move8;
+      const int base = max(kBase8 - mv, 0);
+      int xJt = 0;
+      int Bx = min(max(base - entry8, 0), max(ovf_line, 0));
+      bool ovf = ovf_line <= 0;
+      h16x2 acc = as_h2(splat(-Bx));
+      if (!ovf) {
+        h16x2 w[Q];
 #pragma unroll
-      for (int q = 0; q < Q; q++) w[q] = acc;
-      uint32_t nbx = splat(-Bx);
-      // Trigger: some cell reaches T, the smallest value that could change
-      // xB or overflow; in w units, some w > T - Bx - 1.
-      auto trigger_thr = [&]() { return splat(min(ovf_line, max(xJt, kBase8) + 4) - Bx - 1); };
-      uint32_t thr = trigger_thr();
-      // DIAG: byte offset of the next load's row in the table, 4 (row mod
-      // P/2).  The driver stops at every multiple of P/2 rows, so at most one
-      // (discarded) prefetch reads one dword row past P/2: still inside
-      // the residue's table row, which holds P dwords.
-      int lofs = 0;
-      auto load = [&](uint32_t(&c)[Q], int a) {
-        const uint32_t *row = (const uint32_t *)((const char *)tab + a * (kRow * 4) + (DIAG ? lofs : 0));
+        for (int q = 0; q < Q; q++) w[q] = acc;
+        uint32_t nbx = splat(-Bx);
+        // Trigger: some cell reaches T, the smallest value that could change
+        // xB or overflow; in w units, some w > T - Bx - 1.
+        auto trigger_thr = [&]() { return splat(min(ovf_line, max(xJt, kBase8) + 4) - Bx - 1); };
+        uint32_t thr = trigger_thr();
+        auto load = [&](uint32_t(&c)[Q], int a) {
+          const uint32_t *row = (const uint32_t *)((const char *)tab + a * (kRow * 4));
 #pragma unroll
-        for (int q = 0; q < Q; q++) c[q] = row[q * kWave];
-        if (DIAG) lofs += 4;
-      };
-      // One row.  Only w and the running maximum change here, on every row:
-      // a trigger stops the row driver, and so does (DIAG) the end of a
-      // P/2-row phase; the caller then updates xJ and xB, re-bases or swaps
-      // w, and resumes at the next row.
-      auto row = [&](const uint32_t(&c)[Q]) -> bool {
-        if (DIAG) {
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const h16x2 e = as_h2(c[q]);
-            w[q] = h2_max3(w[q] + e, e, as_h2(nbx));
-          }
-        } else {
+          for (int q = 0; q < Q; q++) c[q] = row[q * kWave];
+        };
+        // One row.  Only w and the running maximum change here, on every row:
+        // a trigger stops the row driver; the caller then updates xJ and xB,
+        // re-bases w, and resumes at the next row.
+        auto row = [&](const uint32_t(&c)[Q]) -> bool {
           const uint32_t sh = slot_up16(as_u(w[Q - 1]));
 #pragma unroll
           for (int q = Q - 1; q >= 0; q--) {
             const h16x2 e = as_h2(c[q]);
             w[q] = h2_max3((q ? w[q - 1] : as_h2(sh)) + e, e, as_h2(nbx));
           }
-        }
 #pragma unroll
-        for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
-        if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
-        return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr);
-      };
-      uint32_t ca[Q], cb[Q];
-      int r = 0;
-      for (;;) {
-        int stop = 0;
-        const int limit = DIAG ? (r / kHalf + 1) * kHalf : 0;   // end of the current phase
-        if (!drive_rows<DIAG>(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
-        const int m = wave_max_i32(h2_hmax(acc)) + Bx;      // largest cell so far
-        if (m >= ovf_line) {
-          ovf = true;
-          break;
-        }
-        xJt = max(xJt, max(m - exit8, 0));
-        const int nBx = min(max(max(base, max(xJt - mv, 0)) - entry8, 0), ovf_line);
-        if (nBx != Bx) {  // re-base w (and the running maximum) to the new Bx
-          const h16x2 d = as_h2(splat(Bx - nBx));
-#pragma unroll
-          for (int q = 0; q < Q; q++) w[q] += d;
-          acc += d;
-          Bx = nBx;
-          nbx = splat(-Bx);
-        }
-        thr = trigger_thr();
-        r = stop + 1;
-        if (r >= L) break;
-        if (DIAG) {
-          lofs = 4 * (r % kHalf);
-          if (lofs == 0) {  // the halves of every state dword swap diagonals
-#pragma unroll
-            for (int q = 0; q < Q; q++) {
-              const uint32_t u = as_u(w[q]);
-              w[q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
-            }
+          for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
+          if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
+          return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr);
+        };
+        uint32_t ca[Q], cb[Q];
+        int r = 0;
+        for (;;) {
+          int stop = 0;
+          if (!drive_rows(x, L, r, 0, stop, lane, ca, cb, load, row)) break;
+          const int m = wave_max_i32(h2_hmax(acc)) + Bx;      // largest cell so far
+          if (m >= ovf_line) {
+            ovf = true;
+            break;
           }
+          xJt = max(xJt, max(m - exit8, 0));
+          const int nBx = min(max(max(base, max(xJt - mv, 0)) - entry8, 0), ovf_line);
+          if (nBx != Bx) {  // re-base w (and the running maximum) to the new Bx
+            const h16x2 d = as_h2(splat(Bx - nBx));
+#pragma unroll
+            for (int q = 0; q < Q; q++) w[q] += d;
+            acc += d;
+            Bx = nBx;
+            nbx = splat(-Bx);
+          }
+          thr = trigger_thr();
+          r = stop + 1;
+          if (r >= L) break;
         }
       }
+      res.ovf = ovf;
+      res.raw = 255;
+      if (!ovf) {
+        const int m = wave_max_i32(h2_hmax(acc)) + Bx;
+        const int xJ = max(m - exit8, 0);
+        res.raw = max(xJ - mv, 0);
+      }
     }
+    const bool ovf = res.ovf;
+    const int raw = res.raw;
     if (t + nw < n) {
       Lnext = uni(db.len[t + nw]);
       snext = db.start[t + nw];
-    }
-    int raw = 255;
-    if (!ovf) {
-      const int m = wave_max_i32(h2_hmax(acc)) + Bx;
-      const int xJ = max(m - exit8, 0);
-      raw = max(xJ - mv, 0);
     }
     const bool pass = ovf || raw >= lp.thr8;
     const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
@@ -340,6 +575,7 @@ __global__ void reset_ovf(int32_t *c) {
 // so the wave-wide maximum is taken only when a cell reaches the value that
 // would raise it.  The delete chain is computed inside each slot, then
 // propagated across slots until no lane changes (exact: sat is monotone).
+
 
 // Threads per block of the Viterbi kernel.  Large instances run one wave per
 // SIMD (4 waves per block): each wave may then use the whole register file,
