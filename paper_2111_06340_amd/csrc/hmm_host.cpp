@@ -426,6 +426,12 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   dv.exit8 = p->exit8;
   dv.entry16 = p->entry16;
   dv.ej16 = p->ej16;
+  dv.dm_max16 = kNeg16;
+  dv.dm_max32 = kNeg32;
+  for (int c = 1; c < M; c++) {
+    dv.dm_max16 = std::max(dv.dm_max16, lo16(tr_cell(TR_DMIN, c)));
+    dv.dm_max32 = std::max(dv.dm_max32, w32(tr_cell(TR_DMIN, c)));
+  }
   dv.entry_p = (float)(2.0 / ((double)M * ((double)M + 1.0)));
   for (int a = 0; a < kAlpha; a++) {
     double m = 0.0;

@@ -43,6 +43,10 @@ struct DevProfile {
   int32_t msv_diag;             // MSV layout: 1 diagonal, 0 striped (see msv below)
   int32_t bias8, entry8, exit8;
   int32_t entry16, ej16;
+  // Largest D->M transition score over the nodes (int16 and int32 scales;
+  // minus infinity when M = 1): a delete value d with d + dm_max <= the
+  // B->M entry value can no longer change any match cell.
+  int32_t dm_max16, dm_max32;
   float entry_p;                // 2/(M(M+1))
   float bias_r[kAlpha];         // composition-bias filter: mean match emission / background
   // MSV table, packed fp16 scores E = BIAS8 - COST8 (padding cells -1024).

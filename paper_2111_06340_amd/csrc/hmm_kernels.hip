@@ -575,7 +575,17 @@ __global__ void reset_ovf(int32_t *c) {
 // so the wave-wide maximum is taken only when a cell reaches the value that
 // would raise it.  The delete chain is computed inside each slot, then
 // propagated across slots until no lane changes (exact: sat is monotone).
-
+//
+// Delete floor: D only feeds match cells (through D->M) and later deletes
+// (through D->D <= 0), and every match cell of this and every later row
+// includes the entry value xBe, which never decreases.  So a delete value
+// d <= tau = xBe - max_k DM_k, and everything the chain derives from it, can
+// never change a match cell: the kernel keeps D' = max(D, tau) instead of D
+// (the floored recurrence's fixed point is exactly max(D, tau), since
+// sat(tau + DD) <= tau), and sat(D' + DM) differs from sat(D + DM) only
+// where both are <= xBe.  M, I, xE and the overflow test are unchanged, and
+// the lazy propagation stops as soon as the chains that cross a slot
+// boundary fall to the floor, instead of running every chain to its end.
 
 // Threads per block of the Viterbi kernel.  Large instances run one wave per
 // SIMD (4 waves per block): each wave may then use the whole register file,
@@ -604,6 +614,8 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
   int xJt = kNeg16;
   int xB = sat16(mv);
   uint32_t xbe2 = splat16(sat16(xB + entry));
+  auto floor_of = [&](int xbe) { return splat16(min(xbe - P.dm_max16, 32767)); };
+  uint32_t tau2 = floor_of(sat16(xB + entry));
   int T = min(-ej + 1, 32767);
   uint32_t tm1 = splat16(T - 1);
   bool ovf = false;
@@ -633,7 +645,7 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     const uint32_t din = slot_up16(M[Q - 1]);
 #pragma unroll
     for (int q = 0; q < Q; q++) {
-      D[q] = i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q]));
+      D[q] = i16_max(i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q])), tau2);
       dc = D[q];
     }
     for (int it = 0; it < 2 * kWave; it++) {
@@ -656,6 +668,7 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
       xJt = max(xJt, sat16(m + ej));
       xB = max(sat16(mv), sat16(xJt + mv));
       xbe2 = splat16(sat16(xB + entry));
+      tau2 = floor_of(sat16(xB + entry));
       T = min(max(xJt, 0) - ej + 1, 32767);
       tm1 = splat16(T - 1);
     }
@@ -751,6 +764,7 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
     int xJt = kNeg32;
     int xB = fl32(mv);
     int xbe = fl32(xB + entry);
+    int tau = xbe - P.dm_max32;   // delete floor (as in the int16 kernel); >= xbe >= -2^30
     int T = -ej + 1;
     auto load = [&](int(&e)[2 * Q], int a) {
       const int *er = emit + a * (2 * Q * kWave);
@@ -779,7 +793,7 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
       const int din = lane_up_i(M[Q - 1]);
 #pragma unroll
       for (int q = 0; q < Q; q++) {
-        D[q] = max(max((q ? M[q - 1] : din) + TR(TR_MDIN, q), dc + TR(TR_DDIN, q)), kNeg32);
+        D[q] = max(max((q ? M[q - 1] : din) + TR(TR_MDIN, q), dc + TR(TR_DDIN, q)), tau);
         dc = D[q];
       }
       for (int it = 0; it < kWave; it++) {
@@ -788,7 +802,7 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
 #pragma unroll
         for (int q = 0; q < Q; q++) {
           if (moved) {
-            const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= -2^30 already
+            const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= tau >= -2^30 already
             moved = any_lane(nd != D[q]);
             D[q] = nd;
             dc = nd;
@@ -801,6 +815,7 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
         xJt = max(xJt, fl32(m + ej));
         xB = max(fl32(mv), fl32(xJt + mv));
         xbe = fl32(xB + entry);
+        tau = xbe - P.dm_max32;
         T = max(xJt, 0) - ej + 1;
       }
       return false;
