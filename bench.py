@@ -260,8 +260,11 @@ def main():
     if os.path.exists(args.traffic) and not batched and not args.cutoffs:
         with open(args.traffic) as f:
             tr = json.load(f)
-        if tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha():
-            traffic = tr.get("bytes_per_launch")
+        # the MSV stage's HBM bytes per search (all of its launches), while
+        # the kernel source and the launches per search are the measured ones
+        if (tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha()
+                and tr.get("launches_per_search") == chunks):
+            traffic = tr.get("bytes_per_search")
     if batched:
         wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
               f"against {D.n} synthetic sequences ({D.n_residues} residues, the C3 database)")
@@ -302,6 +305,7 @@ def main():
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
                      "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic,
+                     "traffic_note": "HBM bytes of the MSV stage per search (all its launches), rocprofv3 counters",
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
                      "msv_launches_per_search": chunks}
         if timed_stages else None,
