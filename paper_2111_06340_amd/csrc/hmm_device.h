@@ -80,10 +80,6 @@ __device__ __forceinline__ uint32_t slot_up16(uint32_t v) {
 
 __device__ __forceinline__ bool any_lane(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
 
-__device__ __forceinline__ int wave_max_i32(int v) {
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off));
-  return uni(v);
-}
 
 // DPP row shift within 16-lane rows; lanes without a source get `fill`.
 template <int CTRL, int ROWMASK = 0xf>
@@ -94,6 +90,21 @@ __device__ __forceinline__ float dpp_f(float v, float fill) {
 }
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
 constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+
+// Maximum across the wave (result uniform): an inclusive DPP max-scan of
+// each 16-lane row, the rows joined by row broadcasts; lane 63 ends with the
+// maximum of all 64 lanes.  No LDS round trip (a shuffle-based reduction
+// costs six of them and four times the instructions).
+__device__ __forceinline__ int wave_max_i32(int v) {
+  constexpr int kMin = INT32_MIN;
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowShr1, 0xf, 0xf, false));
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowShr2, 0xf, 0xf, false));
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowShr4, 0xf, 0xf, false));
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowShr8, 0xf, 0xf, false));
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowBcast15, 0xa, 0xf, false));
+  v = max(v, __builtin_amdgcn_update_dpp(kMin, v, kRowBcast31, 0xc, 0xf, false));
+  return __builtin_amdgcn_readlane(v, 63);
+}
 
 // Sum across the wave (result uniform).
 __device__ __forceinline__ float wave_sum_f(float v) {
