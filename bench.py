@@ -138,6 +138,9 @@ def main():
                     help="chunks a search is pipelined in (hmm_db_pipeline; 0 = the library's default, "
                          "1 = sequential stages, whose per-stage times give per-stage roofline fractions; "
                          "-1 = 1 for C4, whose 64 searches overlap through --streams, else the default)")
+    ap.add_argument("--group", type=int, default=-1,
+                    help="C4: searches per hmm_search_group call, each through its own database handle "
+                         "(default: all 64 in one call; 0: separate hmm_search calls spread over --streams)")
     ap.add_argument("--bias", action="store_true",
                     help="run the cascade with the composition-bias filter between MSV and Viterbi")
     ap.add_argument("--iterations", type=int, default=1,
@@ -163,6 +166,13 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     batched = args.workload == "C4"
+    if args.group < 0:
+        args.group = 64 if batched and args.dbs == 1 else 0
+    if args.group and (not batched or args.dbs != 1):
+        print("--group applies to C4 with one database", file=sys.stderr)
+        sys.exit(2)
+    if args.group:
+        args.streams = 1
     if args.streams <= 0:
         args.streams = 4 if batched else 1
     if args.pipeline < 0:
@@ -212,12 +222,20 @@ def main():
         log(f"copy probe: {src.numel()} bytes read and written once")
         del src, dst
 
+    # group mode: search i through handle i of the database, `group` searches per call
+    ghandles = [D] + [D.share() for _ in range(len(Ps) - 1)] if args.group else []
+
     def step():
+        if args.group:
+            for a in range(0, len(Ps), args.group):
+                b = min(len(Ps), a + args.group)
+                hg.search_group(Ps[a:b], ghandles[a:b], F, outs[a:b], stream=stream, bias_filter=args.bias)
+            return
         for i, ((pi, di), out) in enumerate(zip(jobs, outs)):
             j = i % S
             hg.search(Ps[pi], lanes[j][di], F, out, stream=streams[j], bias_filter=args.bias)
 
-    timed_stages = S == 1 and len(Ds) == 1
+    timed_stages = S == 1 and len(Ds) == 1 and not args.group
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -276,6 +294,8 @@ def main():
                f"{sum(Dx.n_residues for Dx in Ds)} residues in all)")
     if S > 1:
         wl += f", searches spread over {S} concurrent streams and database handles"
+    if args.group:
+        wl += f", hmm_search_group of {args.group} searches per call (one handle each)"
     wl += f", MSV P<{F[0]:g}{' -> composition-bias filter' if args.bias else ''} -> Viterbi P<{F[1]:g} -> Forward"
     rec = {
         "metric": "GCUPS (profile cols x DB residues /s), MSV+Viterbi+Forward, M=734 vs 1M seqs",
@@ -326,6 +346,8 @@ def main():
     for lane in lanes[1:]:
         for h in lane:
             h.close()
+    for h in ghandles[1:]:
+        h.close()
     for Dx in Ds:
         Dx.close()
     if not args.no_cpu_baseline and not batched and len(Ds) == 1:

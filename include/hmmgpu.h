@@ -182,6 +182,28 @@ int hmm_db_share(const hmm_db *db, hmm_db **out);
 int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t,
                const hmm_results *out, hmm_stream stream);
 
+/* A group of searches of one database by n different profiles: search i is
+ * profile p[i] against handle db[i] with cutoffs t[i] into out[i], and every
+ * result equals that of hmm_search(p[i], db[i], &t[i], &out[i], stream).
+ * The handles must be n distinct handles of one uploaded database (the
+ * first from hmm_db_upload, the others from hmm_db_share).  This is the
+ * many-queries mode of the paper's large-scale run (thousands of proteins,
+ * each searched against the same databases; Evaluation section): the MSV
+ * stage of profiles that share a kernel instance (the diagonal layout with
+ * 1-3 vectors per lane, i.e. M up to 383) runs as one kernel for up to 4 of
+ * them, so one wave scores a target against several profiles and the
+ * residue stream and its scalar handling are shared; the other profiles'
+ * MSV runs as in hmm_search.  Each search then runs its later stages on its
+ * own handle's streams, concurrently with the others, all joined back into
+ * `stream`.  Searches are not chunked (hmm_db_pipeline does not apply).
+ * Enqueued on `stream` like hmm_search (same host waits when a handle's
+ * profile or cutoffs change); allocates nothing.
+ * Errors: HMM_EINVAL (n < 1; NULL array or element; a handle twice; handles
+ * of different databases; bad cutoffs or NULL output buffers as in
+ * hmm_search), HMM_EDEVICE; on an error nothing is enqueued. */
+int hmm_search_group(const hmm_profile *const *p, hmm_db *const *db, const hmm_thresholds *t,
+                     const hmm_results *out, int32_t n, hmm_stream stream);
+
 /* ---------------------------------------------------------------- decoding
  *
  * The step after the filter cascade: for the targets that passed it, the

@@ -29,7 +29,7 @@ HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
             "hmm_count", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables",
             "hmm_decode", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
-            "hmm_profile_upload", "hmm_search", "hmm_strerror")
+            "hmm_profile_upload", "hmm_search", "hmm_search_group", "hmm_strerror")
 
 
 class HmmError(RuntimeError):
@@ -86,6 +86,8 @@ def lib():
         L.hmm_db_share.argtypes = [vp, C.POINTER(vp)]
         L.hmm_search.restype = C.c_int
         L.hmm_search.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), vp]
+        L.hmm_search_group.restype = C.c_int
+        L.hmm_search_group.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), i32, vp]
         L.hmm_count.restype = C.c_int
         L.hmm_count.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp]
         L.hmm_rebuild.restype = C.c_int
@@ -211,6 +213,29 @@ def hmm_search(profile: int, db: int, F, out: dict, stream=None, bias_filter: bo
            "hmm_search")
 
 
+def _results(out: dict) -> hmm_results:
+    return hmm_results(out["msv"].data_ptr(), out["vit"].data_ptr(), out["fwd"].data_ptr(),
+                       out["flags"].data_ptr(), out["counts"].data_ptr() if out.get("counts") is not None else None,
+                       out["bias"].data_ptr() if out.get("bias") is not None else None)
+
+
+def hmm_search_group(profiles, dbs, Fs, outs, stream=None, bias_filter=False) -> None:
+    """Enqueue a group of searches: search i is profiles[i] against handle
+    dbs[i] (distinct handles of one database) with cutoffs Fs[i] into
+    outs[i] (dicts as in hmm_search); bias_filter: one flag or one per
+    search."""
+    n = len(profiles)
+    bf = list(bias_filter) if isinstance(bias_filter, (list, tuple)) else [bias_filter] * n
+    if not (len(dbs) == len(Fs) == len(outs) == len(bf) == n):
+        raise ValueError("profiles, dbs, Fs, outs (and bias_filter) must have one entry per search")
+    P = (C.c_void_p * max(n, 1))(*[C.c_void_p(h) for h in profiles])
+    D = (C.c_void_p * max(n, 1))(*[C.c_void_p(h) for h in dbs])
+    T = (hmm_thresholds * max(n, 1))(*[hmm_thresholds(*[float(v) for v in F[:3]], int(bool(b)))
+                                       for F, b in zip(Fs, bf)])
+    R = (hmm_results * max(n, 1))(*[_results(o) for o in outs])
+    _check(lib().hmm_search_group(P, D, T, R, int(n), _stream_handle(stream)), "hmm_search_group")
+
+
 def hmm_decode(profile: int, db: int, flags, mask: int, out: dict, stream=None) -> None:
     """Enqueue posterior decoding.  `flags`: device uint8 tensor (caller
     order) or None (decode every target); `out` maps dom (int32 [max_dom, 9])
@@ -331,6 +356,22 @@ def search(profile: Profile, db: Database, F, out: dict | None = None, stream=No
         stream = torch.cuda.current_stream()
     hmm_search(profile.handle, db.handle, F, out, stream, bias_filter)
     return out
+
+
+def search_group(profiles, dbs, F, outs=None, stream=None, bias_filter=False) -> list:
+    """Run a group of searches (profiles[i] against dbs[i], distinct
+    handles of one database, e.g. a Database and its .share() handles) on
+    the current torch stream (or `stream`); F: one cutoff triple or one per
+    search.  Returns the device result dicts, in order."""
+    import torch
+    n = len(profiles)
+    Fs = list(F) if F and isinstance(F[0], (list, tuple)) else [F] * n
+    if outs is None:
+        outs = [alloc_results(d.n) for d in dbs]
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    hmm_search_group([p.handle for p in profiles], [d.handle for d in dbs], Fs, outs, stream, bias_filter)
+    return outs
 
 
 def decode(profile: Profile, db: Database, flags=None, mask: int = HMM_FWD_PASS, max_dom: int | None = None,

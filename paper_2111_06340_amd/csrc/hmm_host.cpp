@@ -886,6 +886,58 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   return HMM_OK;
 }
 
+int hmm_search_group(const hmm_profile *const *p, hmm_db *const *db, const hmm_thresholds *t,
+                     const hmm_results *out, int32_t n, hmm_stream stream) {
+  if (n < 1) return fail(HMM_EINVAL, "n = %d; need at least one search", n);
+  if (!p || !db || !t || !out) return fail(HMM_EINVAL, "NULL profile, db, thresholds or results array");
+  // every check before any HIP call: a rejected group enqueues nothing
+  for (int i = 0; i < n; i++) {
+    if (!p[i] || !db[i]) return fail(HMM_EINVAL, "search %d: NULL profile or db", i);
+    if (db[i]->data != db[0]->data) return fail(HMM_EINVAL, "search %d: handle of another database", i);
+    for (int j = 0; j < i; j++)
+      if (db[j] == db[i]) return fail(HMM_EINVAL, "searches %d and %d use the same handle", j, i);
+    const hmm_thresholds &ti = t[i];
+    if (std::isnan(ti.F1) || std::isnan(ti.F2) || std::isnan(ti.F3) || !(ti.F1 > 0) || !(ti.F2 > 0) ||
+        !(ti.F3 > 0))
+      return fail(HMM_EINVAL, "search %d: P-value cutoffs must be > 0", i);
+    if (ti.bias_filter != 0 && ti.bias_filter != 1)
+      return fail(HMM_EINVAL, "search %d: bias_filter = %d; need 0 or 1", i, ti.bias_filter);
+    if (db[i]->n > 0 && (!out[i].msv || !out[i].vit || !out[i].fwd || !out[i].flags))
+      return fail(HMM_EINVAL, "search %d: NULL output buffer", i);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (db[0]->n == 0) return HMM_OK;
+  std::vector<DevProfile> P(n);
+  std::vector<DevDb> D(n);
+  std::vector<DevOut> O(n);
+  std::vector<const SearchSync *> Y(n);
+  for (int i = 0; i < n; i++) {
+    hmm_db *d = db[i];
+    if (d->searched) HIP_TRY(hipStreamWaitEvent(s, d->done, 0), "hipStreamWaitEvent");
+    if (d->lp_serial != p[i]->serial || d->lp_F[0] != t[i].F1 || d->lp_F[1] != t[i].F2 || d->lp_F[2] != t[i].F3) {
+      if (d->searched) HIP_TRY(hipEventSynchronize(d->done), "hipEventSynchronize");
+      for (int L = 0; L <= d->max_len; L++) length_params(p[i], &t[i], L < 1 ? 1 : L, &d->h_lp[L], nullptr);
+      HIP_TRY(hipMemcpyAsync(d->d_lp, d->h_lp, sizeof(LenParams) * ((size_t)d->max_len + 1),
+                             hipMemcpyHostToDevice, s),
+              "hipMemcpyAsync(length table)");
+      d->lp_serial = p[i]->serial;
+      d->lp_F[0] = t[i].F1;
+      d->lp_F[1] = t[i].F2;
+      d->lp_F[2] = t[i].F3;
+    }
+    P[i] = p[i]->dev;
+    D[i] = chunk_of(d->dev, 0, d->n, 0);
+    O[i] = DevOut{out[i].msv, out[i].vit, out[i].fwd, out[i].flags, out[i].counts, out[i].bias, t[i].bias_filter};
+    Y[i] = &d->sync;
+  }
+  HIP_TRY(launch_search_group(P.data(), D.data(), O.data(), n, s, Y.data()), "kernel launch");
+  for (int i = 0; i < n; i++) {
+    HIP_TRY(hipEventRecord(db[i]->done, s), "hipEventRecord");
+    db[i]->searched = true;
+  }
+  return HMM_OK;
+}
+
 int hmm_count(const hmm_profile *p, hmm_db *db, const hmm_domain *dom, const int32_t *n_dom, int32_t max_dom,
               const int16_t *aln, uint32_t *counts, hmm_stream stream) {
   if (!p || !db || !dom || !n_dom || !aln || !counts) return fail(HMM_EINVAL, "NULL argument");

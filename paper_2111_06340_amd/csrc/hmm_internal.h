@@ -180,6 +180,12 @@ inline DevDb chunk_of(const DevDb &d, int64_t a, int64_t b, int k) {
 hipError_t launch_search(const DevProfile &p, const DevDb *chunk, int nchunks, const DevOut &out,
                          hipStream_t stream, const SearchSync &sync, hipEvent_t *ev);
 
+// Enqueue a group of n one-chunk searches of one database (one handle each):
+// MSV of profiles sharing a diagonal instance as group kernels, then each
+// search's tail on its own streams y[i], joined back into `stream`.
+hipError_t launch_search_group(const DevProfile *P, const DevDb *db, const DevOut *o, int n, hipStream_t stream,
+                               const SearchSync *const *y);
+
 // Enqueue the emission and transition counts of the alignments of
 // dom[0 .. min(*n_dom, max_dom)) (codes in aln, caller residue layout) into
 // counts: uint32 [M][20] match, [M-1][20] insert, [M-1][7] transitions.

@@ -26,6 +26,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <vector>
 
 #include "hmm_device.h"
 #include "hmm_internal.h"
@@ -530,6 +531,231 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   }
 }
 
+// ---------------------------------------------------------------- MSV of a group of profiles
+// Several searches of one database by different profiles of the same
+// diagonal instance (Q): one wave scores a target against G profiles at
+// once.  The residue stream, its scalar handling and M0 are shared: the
+// tables sit interleaved in LDS as [residue][profile][P], so one M0 serves
+// the G profiles' reads (profile g at immediate offset g * P * 4).  Each
+// profile keeps its own state, running maxima, xJ/xB and trigger value,
+// exactly as msv_target_diag, and its own outputs and survivor list.  A
+// profile that overflows stops taking part in the tests (its trigger value
+// becomes +inf); its cells keep being computed and are ignored.
+template <int G>
+struct MsvGroup {
+  DevProfile P[G];
+  DevDb db[G];
+  DevOut out[G];
+};
+
+template <int Q, int G>
+__device__ __forceinline__ void lds_load_group(uint32_t (&c)[G * Q], int m0) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(m0));
+#pragma unroll
+  for (int g = 0; g < G; g++)
+#pragma unroll
+    for (int q = 0; q < Q; q++)
+      asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[g * Q + q]) : "i"((g * 2 * Q + q) * kWave * 4));
+}
+
+template <int Q, int G>
+__global__ void __launch_bounds__(1024) msv_group_kernel(MsvGroup<G> A) {
+  constexpr int kHalf = Q * kWave;       // P/2
+  constexpr int kRowB = 2 * kHalf * 4;   // bytes per residue and profile
+  extern __shared__ uint32_t lds[];
+  for (int g = 0; g < G; g++) {
+    const uint32_t *src = A.P[g].msv;
+    for (int i = threadIdx.x; i < kAlpha * 2 * kHalf; i += blockDim.x) {
+      const int a = i / (2 * kHalf), c = i - a * (2 * kHalf);
+      lds[(a * G + g) * (2 * kHalf) + c] = src[i];
+    }
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
+  const DevDb &D0 = A.db[0];
+  const int n = (int)D0.n;
+  auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
+  constexpr uint32_t kInf2 = 0x7c007c00u;   // (+inf, +inf): never fires
+  uint32_t ca[G * Q], cb[G * Q];
+#pragma unroll
+  for (int i = 0; i < G * Q; i++) ca[i] = cb[i] = 0;
+  int t = wave_id();
+  int Lnext = 0;
+  int64_t snext = 0;
+  if (t < n) {
+    Lnext = uni(D0.len[t]);
+    snext = D0.start[t];
+  }
+  for (; t < n; t += nw) {
+    const int L = Lnext;
+    const uint8_t *x = D0.res + snext;
+    const int cperm = D0.perm[t];
+    int mv[G], base[G], xJt[G], Bx[G], ovf_line[G];
+    bool ovf[G];
+    uint32_t nbx[G], thr[G];
+    h16x2 w[G][Q], acc_e[G], acc_o[G];
+    auto trigger_thr = [&](int g) {
+      return ovf[g] ? kInf2 : splat(min(ovf_line[g], max(xJt[g], kBase8) + 4) - Bx[g] - 1);
+    };
+#pragma unroll
+    for (int g = 0; g < G; g++) {
+      mv[g] = A.db[g].lp[L].move8;
+      base[g] = max(kBase8 - mv[g], 0);
+      ovf_line[g] = 255 - A.P[g].bias8;
+      xJt[g] = 0;
+      Bx[g] = min(max(base[g] - A.P[g].entry8, 0), max(ovf_line[g], 0));
+      ovf[g] = ovf_line[g] <= 0;
+      acc_e[g] = acc_o[g] = as_h2(splat(-Bx[g]));
+#pragma unroll
+      for (int q = 0; q < Q; q++) w[g][q] = acc_e[g];
+      nbx[g] = splat(-Bx[g]);
+      thr[g] = trigger_thr(g);
+    }
+    auto settle = [&](int g, int m) {
+      xJt[g] = max(xJt[g], max(m - A.P[g].exit8, 0));
+      return min(max(max(base[g], max(xJt[g] - mv[g], 0)) - A.P[g].entry8, 0), ovf_line[g]);
+    };
+    auto fold = [&](h16x2 &acc, const h16x2 (&v)[Q]) {
+#pragma unroll
+      for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, v[q], v[q + 1]);
+      if (Q & 1) acc = __builtin_elementwise_maximum(acc, v[Q - 1]);
+    };
+    auto fired = [&](int g) { return any_lane(as_u(h2_max3(acc_o[g], as_h2(thr[g]), acc_e[g])) != thr[g]); };
+    auto rebase = [&](int g, int nBx) {
+      const h16x2 d = as_h2(splat(Bx[g] - nBx));
+#pragma unroll
+      for (int q = 0; q < Q; q++) w[g][q] += d;
+      acc_e[g] += d;
+      acc_o[g] += d;
+      Bx[g] = nBx;
+      nbx[g] = splat(-nBx);
+    };
+    int lofs = 0;
+    auto pin = [&]() {
+#pragma unroll
+      for (int g = 0; g < G; g++)
+#pragma unroll
+        for (int q = 0; q < Q; q++) asm volatile("" : "+v"(w[g][q]));
+    };
+    auto load = [&](uint32_t(&c)[G * Q], int a) {
+      lds_load_group<Q, G>(c, a * (G * kRowB) + lofs);
+      lofs += 4;
+      pin();
+    };
+    auto row = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int kind) -> bool {
+#pragma unroll
+      for (int g = 0; g < G; g++)
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          const h16x2 e = as_h2(c[g * Q + q]);
+          w[g][q] = h2_max3(w[g][q] + e, e, as_h2(nbx[g]));
+        }
+#pragma unroll
+      for (int g = 0; g < G; g++) fold(kind == 1 ? acc_o[g] : acc_e[g], w[g]);
+      pin();
+      lds_wait(next);
+      if (kind == 0) return false;
+      uint64_t any = 0;
+#pragma unroll
+      for (int g = 0; g < G; g++)
+        any |= __builtin_amdgcn_ballot_w64(as_u(h2_max3(acc_o[g], as_h2(thr[g]), acc_e[g])) != thr[g]);
+      if (!any) return false;
+      bool stop = false;
+#pragma unroll
+      for (int g = 0; g < G; g++) {
+        if (!fired(g)) continue;
+        if (kind == 2 || !any_lane(as_u(__builtin_elementwise_maximum(acc_e[g], as_h2(thr[g]))) != thr[g])) {
+          stop = true;   // the tested row reached the trigger: the caller settles it
+          continue;
+        }
+        // the pair's first row reached the trigger: settle it, correct the second row
+        const int m = wave_max_i32(h2_hmax(acc_e[g])) + Bx[g];
+        if (m >= ovf_line[g]) {
+          ovf[g] = true;
+          thr[g] = kInf2;
+          continue;
+        }
+        const int nBx = settle(g, m);
+        if (nBx != Bx[g]) {
+          const h16x2 d = as_h2(splat(Bx[g] - nBx));
+#pragma unroll
+          for (int q = 0; q < Q; q++) w[g][q] = __builtin_elementwise_maximum(w[g][q] + d, as_h2(c[g * Q + q]));
+          acc_e[g] += d;
+          acc_o[g] += d;
+          fold(acc_o[g], w[g]);
+          Bx[g] = nBx;
+          nbx[g] = splat(-nBx);
+        }
+        thr[g] = trigger_thr(g);
+        if (fired(g)) stop = true;
+      }
+      return stop;
+    };
+    int r = 0;
+    for (;;) {
+      bool all_ovf = true;
+#pragma unroll
+      for (int g = 0; g < G; g++) all_ovf = all_ovf && ovf[g];
+      if (all_ovf) break;
+      int stop = 0;
+      const int limit = (r / kHalf + 1) * kHalf;   // end of the current phase
+      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
+#pragma unroll
+      for (int g = 0; g < G; g++) {   // settle every profile whose trigger fired on the stop row
+        if (!fired(g)) continue;
+        const int m = wave_max_i32(h2_hmax(__builtin_elementwise_maximum(acc_e[g], acc_o[g]))) + Bx[g];
+        if (m >= ovf_line[g]) {
+          ovf[g] = true;
+          thr[g] = kInf2;
+          continue;
+        }
+        const int nBx = settle(g, m);
+        if (nBx != Bx[g]) rebase(g, nBx);
+        thr[g] = trigger_thr(g);
+      }
+      r = stop + 1;
+      if (r >= L) break;
+      lofs = 4 * (r % kHalf);
+      if (lofs == 0) {  // the halves of every state dword swap diagonals
+#pragma unroll
+        for (int g = 0; g < G; g++)
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const uint32_t u = as_u(w[g][q]);
+            w[g][q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
+          }
+      }
+    }
+    if (t + nw < n) {
+      Lnext = uni(D0.len[t + nw]);
+      snext = D0.start[t + nw];
+    }
+    const int c = uni(cperm);
+#pragma unroll
+    for (int g = 0; g < G; g++) {
+      int raw = 255;
+      if (!ovf[g]) {
+        const int m = wave_max_i32(h2_hmax(__builtin_elementwise_maximum(acc_e[g], acc_o[g]))) + Bx[g];
+        raw = max(max(m - A.P[g].exit8, 0) - mv[g], 0);
+      }
+      const DevDb &Dg = A.db[g];
+      const DevOut &Og = A.out[g];
+      const bool pass = ovf[g] || raw >= Dg.lp[L].thr8;
+      const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf[g] ? HMM_MSV_OVF : 0);
+      Dg.flags_sorted[t] = fl;
+      Og.flags[c] = fl;
+      Og.msv[c] = (int16_t)raw;
+      Og.vit[c] = INT32_MIN;
+      Og.fwd[c] = __builtin_nanf("");
+      if (pass) {
+        const bool bf = Og.bias_filter != 0;
+        (bf ? Dg.list_ovf : Dg.list_vit)[wave_fetch_add(&Dg.counters[bf ? CNT_OVF : CNT_VIT], 1)] = t;
+      }
+    }
+  }
+}
+
 // Composition-bias filter on the MSV passes (list_ovf, count CNT_OVF): the
 // bias score of each, and the ones whose MSV score less the bias still
 // reaches the cutoff (or that overflowed MSV) go on to Viterbi's list.
@@ -1025,6 +1251,31 @@ hipError_t launch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, hip
   return hipGetLastError();
 }
 
+template <int Q, int G>
+hipError_t launch_msv_group_t(const DevProfile *P, const DevDb *db, const DevOut *o, hipStream_t s) {
+  MsvGroup<G> A;
+  for (int g = 0; g < G; g++) {
+    A.P[g] = P[g];
+    A.db[g] = db[g];
+    A.out[g] = o[g];
+  }
+  const int threads = 1024;
+  const size_t lds = (size_t)G * kAlpha * 2 * Q * kWave * 4;
+  auto k = msv_group_kernel<Q, G>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  static int bpc = 0;
+  if (!bpc) bpc = blocks_per_cu(k, threads, lds);
+  int64_t blocks = (int64_t)bpc * num_cu();
+  const int64_t cap = (db[0].n + threads / 64 - 1) / (threads / 64);
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), lds, s, A);
+  return hipGetLastError();
+}
+
 template <int Q>
 hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   constexpr bool kLds = Q <= 8;
@@ -1124,6 +1375,20 @@ hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, h
   return hipErrorInvalidValue;
 }
 
+// Largest group of profiles the group MSV kernel takes at Q vectors per lane
+// (diagonal layout): as many tables as two 1024-thread blocks per CU can hold
+// in LDS (about 60 KB each), at most 4; 1 = no group instance.
+int msv_group_max(int Q) { return Q == 1 ? 4 : Q == 2 ? 3 : Q == 3 ? 2 : 1; }
+
+hipError_t dispatch_msv_group(const DevProfile *P, const DevDb *db, const DevOut *o, int G, hipStream_t s) {
+  const int Q = P[0].Qm;
+#define HMM_GROUP(q, g) \
+  if (Q == q && G == g) return launch_msv_group_t<q, g>(P, db, o, s);
+  HMM_GROUP(1, 2) HMM_GROUP(1, 3) HMM_GROUP(1, 4) HMM_GROUP(2, 2) HMM_GROUP(2, 3) HMM_GROUP(3, 2)
+#undef HMM_GROUP
+  return hipErrorInvalidValue;
+}
+
 hipError_t dispatch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   switch (P.Q8) {
 #define HMM_CASE(q) \
@@ -1161,6 +1426,9 @@ hipError_t dispatch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, h
 
 }  // namespace
 
+hipError_t launch_tail(const DevProfile &P, const DevDb *chunk, int K, const DevOut &o, hipStream_t s,
+                       const SearchSync &y, hipEvent_t *ev);
+
 hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const DevOut &o, hipStream_t s,
                          const SearchSync &y, hipEvent_t *ev) {
   if (K < 1 || K > kMaxChunks) return hipErrorInvalidValue;
@@ -1184,9 +1452,24 @@ hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const D
     ok(hipEventRecord(y.msv_done[k], s));
   }
   mark(1, s);
-  // the rest of each chunk's cascade as soon as its MSV is done.  An int16
-  // overflow passes the Viterbi filter whatever its exact score, so Forward
-  // needs nothing from the rescore: the two run side by side.
+  if (e != hipSuccess) return e;
+  return launch_tail(P, chunk, K, o, s, y, ev);
+}
+
+// The rest of each chunk's cascade as soon as its MSV is done (event
+// y.msv_done[k] on the search stream).  An int16 overflow passes the
+// Viterbi filter whatever its exact score, so Forward needs nothing from
+// the rescore: the two run side by side.
+hipError_t launch_tail(const DevProfile &P, const DevDb *chunk, int K, const DevOut &o, hipStream_t s,
+                       const SearchSync &y, hipEvent_t *ev) {
+  hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+    return e == hipSuccess;
+  };
+  auto mark = [&](int i, hipStream_t st) {
+    if (ev) ok(hipEventRecord(ev[i], st));
+  };
   for (int k = 0; k < K && e == hipSuccess; k++) {
     const bool any = chunk[k].n > 0;
     if (!ok(hipStreamWaitEvent(y.tail, y.msv_done[k], 0))) break;
@@ -1206,6 +1489,53 @@ hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const D
     ok(hipGetLastError());
   }
   mark(4, s);
+  return e;
+}
+
+// Several searches of one database (one handle each) by different profiles,
+// one chunk each: their counters are cleared, the MSV of profiles sharing a
+// diagonal instance runs as group kernels (up to msv_group_max profiles per
+// launch; the others alone), then each search's composition-bias filter
+// (if on) and its cascade tail on its own handle's streams, all joined back
+// into `s`.
+hipError_t launch_search_group(const DevProfile *P, const DevDb *db, const DevOut *o, int n, hipStream_t s,
+                               const SearchSync *const *y) {
+  hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t r) {
+    if (e == hipSuccess) e = r;
+    return e == hipSuccess;
+  };
+  for (int i = 0; i < n && e == hipSuccess; i++) {
+    hipLaunchKernelGGL(clear_counters, dim3(1), dim3(256), 0, s, db[i].counters, 1);
+    ok(hipGetLastError());
+  }
+  std::vector<int> done(n, 0);
+  for (int i = 0; i < n && e == hipSuccess; i++) {
+    if (done[i] || db[i].n == 0) continue;
+    const int gmax = P[i].msv_diag ? msv_group_max(P[i].Qm) : 1;
+    std::vector<int> grp{i};
+    for (int j = i + 1; j < n && (int)grp.size() < gmax; j++)
+      if (!done[j] && P[j].msv_diag && P[j].Qm == P[i].Qm) grp.push_back(j);
+    for (int j : grp) done[j] = 1;
+    if (grp.size() == 1) {
+      ok(dispatch_msv(P[i], db[i], o[i], s));
+      continue;
+    }
+    DevProfile gp[4];
+    DevDb gd[4];
+    DevOut go[4];
+    for (size_t g = 0; g < grp.size(); g++) {
+      gp[g] = P[grp[g]];
+      gd[g] = db[grp[g]];
+      go[g] = o[grp[g]];
+    }
+    ok(dispatch_msv_group(gp, gd, go, (int)grp.size(), s));
+  }
+  for (int i = 0; i < n && e == hipSuccess; i++) {
+    if (o[i].bias_filter && db[i].n > 0) ok(launch_bias(P[i], db[i], o[i], s));
+    ok(hipEventRecord(y[i]->msv_done[0], s));
+  }
+  for (int i = 0; i < n && e == hipSuccess; i++) ok(launch_tail(P[i], &db[i], 1, o[i], s, *y[i], nullptr));
   return e;
 }
 

@@ -554,3 +554,108 @@ def test_bias_filter(name, n):
              f"cutoff, max bias error {np.max(np.abs(g['bias'][ran] - o['beta'][ran])):.2e} ok {st}")
     P.close()
     D.close()
+
+
+def _group_db(profs, seed, n_bg=2500):
+    """Background targets of the C2 length law, the ragged edge lengths,
+    and homologs of every profile (so that every profile overflows MSV
+    somewhere and reaches its later stages)."""
+    rng = np.random.default_rng(seed)
+    w = gen.WORKLOADS["C2"]
+    base = gen.workload_database(w, n=n_bg, prof=profs[0])
+    seqs = [base.seq(i) for i in range(base.n)]
+    seqs += [gen.background_residues(rng, L) for L in EDGE_LENGTHS]
+    for p in profs:
+        for h in gen.sample_homologs(rng, p, 3):
+            L = int(h.size + rng.integers(0, 200))
+            s = gen.background_residues(rng, L)
+            o = int(rng.integers(0, L - h.size + 1))
+            s[o:o + h.size] = h
+            seqs.append(s)
+    order = rng.permutation(len(seqs))
+    seqs = [seqs[i] for i in order]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    return np.concatenate(seqs), off
+
+
+def test_search_group_matches_oracle_and_single_searches():
+    """hmm_search_group: profiles of every MSV group size (1-3 vectors per
+    lane, grouped up to 4, 3 and 2 at a time) and larger ones that run
+    alone, each with its own cutoffs (one with the composition-bias
+    filter), against one database through distinct handles.  Every result
+    equals the oracle's and, bit for bit, the single hmm_search's; a second
+    group call (scratch reused, cutoffs changed) again matches."""
+    import torch
+    Ms = [50, 77, 100, 127, 128, 200, 255, 256, 300, 383, 384, 734, 60]
+    profs = []
+    for i, M in enumerate(Ms):
+        if i % 3 == 2:   # peaked random transitions and emissions: many triggers and delete runs
+            profs.append(random_profile(M, 4400 + M, alpha=0.3, talpha=0.5))
+        else:
+            profs.append(gen.make_profile(M, 4300 + M))
+    res, off = _group_db(profs, 4500)
+    calibs = [oracle.calibrate(oracle.OracleProfile(p), nthreads=NTHREADS, n=100) for p in profs]
+    Ps = [hg.Profile(p, *c) for p, c in zip(profs, calibs)]
+    D = hg.Database(res, off)
+    handles = [D] + [D.share() for _ in profs[1:]]
+    Fs = [(0.05, 0.01, 1.0), (0.2, 0.05, 1.0), (1.0, 1.0, 1.0)] * 5
+    Fs = Fs[:len(profs)]
+    bias = [i == 4 for i in range(len(profs))]
+    for rnd in range(2):
+        if rnd == 1:
+            Fs = [(0.02, 1e-3, 1.0)] * len(profs)
+        announce(f"group round {rnd}: {len(profs)} profiles M={Ms} n={D.n} residues={D.n_residues}")
+        outs = hg.search_group(Ps, handles, Fs, bias_filter=bias)
+        torch.cuda.synchronize()
+        for i, (p, c, o) in enumerate(zip(profs, calibs, outs)):
+            g = {k: v.cpu().numpy() for k, v in o.items()}
+            single = hg.alloc_results(D.n)
+            H = D.share()
+            hg.search(Ps[i], H, Fs[i], single, bias_filter=bias[i])
+            torch.cuda.synchronize()
+            H.close()
+            s1 = {k: v.cpu().numpy() for k, v in single.items()}
+            for k in ("msv", "vit", "flags", "counts"):
+                assert np.array_equal(g[k], s1[k]), f"group vs single {k} differ, profile {i} M={p.M}"
+            assert np.array_equal(np.isnan(g["fwd"]), np.isnan(s1["fwd"]))
+            ran = ~np.isnan(g["fwd"])
+            assert np.array_equal(g["fwd"][ran], s1["fwd"][ran])
+            if bias[i]:
+                continue   # the bias filter's own parity test covers the oracle side
+            ref = oracle_search(p, res, off, c, Fs[i])
+            st = compare(g, ref, what=f"group M={p.M}")
+            announce(f"group round {rnd} profile {i} M={p.M} ok {st}")
+    for H in handles:
+        H.close()
+    for P in Ps:
+        P.close()
+
+
+def test_search_group_rejects_bad_groups():
+    w = gen.WORKLOADS["C1"]
+    prof = gen.workload_profile(w)
+    db = gen.workload_database(w, n=200, prof=prof)
+    P = hg.Profile(prof, 0.0, 0.0, 0.0)
+    D = hg.Database(db.residues, db.offsets)
+    S = D.share()
+    E = hg.Database(db.residues, db.offsets)
+    F = (0.5, 0.5, 1.0)
+    outs = [hg.alloc_results(D.n) for _ in range(2)]
+
+    def status(profiles, dbs, Fs, o):
+        try:
+            hg.hmm_search_group([p.handle for p in profiles], [d.handle for d in dbs], Fs, o)
+        except hg.HmmError as e:
+            return e.status
+        return hg.HMM_OK
+
+    assert status([P, P], [D, D], [F, F], outs) == hg.HMM_EINVAL        # one handle twice
+    assert status([P, P], [D, E], [F, F], outs) == hg.HMM_EINVAL        # two databases
+    assert status([P, P], [D, S], [F, (0.0, 0.5, 1.0)], outs) == hg.HMM_EINVAL
+    assert status([], [], [], []) == hg.HMM_EINVAL
+    assert status([P, P], [D, S], [F, F], outs) == hg.HMM_OK
+    import torch
+    torch.cuda.synchronize()
+    for h in (S, D, E, P):
+        h.close()
