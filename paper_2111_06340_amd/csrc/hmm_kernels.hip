@@ -874,19 +874,24 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
       D[q] = i16_max(i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q])), tau2);
       dc = D[q];
     }
-    for (int it = 0; it < 2 * kWave; it++) {
-      dc = slot_up16(D[Q - 1]);
-      bool moved = true;
+    // A chain can cross into the next slot only from a slot whose last
+    // delete value is above the floor (sat(tau + DD) <= tau <= D): when every
+    // slot's last value is at the floor, nothing is left to propagate.
+    if (any_lane(D[Q - 1] != tau2)) {
+      for (int it = 0; it < 2 * kWave; it++) {
+        dc = slot_up16(D[Q - 1]);
+        bool moved = true;
 #pragma unroll
-      for (int q = 0; q < Q; q++) {
-        if (moved) {
-          const uint32_t nd = i16_max(D[q], i16_adds(dc, tr[TR_DDIN][q]));
-          moved = any_lane(nd != D[q]);
-          D[q] = nd;
-          dc = nd;
+        for (int q = 0; q < Q; q++) {
+          if (moved) {
+            const uint32_t nd = i16_max(D[q], i16_adds(dc, tr[TR_DDIN][q]));
+            moved = any_lane(nd != D[q]);
+            D[q] = nd;
+            dc = nd;
+          }
         }
+        if (!moved) break;
       }
-      if (!moved) break;
     }
     if (any_lane(i16_max(accM, tm1) != tm1)) {
       const int m = wave_max_i32(hmax16(accM));
