@@ -163,11 +163,24 @@ __device__ float bias_score(const DevProfile &P, const uint8_t *x, int L, int la
 // scan), never carried across this code.
 // A scalar write of M0 needs one wait state before an add-TID LDS
 // instruction reads it (the s_nop).
-template <int Q>
-__device__ __forceinline__ void lds_load_tid(uint32_t (&c)[Q], int m0) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(m0));
+template <int K, int Q>
+__device__ __forceinline__ void lds_load_tid(uint32_t (&c)[Q], int base, int ofs) {
+  asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0" ::"s"(base), "s"(ofs));
 #pragma unroll
-  for (int q = 0; q < Q; q++) asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[q]) : "i"(q * kWave * 4));
+  for (int q = 0; q < Q; q++) asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[q]) : "i"(q * kWave * 4 + K));
+}
+// compile-time row offset, passed to the table-read functor
+template <int K>
+struct RowK {
+  static constexpr int v = K;
+};
+
+// Lane j: dword j + 1 of the residue stream (lane 63: the next chunk's first
+// dword), so the four rows of dword j find their successor's residue with one
+// read and no branch at the chunk's end.
+__device__ __forceinline__ uint32_t next_dwords(uint32_t cur, uint32_t nxt) {
+  const int first = __builtin_amdgcn_readlane((int)nxt, 0);
+  return (uint32_t)__builtin_amdgcn_update_dpp(first, (int)cur, 0x130 /* wave_shl:1 */, 0xf, 0xf, false);
 }
 template <int Q>
 __device__ __forceinline__ void lds_wait(uint32_t (&c)[Q]) {
@@ -178,20 +191,25 @@ __device__ __forceinline__ void lds_wait(uint32_t (&c)[Q]) {
 
 // Row driver of the diagonal MSV: residues four to a dword as in drive_rows,
 // table buffers in alternation, the rows of a dword taken in pairs.
+// load(RowK<K>{}, buf, a) reads residue a's table entries for the row K rows
+// after the current position; step(n) advances the position by n rows.
 // row(cur, next, kind) computes a row from `cur`, waits for the reads into
 // `next` (issued just before), then tests: kind 0 = first row of a pair (no
 // test), 1 = second row of a pair (tests both), 2 = a row on its own (start
 // or end of a run; tested).  Returns true if a row stopped the driver
-// (`stop` = the last row computed) or the limit was reached (`stop` =
-// limit - 1).
-template <int Q, typename Load, typename Row>
+// (`stop` = the last row computed) or the limit (a multiple of 4) was
+// reached (`stop` = limit - 1).  The residue chunks are loaded two ahead,
+// so the successor dwords of a chunk are at hand without waiting; reads run
+// at most 768 bytes past a target, inside the database's 1 KB zero tail.
+template <int Q, typename Load, typename Step, typename Row>
 __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int limit, int &stop, int lane,
-                                            uint32_t (&ba)[Q], uint32_t (&bb)[Q], Load load, Row row) {
+                                            uint32_t (&ba)[Q], uint32_t (&bb)[Q], Load load, Step step, Row row) {
   auto code = [](uint32_t w, int r) { return (int)((w >> (8 * r)) & 0xffu); };
   int r = r0;
   for (; (r & 3) != 0; r++) {
     if (r >= L) return false;
-    load(ba, uni((int)x[r]));
+    load(RowK<0>{}, ba, uni((int)x[r]));
+    step(1);
     lds_wait(ba);
     if (row(ba, ba, 2)) {
       stop = r;
@@ -203,38 +221,37 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
   const uint32_t *p = (const uint32_t *)(x + cs);
   uint32_t cur = __builtin_nontemporal_load(p + lane);
   uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
+  uint32_t nn = __builtin_nontemporal_load(p + 2 * kWave + lane);
+  uint32_t sh = next_dwords(cur, nxt);
   int j0 = (r & 255) >> 2;
   uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, j0);
-  load(ba, code(w, 0));
+  load(RowK<0>{}, ba, code(w, 0));
   lds_wait(ba);
   for (int c0 = cs;; c0 += 256) {
-    const int nfull = min(kWave, (L - c0) >> 2);
-    for (int j = j0; j < nfull; j++) {
-      const int rr = c0 + 4 * j;
-      if (rr >= limit) {
-        stop = rr - 1;
-        return true;
-      }
-      uint32_t wn;
-      if (j == kWave - 1)
-        wn = (uint32_t)__builtin_amdgcn_readlane((int)nxt, 0);
-      else
-        wn = (uint32_t)__builtin_amdgcn_readlane((int)cur, j + 1);
-      load(bb, code(w, 1));
+    const int nfull = min(kWave, (L - c0) >> 2);      // whole dwords of rows in this chunk
+    const int jlim = min(nfull, (limit - c0) >> 2);   // ... before the limit
+    for (int j = j0; j < jlim; j++) {
+      const uint32_t wn = (uint32_t)__builtin_amdgcn_readlane((int)sh, j);
+      load(RowK<1>{}, bb, code(w, 1));
       row(ba, bb, 0);
-      load(ba, code(w, 2));
+      load(RowK<2>{}, ba, code(w, 2));
       if (row(bb, ba, 1)) {
-        stop = rr + 1;
+        stop = c0 + 4 * j + 1;
         return true;
       }
-      load(bb, code(w, 3));
+      load(RowK<3>{}, bb, code(w, 3));
       row(ba, bb, 0);
-      load(ba, code(wn, 0));
+      load(RowK<4>{}, ba, code(wn, 0));
       if (row(bb, ba, 1)) {
-        stop = rr + 3;
+        stop = c0 + 4 * j + 3;
         return true;
       }
+      step(4);
       w = wn;
+    }
+    if (jlim < nfull) {
+      stop = c0 + 4 * jlim - 1;
+      return true;
     }
     if (nfull < kWave) {  // the target's last 0..3 rows (row 0's table already in ba)
       const int rt = c0 + 4 * nfull;
@@ -245,9 +262,10 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
       }
       for (int k = 0; rt + k < L; k++) {
         if (k) {
-          load(ba, code(w, k));
+          load(RowK<0>{}, ba, code(w, k));
           lds_wait(ba);
         }
+        step(1);
         if (row(ba, ba, 2)) {
           stop = rt + k;
           return true;
@@ -258,7 +276,9 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
     if (c0 + 256 >= L) return false;
     j0 = 0;
     cur = nxt;
-    nxt = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 2) * kWave + lane);
+    nxt = nn;
+    nn = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 3) * kWave + lane);
+    sh = next_dwords(cur, nxt);
   }
 }
 
@@ -319,11 +339,11 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
 #pragma unroll
       for (int q = 0; q < Q; q++) asm volatile("" : "+v"(w[q]));
     };
-    auto load = [&](uint32_t(&c)[Q], int a) {
-      lds_load_tid(c, a * kRowB + lofs);
-      lofs += 4;
+    auto load = [&](auto k, uint32_t(&c)[Q], int a) {
+      lds_load_tid<4 * decltype(k)::v>(c, a * kRowB, uni(lofs));
       pin();
     };
+    auto step = [&](int n) { lofs += 4 * n; };
     auto row = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int kind) -> bool {
 #pragma unroll
       for (int q = 0; q < Q; q++) {
@@ -359,7 +379,7 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
     for (;;) {
       int stop = 0;
       const int limit = (r / kHalf + 1) * kHalf;   // end of the current phase
-      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
+      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, step, row)) break;
       if (ovf) break;
       const int m = wave_max_i32(h2_hmax(__builtin_elementwise_maximum(acc_e, acc_o))) + Bx;
       if (m >= ovf_line) {
@@ -548,14 +568,14 @@ struct MsvGroup {
   DevOut out[G];
 };
 
-template <int Q, int G>
-__device__ __forceinline__ void lds_load_group(uint32_t (&c)[G * Q], int m0) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" ::"s"(m0));
+template <int K, int Q, int G>
+__device__ __forceinline__ void lds_load_group(uint32_t (&c)[G * Q], int base, int ofs) {
+  asm volatile("s_add_u32 m0, %0, %1\n\ts_nop 0" ::"s"(base), "s"(ofs));
 #pragma unroll
   for (int g = 0; g < G; g++)
 #pragma unroll
     for (int q = 0; q < Q; q++)
-      asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[g * Q + q]) : "i"((g * 2 * Q + q) * kWave * 4));
+      asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[g * Q + q]) : "i"((g * 2 * Q + q) * kWave * 4 + K));
 }
 
 template <int Q, int G>
@@ -638,11 +658,11 @@ __global__ void __launch_bounds__(1024) msv_group_kernel(MsvGroup<G> A) {
 #pragma unroll
         for (int q = 0; q < Q; q++) asm volatile("" : "+v"(w[g][q]));
     };
-    auto load = [&](uint32_t(&c)[G * Q], int a) {
-      lds_load_group<Q, G>(c, a * (G * kRowB) + lofs);
-      lofs += 4;
+    auto load = [&](auto k, uint32_t(&c)[G * Q], int a) {
+      lds_load_group<4 * decltype(k)::v, Q, G>(c, a * (G * kRowB), uni(lofs));
       pin();
     };
+    auto step = [&](int n) { lofs += 4 * n; };
     auto row = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int kind) -> bool {
 #pragma unroll
       for (int g = 0; g < G; g++)
@@ -700,7 +720,7 @@ __global__ void __launch_bounds__(1024) msv_group_kernel(MsvGroup<G> A) {
       if (all_ovf) break;
       int stop = 0;
       const int limit = (r / kHalf + 1) * kHalf;   // end of the current phase
-      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, row)) break;
+      if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, step, row)) break;
 #pragma unroll
       for (int g = 0; g < G; g++) {   // settle every profile whose trigger fired on the stop row
         if (!fired(g)) continue;
