@@ -651,10 +651,12 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   db->max_len = max_len;
   memcpy(db->chunk_at, chunk_at, sizeof chunk_at);
   // Pipelining pays once a chunk's MSV outlasts the tail it hides.  Two
-  // chunks measured best on a 348M-residue database: each MSV kernel fills
-  // every CU's LDS, so a chunk's Viterbi runs mostly after the next MSV and
-  // more chunks only add MSV launches.
-  db->chunks = n_res >= ((int64_t)8 << 20) ? 2 : 1;
+  // chunks measured best on a 348M-residue database (M = 734): each MSV
+  // kernel fills every CU's LDS, so a chunk's Viterbi runs mostly after the
+  // next MSV and more chunks only add MSV launches.  On a 707M-residue one
+  // (M = 2500) four chunks beat two by 2.5 %: its long targets' rescore and
+  // Forward run with one workgroup per target and leave room beside MSV.
+  db->chunks = n_res >= ((int64_t)512 << 20) ? 4 : n_res >= ((int64_t)8 << 20) ? 2 : 1;
   db->data = new (std::nothrow) hmm_db_data();
   if (!db->data) {
     delete db;
