@@ -6,22 +6,29 @@
 // state) needs most of the register file for one wave, so a SIMD runs one
 // wave and nothing hides its memory and cross-lane latencies.  Here wave w
 // of the workgroup holds vectors q in [w*QW, (w+1)*QW) of every lane (cell
-// = lane*Q + q, Q = W*QW), so each wave carries a quarter of the state and
-// several workgroups share a CU.  Per row, through a few hundred bytes of
-// LDS and three barriers, the waves exchange:
-//   - the previous row's M, I, D of each wave's last cell (the left
-//     neighbour of the next wave's first cell; wave 0 takes wave W-1's of
-//     the previous lane);
-//   - the current row's M of each wave's last cell (input of the next
-//     wave's first delete cell);
-//   - each wave's delete-chain map over its cells with zero entry value:
-//     the lane's map is their composition, the lanes are then chained by a
-//     DPP prefix scan (affine maps x -> a + P x for Forward, max-plus maps
-//     x -> max(a, x + b) for the rescore), and each wave applies the value
-//     entering its first cell;
-//   - each wave's part of E (Forward: a sum) or of the running maximum
-//     (rescore: only when it crossed the line that could change xJ).
-// All waves then hold the same special states and take the same decisions.
+// = lane*Q + q, Q = W*QW): the cells of a lane form W consecutive segments,
+// one per wave, and several workgroups share a CU.
+//
+// One barrier per row.  Before it, each wave computes its segment's match
+// and insert cells, its delete chain A with nothing entering the segment's
+// first cell, and publishes for its lane, into the row's half of a
+// double-buffered LDS area (row parity: no wave can run two rows ahead of
+// another, as every row ends at the barrier):
+//   xo: what the segment passes to the next segment's first delete cell
+//       when nothing enters its own first cell (last cell's M through M->D
+//       and A through D->D into that cell);
+//   ml, il, al: its last cell's M, I and A;
+//   Forward: es, the sum of its M + A (its part of E);
+//   rescore: its running maximum if it crossed the trigger line.
+// After the barrier every wave composes its lane's W segment maps
+// (x_out = xo + p x_in: affine for Forward, max-plus for the rescore), chains
+// the lanes with a DPP prefix scan, and so knows the value x_j entering every
+// segment j of its lane.  Its own delete cells are then D_q = A_q (+) P_q
+// x_w; Forward's E is the wave sum of sum_j (es_j + S_j x_j); the left
+// neighbour of its first cell for the next row (segment w-1 of the lane, or
+// segment W-1 of the previous lane through a DPP shift) is (ml, il,
+// al (+) P_last x).  All waves hold the same special states and take the
+// same decisions.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -106,14 +113,12 @@ __device__ __forceinline__ int next_target(int32_t *work, int *slot) {
 template <int QW, int W>
 __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db, DevOut out) {
   constexpr int Q = QW * W;
-  __shared__ float bM[W][kWave], bI[W][kWave], bD[W][kWave];   // previous row, last cell of each wave
-  __shared__ float cM[W][kWave];                                // current row M, last cell of each wave
-  __shared__ float mA[W][kWave];                                // delete chain with zero entry, last cell
-  __shared__ float eS[W];                                       // parts of E
+  __shared__ float sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave], ses[2][W][kWave];
   __shared__ int slot;
   const int lane = threadIdx.x & 63;
   const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int q0 = w * QW;
+  const int nb = w > 0 ? w - 1 : W - 1;   // segment of the first cell's left neighbour
   const float *trg = P.f_tr + lane;
   // transition planes of this wave's cells, registers
   float tr[TR_N][QW];
@@ -121,26 +126,39 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
   for (int k = 0; k < TR_N; k++)
 #pragma unroll
     for (int q = 0; q < QW; q++) tr[k][q] = trg[(k * Q + q0 + q) * kWave];
-  // delete chain products: inside this wave up to q, over each wave's cells
-  // of this lane, over the whole lane, and the lane scan's steps
-  float pre[QW], pw[W], ps[6];
+  // transition of `plane` into the first cell after segment j (this lane's
+  // segment j + 1, or the next lane's first cell; probability 0 at the end)
+  auto into_next = [&](int plane, int j) -> float {
+    if (j + 1 < W) return trg[(plane * Q + (j + 1) * QW) * kWave];
+    return lane + 1 < kWave ? trg[plane * Q * kWave + 1] : 0.0f;
+  };
+  // pre[q]: product of DD over this wave's cells 1..q; per segment j of the
+  // lane: pl[j] the product over its cells 1..QW-1, pj[j] = pl[j] DD' (its
+  // map's slope), sj[j] the sum of its pre[q]; the lane map slope's scan steps
+  float pre[QW], pl[W], pj[W], sj[W], ps[6];
   {
     float acc = 1.0f;
 #pragma unroll
     for (int q = 0; q < QW; q++) {
-      acc *= tr[TR_DDIN][q];
+      if (q) acc *= tr[TR_DDIN][q];
       pre[q] = acc;
     }
-    float pl = 1.0f;
+    float lanep = 1.0f;
 #pragma unroll
     for (int j = 0; j < W; j++) {
-      float pj = 1.0f;
-      for (int q = 0; q < QW; q++) pj *= trg[(TR_DDIN * Q + j * QW + q) * kWave];
-      pw[j] = pj;
-      pl *= pj;
+      float a = 1.0f, sum = 0.0f;
+      for (int q = 0; q < QW; q++) {
+        if (q) a *= trg[(TR_DDIN * Q + j * QW + q) * kWave];
+        sum += a;
+      }
+      pl[j] = a;
+      pj[j] = a * into_next(TR_DDIN, j);
+      sj[j] = sum;
+      lanep *= pj[j];
     }
-    affine_steps(pl, ps);
+    affine_steps(lanep, ps);
   }
+  const float mdn = into_next(TR_MDIN, w), ddn = into_next(TR_DDIN, w);
   const float entry_p = P.entry_p;
   const float *emit = P.f_emit + lane;
   const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
@@ -154,10 +172,9 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
     float M[QW], I[QW], D[QW];
 #pragma unroll
     for (int q = 0; q < QW; q++) M[q] = I[q] = D[q] = 0.0f;
-    bM[w][lane] = bI[w][lane] = bD[w][lane] = 0.0f;
-    __syncthreads();
+    float pM = 0.0f, pI = 0.0f, pD = 0.0f;   // previous row, left neighbour of the first cell
     float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
-    int shift = 0;
+    int shift = 0, par = 0;
     auto load = [&](float(&e)[2 * QW], int a) {
       const float *er = emit + a * (2 * Q * kWave);
 #pragma unroll
@@ -167,11 +184,6 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       }
     };
     auto row = [&](const float(&em)[2 * QW]) -> bool {
-      // left neighbours (previous row) of this wave's first cell
-      const int wl = w > 0 ? w - 1 : W - 1;
-      const int ll = w > 0 ? lane : lane - 1;
-      const float pM = ll >= 0 ? bM[wl][max(ll, 0)] : 0.0f, pI = ll >= 0 ? bI[wl][max(ll, 0)] : 0.0f,
-                  pD = ll >= 0 ? bD[wl][max(ll, 0)] : 0.0f;
       const float bent = B * entry_p;
 #pragma unroll
       for (int q = QW - 1; q >= 0; q--) {
@@ -181,38 +193,46 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
         M[q] = em[q] * sm;
         I[q] = em[QW + q] * si;
       }
-      cM[w][lane] = M[QW - 1];
-      __syncthreads();   // B1: current-row boundary M
-      const float cin = ll >= 0 ? cM[wl][max(ll, 0)] : 0.0f;
-      float dc = 0.0f;
+      // delete chain with nothing entering the segment (A), and its sums
+      float es = M[0];
+      D[0] = 0.0f;
 #pragma unroll
-      for (int q = 0; q < QW; q++) {
-        D[q] = fmaf(q ? M[q - 1] : cin, tr[TR_MDIN][q], dc * tr[TR_DDIN][q]);
-        dc = D[q];
+      for (int q = 1; q < QW; q++) {
+        D[q] = fmaf(M[q - 1], tr[TR_MDIN][q], D[q - 1] * tr[TR_DDIN][q]);
+        es += M[q] + D[q];
       }
-      mA[w][lane] = D[QW - 1];
-      __syncthreads();   // B2: delete-chain maps
-      float a = 0.0f, cw = 0.0f;
+      sxo[par][w][lane] = fmaf(M[QW - 1], mdn, D[QW - 1] * ddn);
+      sml[par][w][lane] = M[QW - 1];
+      sil[par][w][lane] = I[QW - 1];
+      sal[par][w][lane] = D[QW - 1];
+      ses[par][w][lane] = es;
+      __syncthreads();
+      // the values entering the lane's segments
+      float a = 0.0f;
 #pragma unroll
-      for (int j = 0; j < W; j++) a = fmaf(pw[j], a, mA[j][lane]);
-      const float lane_in = lane_up_f(affine_scan(a, ps));
-      cw = lane_in;
-      for (int j = 0; j < w; j++) cw = fmaf(pw[j], cw, mA[j][lane]);
-      float part = 0.0f;
+      for (int j = 0; j < W; j++) a = fmaf(pj[j], a, sxo[par][j][lane]);
+      float x = lane_up_f(affine_scan(a, ps));
+      float xw = 0.0f, xn = 0.0f, e = 0.0f;
 #pragma unroll
-      for (int q = 0; q < QW; q++) {
-        D[q] = fmaf(cw, pre[q], D[q]);
-        part += M[q] + D[q];
+      for (int j = 0; j < W; j++) {
+        if (j == w) xw = x;
+        if (j == nb) xn = x;
+        e += fmaf(sj[j], x, ses[par][j][lane]);
+        x = fmaf(pj[j], x, sxo[par][j][lane]);
       }
-      const float ws = wave_sum_f(part);
-      if (lane == 0) eS[w] = ws;
-      bM[w][lane] = M[QW - 1];
-      bI[w][lane] = I[QW - 1];
-      bD[w][lane] = D[QW - 1];
-      __syncthreads();   // B3: E parts and the next row's boundaries
-      float E = 0.0f;
 #pragma unroll
-      for (int j = 0; j < W; j++) E += eS[j];
+      for (int q = 0; q < QW; q++) D[q] = fmaf(pre[q], xw, D[q]);
+      // the first cell's left neighbour for the next row
+      pM = sml[par][nb][lane];
+      pI = sil[par][nb][lane];
+      pD = fmaf(pl[nb], xn, sal[par][nb][lane]);
+      if (w == 0) {
+        pM = lane_up_f(pM);
+        pI = lane_up_f(pI);
+        pD = lane_up_f(pD);
+      }
+      par ^= 1;
+      const float E = wave_sum_f(e);
       J = fmaf(J, loop, 0.5f * E);
       C = fmaf(C, loop, 0.5f * E);
       N = N * loop;
@@ -222,24 +242,21 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
         int ex;
         (void)frexpf(big, &ex);
         ex = uni(ex);
-        const float s = ldexpf(1.0f, -ex);
+        const float sc = ldexpf(1.0f, -ex);
 #pragma unroll
         for (int q = 0; q < QW; q++) {
-          M[q] *= s;
-          I[q] *= s;
-          D[q] *= s;
+          M[q] *= sc;
+          I[q] *= sc;
+          D[q] *= sc;
         }
-        J *= s;
-        C *= s;
-        N *= s;
-        B *= s;
+        pM *= sc;
+        pI *= sc;
+        pD *= sc;
+        J *= sc;
+        C *= sc;
+        N *= sc;
+        B *= sc;
         shift += ex;
-        // the stored boundaries are read after the next B3 only for the
-        // row after next; the next row reads them scaled:
-        bM[w][lane] = M[QW - 1];
-        bI[w][lane] = I[QW - 1];
-        bD[w][lane] = D[QW - 1];
-        __syncthreads();   // every wave takes the same branch
       }
       return false;
     };
@@ -259,43 +276,55 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
 }
 
 // ============================================================================ int32 rescore
+// Lane l receives lane l-1's value; lane 0 receives `fill`.
+__device__ __forceinline__ int lane_up_fill(int v, int fill) {
+  return __builtin_amdgcn_update_dpp(fill, v, 0x138 /* wave_shr:1 */, 0xf, 0xf, false);
+}
+
 template <int QW, int W>
 __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb db, DevOut out) {
   constexpr int Q = QW * W;
-  __shared__ int bM[W][kWave], bI[W][kWave], bD[W][kWave];
-  __shared__ int cM[W][kWave];
-  __shared__ int mA[W][kWave];
-  __shared__ int xS[W];        // per wave: its maximum when it crossed the trigger line, else kNeg32
+  __shared__ int sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave];
+  __shared__ int sxs[2][W];    // per wave: its maximum when it crossed the trigger line, else kNeg32
+  __shared__ int fin[W];
   __shared__ int slot;
   const int lane = threadIdx.x & 63;
   const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int q0 = w * QW;
+  const int nb = w > 0 ? w - 1 : W - 1;
   const int *trg = P.v32_tr + lane;
   int tr[TR_N][QW];
 #pragma unroll
   for (int k = 0; k < TR_N; k++)
 #pragma unroll
     for (int q = 0; q < QW; q++) tr[k][q] = trg[(k * Q + q0 + q) * kWave];
-  // delete chain sums (max-plus b parts): inside this wave up to q, over each
-  // wave's cells of this lane, over the lane, and the lane scan's steps
-  int pre[QW], bw[W], bs[6];
+  auto into_next = [&](int plane, int j) -> int {
+    if (j + 1 < W) return trg[(plane * Q + (j + 1) * QW) * kWave];
+    return lane + 1 < kWave ? trg[plane * Q * kWave + 1] : kNeg32;
+  };
+  // max-plus counterparts of the Forward kernel's products: sums of DD
+  // (minus infinity absorbing) over cells 1..q of this wave, over cells
+  // 1..QW-1 of each segment (pl), plus DD' (pj); the lane map's scan steps
+  int pre[QW], pl[W], pj[W], bs[6];
   {
     int acc = 0;
 #pragma unroll
     for (int q = 0; q < QW; q++) {
-      acc = ninf_add(acc, tr[TR_DDIN][q]);
+      if (q) acc = ninf_add(acc, tr[TR_DDIN][q]);
       pre[q] = acc;
     }
-    int bl = 0;
+    int lanep = 0;
 #pragma unroll
     for (int j = 0; j < W; j++) {
-      int bj = 0;
-      for (int q = 0; q < QW; q++) bj = ninf_add(bj, trg[(TR_DDIN * Q + j * QW + q) * kWave]);
-      bw[j] = bj;
-      bl = ninf_add(bl, bj);
+      int a = 0;
+      for (int q = 1; q < QW; q++) a = ninf_add(a, trg[(TR_DDIN * Q + j * QW + q) * kWave]);
+      pl[j] = a;
+      pj[j] = ninf_add(a, into_next(TR_DDIN, j));
+      lanep = ninf_add(lanep, pj[j]);
     }
-    maxplus_steps_i(bl, bs);
+    maxplus_steps_i(lanep, bs);
   }
+  const int mdn = into_next(TR_MDIN, w), ddn = into_next(TR_DDIN, w);
   const int *emit = P.v32_emit + lane;
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
@@ -308,11 +337,11 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
     int M[QW], I[QW], D[QW];
 #pragma unroll
     for (int q = 0; q < QW; q++) M[q] = I[q] = D[q] = kNeg32;
-    bM[w][lane] = bI[w][lane] = bD[w][lane] = kNeg32;
-    __syncthreads();
+    int pM = kNeg32, pI = kNeg32, pD = kNeg32;
     int accM = kNeg32, xJt = kNeg32;
     int xbe = fl32(fl32(mv) + entry);
     int T = -ej + 1;
+    int par = 0;
     auto load = [&](int(&e)[2 * QW], int a) {
       const int *er = emit + a * (2 * Q * kWave);
 #pragma unroll
@@ -322,14 +351,9 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
       }
     };
     auto row = [&](const int(&em)[2 * QW]) -> bool {
-      const int wl = w > 0 ? w - 1 : W - 1;
-      const int ll = w > 0 ? lane : lane - 1;
-      // the value shifted into cell 0 is irrelevant: every transition into
-      // it is kNeg32
-      const int pM = ll >= 0 ? bM[wl][max(ll, 0)] : 0, pI = ll >= 0 ? bI[wl][max(ll, 0)] : 0,
-                pD = ll >= 0 ? bD[wl][max(ll, 0)] : 0;
       // every state and table value is >= -2^30, so each add fits in int32
-      // and the floors inside a maximum merge into one
+      // and the floors inside a maximum merge into one; the value shifted
+      // into cell 0 is irrelevant, as every transition into it is kNeg32
 #pragma unroll
       for (int q = QW - 1; q >= 0; q--) {
         const int pm = q ? M[q - 1] : pM, pi = q ? I[q - 1] : pI, pd = q ? D[q - 1] : pD;
@@ -340,39 +364,44 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
         M[q] = mn;
         I[q] = in;
       }
-      cM[w][lane] = M[QW - 1];
-      __syncthreads();   // B1
-      const int cin = ll >= 0 ? cM[wl][max(ll, 0)] : kNeg32;
-      // delete chain inside the wave with minus infinity entering it
-      int dc = kNeg32;
+      // delete chain with nothing (minus infinity) entering the segment
+      D[0] = kNeg32;
 #pragma unroll
-      for (int q = 0; q < QW; q++) {
-        D[q] = max(fl32((q ? M[q - 1] : cin) + tr[TR_MDIN][q]), ninf_add(dc, tr[TR_DDIN][q]));
-        dc = D[q];
-      }
-      mA[w][lane] = D[QW - 1];
-      __syncthreads();   // B2
-      int a = kNeg32;
-#pragma unroll
-      for (int j = 0; j < W; j++) a = max(mA[j][lane], ninf_add(a, bw[j]));
-      // lane l-1's value (lane 0 receives 0, which is harmless: the first
-      // cell's DDIN is minus infinity and every fold below starts with it)
-      int cw = lane_up_i(maxplus_scan_i(a, bs));
-      for (int j = 0; j < w; j++) cw = max(mA[j][lane], ninf_add(cw, bw[j]));
-#pragma unroll
-      for (int q = 0; q < QW; q++) D[q] = max(D[q], ninf_add(cw, pre[q]));
+      for (int q = 1; q < QW; q++) D[q] = max(fl32(M[q - 1] + tr[TR_MDIN][q]), ninf_add(D[q - 1], tr[TR_DDIN][q]));
+      sxo[par][w][lane] = max(fl32(M[QW - 1] + mdn), ninf_add(D[QW - 1], ddn));
+      sml[par][w][lane] = M[QW - 1];
+      sil[par][w][lane] = I[QW - 1];
+      sal[par][w][lane] = D[QW - 1];
       // some cell reached the line that could raise xJ: its wave's maximum
       const bool trig = __builtin_amdgcn_ballot_w64(accM >= T) != 0;
-      int wm = kNeg32;
-      if (trig) wm = wave_max_i32(accM);
-      if (lane == 0) xS[w] = wm;
-      bM[w][lane] = M[QW - 1];
-      bI[w][lane] = I[QW - 1];
-      bD[w][lane] = D[QW - 1];
-      __syncthreads();   // B3
+      const int wm = trig ? wave_max_i32(accM) : kNeg32;
+      if (lane == 0) sxs[par][w] = wm;
+      __syncthreads();
+      int a = kNeg32;
+#pragma unroll
+      for (int j = 0; j < W; j++) a = max(sxo[par][j][lane], ninf_add(a, pj[j]));
+      int x = lane_up_fill(maxplus_scan_i(a, bs), kNeg32);
+      int xw = kNeg32, xn = kNeg32;
+#pragma unroll
+      for (int j = 0; j < W; j++) {
+        if (j == w) xw = x;
+        if (j == nb) xn = x;
+        x = max(sxo[par][j][lane], ninf_add(x, pj[j]));
+      }
+#pragma unroll
+      for (int q = 0; q < QW; q++) D[q] = max(D[q], ninf_add(xw, pre[q]));
+      pM = sml[par][nb][lane];
+      pI = sil[par][nb][lane];
+      pD = max(sal[par][nb][lane], ninf_add(xn, pl[nb]));
+      if (w == 0) {
+        pM = lane_up_fill(pM, kNeg32);
+        pI = lane_up_fill(pI, kNeg32);
+        pD = lane_up_fill(pD, kNeg32);
+      }
       int m = kNeg32;
 #pragma unroll
-      for (int j = 0; j < W; j++) m = max(m, xS[j]);
+      for (int j = 0; j < W; j++) m = max(m, sxs[par][j]);
+      par ^= 1;
       if (m > kNeg32) {
         xJt = max(xJt, fl32(m + ej));
         const int xB = max(fl32(mv), fl32(xJt + mv));
@@ -384,16 +413,14 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
     int ea[2 * QW], eb[2 * QW];
     int stop;
     (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
-    // the final maximum over every cell of every row, all waves (the
-    // barrier first: the last row's maxima are still being read)
+    // the final maximum over every cell of every row, all waves
     {
       const int v = wave_max_i32(accM);
-      __syncthreads();
-      if (lane == 0) xS[w] = v;
+      if (lane == 0) fin[w] = v;
       __syncthreads();
       int m = kNeg32;
 #pragma unroll
-      for (int j = 0; j < W; j++) m = max(m, xS[j]);
+      for (int j = 0; j < W; j++) m = max(m, fin[j]);
       if (w == 0) out.vit[uni(db.perm[t])] = fl32(fl32(m + ej) + mv);
     }
   }
