@@ -274,6 +274,11 @@ def main():
     achieved = MSV_OPS_PER_CELL * cells / (msv_ms / 1e3) / 1e12 if msv_ms > 0 else 0.0
     log(f"{ms_step:.3f} ms/step, {gcups:.1f} GCUPS; stages ms: MSV {st_ms[0]:.3f} Viterbi {st_ms[1]:.3f} "
         f"rescore {st_ms[2]:.3f} (concurrent with) Forward {st_ms[3]:.3f}; counts {counts}")
+    # the packed 16-bit VALU rate this device sustains (a timed kernel of
+    # independent chains of the MSV recurrence's instructions)
+    probe_ops, _ = hg.hmm_probe_pk16(stream)
+    probe_tops = probe_ops / 1e12
+    log(f"packed 16-bit VALU probe: {probe_tops:.2f} Tops/s sustained (datasheet peak {PEAK_PK16_TOPS:.2f})")
     traffic = None
     if os.path.exists(args.traffic) and not batched and not args.cutoffs:
         with open(args.traffic) as f:
@@ -326,6 +331,7 @@ def main():
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
                      "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic,
                      "traffic_note": "HBM bytes of the MSV stage per search (all its launches), rocprofv3 counters",
+                     "peak_measured": round(probe_tops, 3), "frac_of_measured": round(achieved / probe_tops, 4),
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
                      "msv_launches_per_search": chunks}
         if timed_stages else None,

@@ -323,6 +323,17 @@ int hmm_db_stage_timing(hmm_db *db, int32_t capacity);
  * clears the record.  Errors: HMM_EINVAL, HMM_EDEVICE. */
 int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n);
 
+/* Measurement hook: the packed 16-bit VALU rate this device sustains, in
+ * element-ops per second (one wave64 packed instruction = 128), from a timed
+ * kernel of independent chains of the MSV recurrence's two instructions
+ * (packed fp16 add and maximum) at 32 waves per CU: the practical ceiling of
+ * the integer filters, beside the datasheet peak 256 CU x 64 lanes x 2 x
+ * 2.4 GHz = 78.64e12.  Allocates and frees a work buffer of 4 bytes per
+ * thread of the launch (2 MB on 256 CUs); synchronises `stream`.  *ms
+ * (if non-NULL) receives the timed launch's duration.
+ * Errors: HMM_EINVAL (NULL ops_per_s), HMM_ENOMEM, HMM_EDEVICE. */
+int hmm_probe_pk16(hmm_stream stream, double *ops_per_s, float *ms);
+
 /* Tuning hook: the number of chunks (1..8) a search on this handle is
  * pipelined in.  The length-sorted targets are split into that many
  * contiguous ranges of about equal residue counts; the MSV kernels of the

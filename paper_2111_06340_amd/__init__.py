@@ -29,7 +29,7 @@ HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
             "hmm_count", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables",
             "hmm_decode", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
-            "hmm_profile_upload", "hmm_search", "hmm_search_group", "hmm_strerror")
+            "hmm_probe_pk16", "hmm_profile_upload", "hmm_search", "hmm_search_group", "hmm_strerror")
 
 
 class HmmError(RuntimeError):
@@ -86,6 +86,8 @@ def lib():
         L.hmm_db_share.argtypes = [vp, C.POINTER(vp)]
         L.hmm_search.restype = C.c_int
         L.hmm_search.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), vp]
+        L.hmm_probe_pk16.restype = C.c_int
+        L.hmm_probe_pk16.argtypes = [vp, C.POINTER(C.c_double), C.POINTER(C.c_float)]
         L.hmm_search_group.restype = C.c_int
         L.hmm_search_group.argtypes = [vp, vp, C.POINTER(hmm_thresholds), C.POINTER(hmm_results), i32, vp]
         L.hmm_count.restype = C.c_int
@@ -211,6 +213,15 @@ def hmm_search(profile: int, db: int, F, out: dict, stream=None, bias_filter: bo
                     out["bias"].data_ptr() if out.get("bias") is not None else None)
     _check(lib().hmm_search(C.c_void_p(profile), C.c_void_p(db), C.byref(t), C.byref(r), _stream_handle(stream)),
            "hmm_search")
+
+
+def hmm_probe_pk16(stream=None) -> tuple[float, float]:
+    """The packed 16-bit VALU rate the device sustains (element-ops/s) and
+    the timed launch's milliseconds."""
+    ops = C.c_double(0.0)
+    ms = C.c_float(0.0)
+    _check(lib().hmm_probe_pk16(_stream_handle(stream), C.byref(ops), C.byref(ms)), "hmm_probe_pk16")
+    return ops.value, ms.value
 
 
 def _results(out: dict) -> hmm_results:

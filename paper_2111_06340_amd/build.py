@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhmmgpu.so")
-SOURCES = ["hmm_host.cpp", "hmm_kernels.hip", "hmm_decode.hip", "hmm_coop.hip"]
+SOURCES = ["hmm_host.cpp", "hmm_kernels.hip", "hmm_decode.hip", "hmm_coop.hip", "hmm_probe.hip"]
 ARCH = os.environ.get("HMM_OFFLOAD_ARCH", "gfx950")
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -816,6 +816,23 @@ int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n) {
   return HMM_OK;
 }
 
+int hmm_probe_pk16(hmm_stream stream, double *ops_per_s, float *ms) {
+  if (!ops_per_s) return fail(HMM_EINVAL, "NULL ops_per_s");
+  int dev = 0, ncu = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  HIP_TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
+  const int64_t words = (int64_t)2 * (ncu > 0 ? ncu : 256) * 1024;
+  void *buf = nullptr;
+  hipError_t e = hipMalloc(&buf, (size_t)words * 4);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "probe buffer") : fail_hip(e, "hipMalloc(probe buffer)");
+  e = probe_pk16((uint32_t *)buf, words, (hipStream_t)stream, ops_per_s, ms);
+  const hipError_t f = hipFree(buf);
+  if (e != hipSuccess) return fail_hip(e, "packed 16-bit probe");
+  if (f != hipSuccess) return fail_hip(f, "hipFree(probe buffer)");
+  return HMM_OK;
+}
+
 int hmm_db_free(hmm_db *db) {
   if (!db) return HMM_OK;
   hipError_t e = hipSuccess;

@@ -192,6 +192,12 @@ hipError_t launch_search_group(const DevProfile *P, const DevDb *db, const DevOu
 hipError_t launch_count(const DevProfile &p, const DevDb &db, const hmm_domain *dom, const int32_t *n_dom,
                         int32_t max_dom, const int16_t *aln, uint32_t *counts, hipStream_t stream);
 
+// The packed 16-bit VALU rate the device sustains (element-ops per second),
+// measured by a timed kernel of independent add/maximum chains; scratch
+// holds one word per thread of the launch (2 x CUs x 1024).
+hipError_t probe_pk16(uint32_t *scratch, int64_t scratch_words, hipStream_t stream, double *ops_per_s,
+                      float *ms);
+
 // Number of packed vectors per lane.
 inline int q8_of(int M) { return (M + 2 * kWave - 1) / (2 * kWave); }
 inline int q32_of(int M) { return (M + kWave - 1) / kWave; }

@@ -659,3 +659,13 @@ def test_search_group_rejects_bad_groups():
     torch.cuda.synchronize()
     for h in (S, D, E, P):
         h.close()
+
+
+def test_packed16_probe_rate_is_plausible():
+    """hmm_probe_pk16: the sustained packed 16-bit rate lies between a third
+    of the datasheet peak and the peak at a 10 % higher clock."""
+    import torch
+    ops, ms = hg.hmm_probe_pk16(torch.cuda.current_stream())
+    announce(f"packed 16-bit probe: {ops / 1e12:.2f} Tops/s in {ms:.3f} ms")
+    assert ms > 0
+    assert 26e12 < ops < 86.5e12
