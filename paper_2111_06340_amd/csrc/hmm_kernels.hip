@@ -578,8 +578,12 @@ __device__ __forceinline__ void lds_load_group(uint32_t (&c)[G * Q], int base, i
       asm volatile("ds_read_addtid_b32 %0 offset:%1" : "=v"(c[g * Q + q]) : "i"((g * 2 * Q + q) * kWave * 4 + K));
 }
 
+// Eight waves per SIMD (two blocks per CU), as the single-profile kernel:
+// the G profiles' scalar state would otherwise take more than the 100 SGPRs
+// that allows, and leave one block per CU.
 template <int Q, int G>
-__global__ void __launch_bounds__(1024) msv_group_kernel(MsvGroup<G> A) {
+__global__ void __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8, 8)))
+msv_group_kernel(MsvGroup<G> A) {
   constexpr int kHalf = Q * kWave;       // P/2
   constexpr int kRowB = 2 * kHalf * 4;   // bytes per residue and profile
   extern __shared__ uint32_t lds[];
@@ -1402,7 +1406,8 @@ hipError_t dispatch_msv(const DevProfile &P, const DevDb &db, const DevOut &o, h
 
 // Largest group of profiles the group MSV kernel takes at Q vectors per lane
 // (diagonal layout): as many tables as two 1024-thread blocks per CU can hold
-// in LDS (about 60 KB each), at most 4; 1 = no group instance.
+// in LDS (about 60 KB each) within the 64 registers per lane of eight waves
+// per SIMD, at most 4; 1 = no group instance.
 int msv_group_max(int Q) { return Q == 1 ? 4 : Q == 2 ? 3 : Q == 3 ? 2 : 1; }
 
 hipError_t dispatch_msv_group(const DevProfile *P, const DevDb *db, const DevOut *o, int G, hipStream_t s) {
