@@ -46,7 +46,8 @@ extern "C" {
 
 #define HMM_OK 0
 #define HMM_EINVAL (-1)   /* bad argument: NULL pointer, M < 1, bad probabilities, bad residue code, empty sequence, offsets not increasing */
-#define HMM_ERANGE (-2)   /* size beyond a library limit (M > HMM_MAX_M, sequence longer than HMM_MAX_LEN) */
+#define HMM_ERANGE (-2)   /* size beyond a library limit (M > HMM_MAX_M, sequence longer than HMM_MAX_LEN,
+                             scores beyond the int32 rescore's exact range) */
 #define HMM_ENOMEM (-3)   /* host or device allocation failed */
 #define HMM_EDEVICE (-4)  /* a HIP runtime call failed; the message carries the HIP error string */
 
@@ -178,7 +179,12 @@ int hmm_db_share(const hmm_db *db, hmm_db **out);
  * cutoffs or the profile between searches on a database rebuilds a small
  * per-length table, which waits for the database's previous search on the
  * host.  Errors: HMM_EINVAL (NULL profile/db/thresholds/out or NULL output
- * buffer with n_seqs > 0), HMM_EDEVICE. */
+ * buffer with n_seqs > 0), HMM_ERANGE (the database's longest sequence
+ * times the profile's largest emission score, in the Viterbi filter's
+ * 1/500-bit units, reaches 2^29: beyond that bound the int32 rescore is not
+ * guaranteed exact; with a background whose rarest residue has frequency
+ * 1.3 %, no emission scores above about 3,100 units, against the 5,368
+ * allowed at HMM_MAX_LEN), HMM_EDEVICE. */
 int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t,
                const hmm_results *out, hmm_stream stream);
 
@@ -200,7 +206,8 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t,
  * profile or cutoffs change); allocates nothing.
  * Errors: HMM_EINVAL (n < 1; NULL array or element; a handle twice; handles
  * of different databases; bad cutoffs or NULL output buffers as in
- * hmm_search), HMM_EDEVICE; on an error nothing is enqueued. */
+ * hmm_search), HMM_ERANGE (as in hmm_search), HMM_EDEVICE; on an error
+ * nothing is enqueued. */
 int hmm_search_group(const hmm_profile *const *p, hmm_db *const *db, const hmm_thresholds *t,
                      const hmm_results *out, int32_t n, hmm_stream stream);
 

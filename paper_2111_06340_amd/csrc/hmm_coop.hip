@@ -65,24 +65,29 @@ __device__ __forceinline__ void affine_steps(float p, float (&ps)[6]) {
   ps[5] = p;
 }
 
-// int32 max-plus maps x -> max(a, x + b) of the rescore's delete chain.  A
-// value or a b at or below kNeg32 is minus infinity (a structural entry:
-// no delete transition into cell 0 or into padding cells), and sums
-// involving it stay there; every other b is a sum of at most 3071
-// transition scores >= -32768, so no sum leaves int32.
+// int32 max-plus maps x -> max(a, x + b) of the rescore's delete chain.
+// Their slopes b (profile constants, composed once per kernel) treat a b at
+// or below kNeg32 as minus infinity (a structural entry: no delete
+// transition into cell 0 or into padding cells), and sums involving it stay
+// at kNeg32; every other b is a sum of at most 3071 transition scores
+// >= -32768, so no sum leaves int32 and every composed b is >= -2^30.
 __device__ __forceinline__ int ninf_add(int x, int b) { return (x <= kNeg32 || b <= kNeg32) ? kNeg32 : x + b; }
 
 template <int CTRL, int ROWMASK>
 __device__ __forceinline__ int dpp_i(int v, int fill) {
   return __builtin_amdgcn_update_dpp(fill, v, CTRL, ROWMASK, 0xf, false);
 }
+// The per-row scan: every map value is at or above the delete floor tau >=
+// -2^30 and every composed b at or above -2^30 (see the rescore kernel), so
+// plain adds cannot leave int32 and a sum with a minus-infinity b stays
+// below the floor, where the maximum with the lane's own value drops it.
 __device__ __forceinline__ int maxplus_scan_i(int a, const int (&bs)[6]) {
-  a = max(a, ninf_add(dpp_i<kRowShr1, 0xf>(a, kNeg32), bs[0]));
-  a = max(a, ninf_add(dpp_i<kRowShr2, 0xf>(a, kNeg32), bs[1]));
-  a = max(a, ninf_add(dpp_i<kRowShr4, 0xf>(a, kNeg32), bs[2]));
-  a = max(a, ninf_add(dpp_i<kRowShr8, 0xf>(a, kNeg32), bs[3]));
-  a = max(a, ninf_add(dpp_i<kRowBcast15, 0xa>(a, kNeg32), bs[4]));
-  a = max(a, ninf_add(dpp_i<kRowBcast31, 0xc>(a, kNeg32), bs[5]));
+  a = max(a, dpp_i<kRowShr1, 0xf>(a, kNeg32) + bs[0]);
+  a = max(a, dpp_i<kRowShr2, 0xf>(a, kNeg32) + bs[1]);
+  a = max(a, dpp_i<kRowShr4, 0xf>(a, kNeg32) + bs[2]);
+  a = max(a, dpp_i<kRowShr8, 0xf>(a, kNeg32) + bs[3]);
+  a = max(a, dpp_i<kRowBcast15, 0xa>(a, kNeg32) + bs[4]);
+  a = max(a, dpp_i<kRowBcast31, 0xc>(a, kNeg32) + bs[5]);
   return a;
 }
 __device__ __forceinline__ void maxplus_steps_i(int b, int (&bs)[6]) {
@@ -276,6 +281,24 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
 }
 
 // ============================================================================ int32 rescore
+//
+// The delete floor of the one-wave kernels: the chain keeps D' = max(D,
+// tau), tau = xBe - max_k DM_k >= -2^30, which changes no match cell (a
+// delete value at or below tau enters a match cell at or below xBe, which
+// every match cell already includes).  With it the segment maps are exact
+// in plain int32 adds:
+//   - inside a segment D'_q = max(M_{q-1} + MD, D'_{q-1} + DD, tau), from
+//     D'_0 = tau with nothing entering; the value x entering the first cell
+//     then gives D'_q = max(A_q, x + pre_q), and the next segment receives
+//     max(xo, x + pj) with xo >= tau;
+//   - every operand of an add is >= -2^30 (states, floors, table entries
+//     and the composed b, which are exact DD sums >= -3072 * 32768 or the
+//     structural -2^30), so no add leaves int32;
+//   - a sum with a structural -2^30 is at most (largest score) - 2^30, below
+//     tau >= -2^17 while every score stays below 2^29 (the host rejects a
+//     search whose longest target times largest emission score could reach
+//     that), and each such sum meets a maximum with a term >= tau, so it
+//     is dropped exactly as minus infinity would be.
 // Lane l receives lane l-1's value; lane 0 receives `fill`.
 __device__ __forceinline__ int lane_up_fill(int v, int fill) {
   return __builtin_amdgcn_update_dpp(fill, v, 0x138 /* wave_shr:1 */, 0xf, 0xf, false);
@@ -340,6 +363,7 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
     int pM = kNeg32, pI = kNeg32, pD = kNeg32;
     int accM = kNeg32, xJt = kNeg32;
     int xbe = fl32(fl32(mv) + entry);
+    int tau = xbe - P.dm_max32;   // delete floor
     int T = -ej + 1;
     int par = 0;
     auto load = [&](int(&e)[2 * QW], int a) {
@@ -364,11 +388,11 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
         M[q] = mn;
         I[q] = in;
       }
-      // delete chain with nothing (minus infinity) entering the segment
-      D[0] = kNeg32;
+      // delete chain with only the floor entering the segment
+      D[0] = tau;
 #pragma unroll
-      for (int q = 1; q < QW; q++) D[q] = max(fl32(M[q - 1] + tr[TR_MDIN][q]), ninf_add(D[q - 1], tr[TR_DDIN][q]));
-      sxo[par][w][lane] = max(fl32(M[QW - 1] + mdn), ninf_add(D[QW - 1], ddn));
+      for (int q = 1; q < QW; q++) D[q] = max(max(M[q - 1] + tr[TR_MDIN][q], D[q - 1] + tr[TR_DDIN][q]), tau);
+      sxo[par][w][lane] = max(max(M[QW - 1] + mdn, D[QW - 1] + ddn), tau);
       sml[par][w][lane] = M[QW - 1];
       sil[par][w][lane] = I[QW - 1];
       sal[par][w][lane] = D[QW - 1];
@@ -377,22 +401,22 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
       const int wm = trig ? wave_max_i32(accM) : kNeg32;
       if (lane == 0) sxs[par][w] = wm;
       __syncthreads();
-      int a = kNeg32;
+      int a = sxo[par][0][lane];
 #pragma unroll
-      for (int j = 0; j < W; j++) a = max(sxo[par][j][lane], ninf_add(a, pj[j]));
-      int x = lane_up_fill(maxplus_scan_i(a, bs), kNeg32);
-      int xw = kNeg32, xn = kNeg32;
+      for (int j = 1; j < W; j++) a = max(sxo[par][j][lane], a + pj[j]);
+      int x = lane_up_fill(maxplus_scan_i(a, bs), tau);
+      int xw = tau, xn = tau;
 #pragma unroll
       for (int j = 0; j < W; j++) {
         if (j == w) xw = x;
         if (j == nb) xn = x;
-        x = max(sxo[par][j][lane], ninf_add(x, pj[j]));
+        x = max(sxo[par][j][lane], x + pj[j]);
       }
 #pragma unroll
-      for (int q = 0; q < QW; q++) D[q] = max(D[q], ninf_add(xw, pre[q]));
+      for (int q = 0; q < QW; q++) D[q] = max(D[q], xw + pre[q]);
       pM = sml[par][nb][lane];
       pI = sil[par][nb][lane];
-      pD = max(sal[par][nb][lane], ninf_add(xn, pl[nb]));
+      pD = max(sal[par][nb][lane], xn + pl[nb]);
       if (w == 0) {
         pM = lane_up_fill(pM, kNeg32);
         pI = lane_up_fill(pI, kNeg32);
@@ -406,6 +430,7 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
         xJt = max(xJt, fl32(m + ej));
         const int xB = max(fl32(mv), fl32(xJt + mv));
         xbe = fl32(xB + entry);
+        tau = xbe - P.dm_max32;
         T = max(xJt, 0) - ej + 1;
       }
       return false;

@@ -95,6 +95,7 @@ struct hmm_profile {
   int bias8 = 0, entry8 = 0, exit8 = 0, entry16 = 0, ej16 = 0;
   std::vector<uint8_t> cost8;
   std::vector<int16_t> msc16, isc16, t16;
+  int s_max = 0;  // largest emission score (int16 units, >= 0)
   DevProfile dev{};
   void *dmem = nullptr;  // one device allocation holding every table
 };
@@ -240,6 +241,9 @@ void quantize(const hmm_profile_desc *d, hmm_profile *p) {
           v > 0.0 ? (int16_t)clampl(q_round(kS16 * std::log(v)), -32768, 32767) : (int16_t)kNeg16;
     }
   }
+  p->s_max = 0;
+  for (int16_t v : p->msc16) p->s_max = std::max(p->s_max, (int)v);
+  for (int16_t v : p->isc16) p->s_max = std::max(p->s_max, (int)v);
   p->entry16 = (int)clampl(q_round(kS16 * entry), -32768, 32767);
   p->ej16 = (int)clampl(q_round(kS16 * std::log(0.5)), -32768, 32767);
 
@@ -869,6 +873,16 @@ int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t 
   return HMM_OK;
 }
 
+// Every transition score is <= 0 and a path emits at most once per residue,
+// so no Viterbi value of a target of length L exceeds L * s_max.  The int32
+// rescore is exact while that stays below 2^29 (its delete floor drops
+// sums with a structural -2^30 only below that).  With a background whose
+// rarest residue has frequency 1.3 %, no emission scores above about 3,100
+// units, against the 5,368 allowed for 100,000 residues.
+static bool int32_range_ok(const hmm_profile *p, const hmm_db *db) {
+  return (int64_t)db->max_len * p->s_max < ((int64_t)1 << 29);
+}
+
 int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const hmm_results *out,
                hmm_stream stream) {
   if (!p || !db || !t || !out) return fail(HMM_EINVAL, "NULL profile, db, thresholds or results");
@@ -878,6 +892,9 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
   if (t->bias_filter != 0 && t->bias_filter != 1) return fail(HMM_EINVAL, "bias_filter = %d; need 0 or 1", t->bias_filter);
   if (db->n > 0 && (!out->msv || !out->vit || !out->fwd || !out->flags))
     return fail(HMM_EINVAL, "NULL output buffer");
+  if (!int32_range_ok(p, db))
+    return fail(HMM_ERANGE, "longest target (%d) times largest emission score (%d) reaches 2^29", db->max_len,
+                p->s_max);
   hipStream_t s = (hipStream_t)stream;
   if (db->n == 0) return HMM_OK;
   // serialise searches on this database (scratch and per-length table)
@@ -923,6 +940,9 @@ int hmm_search_group(const hmm_profile *const *p, hmm_db *const *db, const hmm_t
       return fail(HMM_EINVAL, "search %d: bias_filter = %d; need 0 or 1", i, ti.bias_filter);
     if (db[i]->n > 0 && (!out[i].msv || !out[i].vit || !out[i].fwd || !out[i].flags))
       return fail(HMM_EINVAL, "search %d: NULL output buffer", i);
+    if (!int32_range_ok(p[i], db[i]))
+      return fail(HMM_ERANGE, "search %d: longest target (%d) times largest emission score (%d) reaches 2^29", i,
+                  db[i]->max_len, p[i]->s_max);
   }
   hipStream_t s = (hipStream_t)stream;
   if (db[0]->n == 0) return HMM_OK;

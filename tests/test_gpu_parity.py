@@ -381,6 +381,63 @@ def test_degenerate_and_extreme_profiles():
     assert rng is not None
 
 
+def _rare_residue_profile(M, seed):
+    """Residue 0 has background frequency 1e-9 and match probability 1/2 at
+    every node: each match of it scores about 14,400 units (1/500 bit), so
+    a run of it drives the Viterbi score towards the int32 rescore's bound."""
+    prof = gen.make_profile(M, seed)
+    bg = prof.bg.copy()
+    bg[1:] *= (1.0 - 1e-9) / bg[1:].sum()
+    bg[0] = 1e-9
+    match = prof.match.copy()
+    match[:, 1:] *= 0.5 / match[:, 1:].sum(axis=1, keepdims=True)
+    match[:, 0] = 0.5
+    insert = np.tile(bg, (M - 1, 1))
+    return gen.Profile(M, bg, match, insert, prof.trans)
+
+
+def test_scores_near_the_int32_bound_and_beyond():
+    """hmm_search is exact up to the bound (longest target x largest
+    emission score < 2^29), here with targets whose best score lies within
+    a factor 1.3 of it through the cooperative long-profile kernels, and
+    rejects a database one step past it with HMM_ERANGE before enqueuing
+    anything."""
+    import torch
+    M = 2000
+    prof = _rare_residue_profile(M, 31)
+    tab = hg.hmm_debug_tables(prof)
+    s_max = int(max(tab["msc16"].max(), tab["isc16"].max(), 0))
+    limit = -(-(1 << 29) // s_max)                # shortest length the bound rejects
+    assert 30000 < limit < 40000, (s_max, limit)
+    rng = np.random.default_rng(8)
+    L = limit - 1
+    run = np.zeros(L, np.uint8)                   # residue 0 throughout: about L * s_max
+    mixed = gen.background_residues(rng, L)
+    mixed[rng.random(L) < 0.7] = 0
+    seqs = [run, mixed, gen.background_residues(rng, 500), np.zeros(3, np.uint8)]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([x.size for x in seqs])
+    res = np.concatenate(seqs)
+    g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    st = compare(g, o, what="near the int32 bound")
+    assert g["vit"][0] > (1 << 29) // 2, g["vit"][0]
+    announce(f"int32 bound: s_max={s_max} L={L} vit={g['vit'][0]} ok {st}")
+    # one residue longer: rejected by hmm_search and hmm_search_group
+    P = hg.Profile(prof, 0.0, 0.0, 0.0)
+    D = hg.Database(np.zeros(limit, np.uint8), np.array([0, limit], np.int64))
+    out = hg.alloc_results(D.n)
+    with pytest.raises(hg.HmmError) as e:
+        hg.search(P, D, (1.0, 1.0, 1.0), out)
+    assert e.value.status == hg.HMM_ERANGE
+    with pytest.raises(hg.HmmError) as e:
+        hg.hmm_search_group([P.handle], [D.handle], [(1.0, 1.0, 1.0)], [out])
+    assert e.value.status == hg.HMM_ERANGE
+    torch.cuda.synchronize()
+    D.close()
+    P.close()
+
+
 def test_empty_and_single_target_databases():
     import torch
     prof = gen.make_profile(50, 1)
