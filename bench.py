@@ -16,10 +16,14 @@ every target).
 
 Roofline of the dominant kernel (MSV): plain packed-int16 VALU arithmetic,
 4 element-ops per cell (max, saturating add, saturating subtract, max), so
-achieved = 4 x cells / (average MSV duration), against the MI355X packed
-16-bit VALU peak 256 CU x 64 lanes x 2 elements x 2.4 GHz = 78.64 Tops/s.
-The MSV duration is measured with HIP events that the library records on
-the search stream around the stage.  `stage_roofline` gives the same
+achieved = 4 x cells per launch / (average MSV launch duration), against
+the MI355X packed 16-bit VALU peak 256 CU x 64 lanes x 2 elements x 2.4 GHz
+= 78.64 Tops/s.  The MSV launches of a search (one per pipelined chunk) run
+back to back on the search stream, between HIP events that the library
+records there, so the average launch lasts the stage's time divided by the
+launches.  `traffic` is the HBM bytes per MSV launch that rocprofv3's
+FETCH_SIZE and WRITE_SIZE counters measured for the same kernel source
+(scaled by a plain 1 GiB copy), beside the launch's algorithmic bytes.  `stage_roofline` gives the same
 fraction for every stage (Viterbi 18 ops/cell, rescore 17 int32 ops/cell
 against 39.32 Tops/s, Forward 18 flops/cell against 157.3 TFLOP/s).
 """
@@ -287,7 +291,7 @@ def main():
         # the kernel source and the launches per search are the measured ones
         if (tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha()
                 and tr.get("launches_per_search") == chunks):
-            traffic = tr.get("bytes_per_search")
+            traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"))
     if batched:
         wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
               f"against {D.n} synthetic sequences ({D.n_residues} residues, the C3 database)")
@@ -329,8 +333,12 @@ def main():
                       "forward_cells": ran["forward"]},
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
-                     "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic,
-                     "traffic_note": "HBM bytes of the MSV stage per search (all its launches), rocprofv3 counters",
+                     "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic[0] if traffic else None,
+                     "traffic_note": ("HBM bytes per MSV launch (FETCH_SIZE + WRITE_SIZE, rocprofv3 counters "
+                                      "scaled by a 1 GiB copy); algorithmic_bytes = residues of the launch's chunk "
+                                      "+ 20 bytes of index and results per target"),
+                     "algorithmic_bytes": traffic[1] if traffic else None,
+                     "ms_per_launch": round(msv_ms / chunks, 4),
                      "peak_measured": round(probe_tops, 3), "frac_of_measured": round(achieved / probe_tops, 4),
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
                      "msv_launches_per_search": chunks}

@@ -130,8 +130,10 @@ __device__ __forceinline__ float wave_sum_f(float v) {
 // time.  With LIMIT, rows from `limit` on (a multiple of 4) are not run.
 // Returns true if a row stopped the driver (`stop` = that row) or the limit
 // was reached (`stop` = limit - 1).  Residue codes are valid (0..19): the
-// database upload checks them, and reads run at most 1 KB past a target,
-// inside the database's zero-filled tail.
+// database upload checks them.  A chunk that holds none of the target's
+// rows is not fetched (its load re-reads the current chunk, already in the
+// cache; no row uses the value), so reads run at most 255 bytes past a
+// target, inside the database's 1 KB zero-filled tail.
 // An empty use of a prefetched table buffer on a driver exit: with it the
 // buffer is live on both sides of the row's stop test, so the compiler keeps
 // its loads ahead of the row (otherwise they sink below the test and every
@@ -158,8 +160,10 @@ __device__ __forceinline__ bool drive_rows(const uint8_t *x, int L, int r0, int 
   if (r >= L) return false;
   const int cs = r & ~255;
   const uint32_t *p = (const uint32_t *)(x + cs);
-  uint32_t cur = __builtin_nontemporal_load(p + lane);
-  uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
+  // chunk k of the target from cs, or chunk `own` when chunk k holds no row
+  auto chunk = [&](int k, int own) { return p[(size_t)(cs + 256 * k < L ? k : own) * kWave + lane]; };
+  uint32_t cur = chunk(0, 0);
+  uint32_t nxt = chunk(1, 0);
   int j0 = (r & 255) >> 2;
   uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, j0);
   load(ba, code(w, 0));
@@ -221,7 +225,7 @@ __device__ __forceinline__ bool drive_rows(const uint8_t *x, int L, int r0, int 
     if (c0 + 256 >= L) return false;
     j0 = 0;
     cur = nxt;
-    nxt = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 2) * kWave + lane);
+    nxt = chunk(((c0 - cs) >> 8) + 2, ((c0 - cs) >> 8) + 1);
   }
 }
 

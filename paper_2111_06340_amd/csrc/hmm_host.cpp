@@ -630,7 +630,7 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
     len[i] = L;
     pos += ((int64_t)L + 15) / 16 * 16;
   }
-  const int64_t res_bytes = pos + 1024;  // residue streams read up to 768 bytes past a target
+  const int64_t res_bytes = pos + 1024;  // residue streams read at most 255 bytes past a target
   // chunk boundaries for every chunk count: about equal residues per chunk
   int64_t chunk_at[kMaxChunks + 1][kMaxChunks + 1] = {};
   for (int K = 1; K <= kMaxChunks; K++) {

@@ -199,8 +199,13 @@ __device__ __forceinline__ void lds_wait(uint32_t (&c)[Q]) {
 // or end of a run; tested).  Returns true if a row stopped the driver
 // (`stop` = the last row computed) or the limit (a multiple of 4) was
 // reached (`stop` = limit - 1).  The residue chunks are loaded two ahead,
-// so the successor dwords of a chunk are at hand without waiting; reads run
-// at most 768 bytes past a target, inside the database's 1 KB zero tail.
+// so the successor dwords of a chunk are at hand without waiting.  A chunk
+// that holds none of the target's rows is not fetched: its load re-reads a
+// chunk already in the cache and no row uses the value, so reads run at
+// most 255 bytes past a target, inside the database's 1 KB zero tail.
+// Plain (cached) loads: the lines a target shares with its neighbours in
+// the length-sorted database, which neighbouring waves of the same block
+// score at about the same time, are then fetched from HBM once.
 template <int Q, typename Load, typename Step, typename Row>
 __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int limit, int &stop, int lane,
                                             uint32_t (&ba)[Q], uint32_t (&bb)[Q], Load load, Step step, Row row) {
@@ -219,9 +224,12 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
   if (r >= L) return false;
   const int cs = r & ~255;
   const uint32_t *p = (const uint32_t *)(x + cs);
-  uint32_t cur = __builtin_nontemporal_load(p + lane);
-  uint32_t nxt = __builtin_nontemporal_load(p + kWave + lane);
-  uint32_t nn = __builtin_nontemporal_load(p + 2 * kWave + lane);
+  // chunk k of the target from cs (its residues cs + 256 k ...), or chunk
+  // `own` when chunk k holds no row
+  auto chunk = [&](int k, int own) { return p[(size_t)(cs + 256 * k < L ? k : own) * kWave + lane]; };
+  uint32_t cur = chunk(0, 0);
+  uint32_t nxt = chunk(1, 0);
+  uint32_t nn = chunk(2, 0);
   uint32_t sh = next_dwords(cur, nxt);
   int j0 = (r & 255) >> 2;
   uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int)cur, j0);
@@ -277,7 +285,7 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
     j0 = 0;
     cur = nxt;
     nxt = nn;
-    nn = __builtin_nontemporal_load(p + (size_t)(((c0 - cs) >> 8) + 3) * kWave + lane);
+    nn = chunk(((c0 - cs) >> 8) + 3, ((c0 - cs) >> 8) + 1);
     sh = next_dwords(cur, nxt);
   }
 }
