@@ -290,6 +290,7 @@ def main():
         # the MSV stage's HBM bytes per search (all of its launches), while
         # the kernel source and the launches per search are the measured ones
         if (tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha()
+                and tr.get("header_sha", kernel_source_sha("hmm_device.h")) == kernel_source_sha("hmm_device.h")
                 and tr.get("launches_per_search") == chunks):
             traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"))
     if batched:
@@ -465,7 +466,9 @@ def measured_traffic(args, name: str, source: str):
         return None
     with open(path) as f:
         tr = json.load(f)
-    return tr.get("bytes_per_launch") if tr.get("kernel_source_sha") == kernel_source_sha(source) else None
+    same = (tr.get("kernel_source_sha") == kernel_source_sha(source)
+            and tr.get("header_sha", kernel_source_sha("hmm_device.h")) == kernel_source_sha("hmm_device.h"))
+    return tr.get("bytes_per_launch") if same else None
 
 
 def kernel_source_sha(source: str = "hmm_kernels.hip") -> str:

@@ -1,0 +1,64 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU contract, the roofline
+arithmetic and the committed counter records it reads."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_peaks_follow_from_the_unit_counts():
+    assert bench.PEAK_PK16_TOPS == pytest.approx(256 * 64 * 2 * 2.4e9 / 1e12)
+    assert bench.PEAK_PK16_TOPS == pytest.approx(78.64, abs=0.01)
+    assert bench.PEAK_I32_TOPS == pytest.approx(bench.PEAK_PK16_TOPS / 2)
+
+
+def test_stage_roofline_arithmetic():
+    # one profile of M = 100 over 1e9 residues: 4e11 MSV ops in 10 ms = 40 Tops/s
+    ran = {"viterbi": 10**9, "rescore": 10**8, "forward": 10**8}
+    out = bench.stage_roofline([100], 10**9, ran, [10.0, 1.0, 1.0, 2.0], chunks=1)
+    assert out["msv"]["achieved"] == pytest.approx(40.0)
+    assert out["msv"]["frac"] == pytest.approx(40.0 / bench.PEAK_PK16_TOPS, abs=1e-4)
+    assert out["viterbi"]["achieved"] == pytest.approx(18.0)          # 18 ops x 1e9 cells / 1 ms
+    assert out["rescore"]["achieved"] == pytest.approx(1.7)           # 17 ops x 1e8 cells / 1 ms
+    assert out["forward"]["achieved"] == pytest.approx(0.9)           # 18 flops x 1e8 cells / 2 ms
+    # pipelined: only MSV's fraction is meaningful
+    piped = bench.stage_roofline([100], 10**9, ran, [10.0, 1.0, 1.0, 2.0], chunks=2)
+    assert set(piped) == {"msv", "note"}
+
+
+@pytest.mark.parametrize("name", ["msv_traffic_C3.json", "decode_traffic_C3.json"])
+def test_counter_records_are_consistent(name):
+    with open(os.path.join(ROOT, "profiles", name)) as f:
+        tr = json.load(f)
+    assert tr["workload"] == "C3"
+    assert len(tr["kernel_source_sha"]) == 16 and len(tr["header_sha"]) == 16
+    fetch = tr.get("fetch_bytes_per_launch", tr.get("fetch_bytes"))
+    write = tr.get("write_bytes_per_launch", tr.get("write_bytes"))
+    assert tr["bytes_per_launch"] == fetch + write
+    assert tr["scale"]["FETCH_SIZE"] == pytest.approx(2.0, abs=0.01)
+    if name.startswith("msv"):
+        assert tr["launches_per_search"] == 2
+        assert tr["bytes_per_search"] == 2 * tr["bytes_per_launch"]
+        # the kernel reads every residue of its chunk at least once
+        assert tr["bytes_per_launch"] >= tr["algorithmic_bytes_per_launch"]
+
+
+def test_kernel_source_sha_is_the_file_hash():
+    import hashlib
+    p = os.path.join(ROOT, "paper_2111_06340_amd", "csrc", "hmm_kernels.hip")
+    with open(p, "rb") as f:
+        assert bench.kernel_source_sha() == hashlib.sha256(f.read()).hexdigest()[:16]
