@@ -41,14 +41,20 @@ namespace hmmgpu {
 namespace {
 
 // Inclusive prefix scan across lanes (lane l-1 -> l) of affine maps
-// x -> a + P x, with the P parts before each step in ps.
+// x -> a + P x, with the P parts before each step in ps.  A lane without a
+// source reads 0 (bound_ctrl), which leaves its map unchanged, so each
+// step can be one fused DPP multiply-add.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ float dpp_f0(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROWMASK, 0xf, true));
+}
 __device__ __forceinline__ float affine_scan(float a, const float (&ps)[6]) {
-  a = fmaf(ps[0], dpp_f<kRowShr1, 0xf>(a, 0.0f), a);
-  a = fmaf(ps[1], dpp_f<kRowShr2, 0xf>(a, 0.0f), a);
-  a = fmaf(ps[2], dpp_f<kRowShr4, 0xf>(a, 0.0f), a);
-  a = fmaf(ps[3], dpp_f<kRowShr8, 0xf>(a, 0.0f), a);
-  a = fmaf(ps[4], dpp_f<kRowBcast15, 0xa>(a, 0.0f), a);
-  a = fmaf(ps[5], dpp_f<kRowBcast31, 0xc>(a, 0.0f), a);
+  a = fmaf(dpp_f0<kRowShr1, 0xf>(a), ps[0], a);
+  a = fmaf(dpp_f0<kRowShr2, 0xf>(a), ps[1], a);
+  a = fmaf(dpp_f0<kRowShr4, 0xf>(a), ps[2], a);
+  a = fmaf(dpp_f0<kRowShr8, 0xf>(a), ps[3], a);
+  a = fmaf(dpp_f0<kRowBcast15, 0xa>(a), ps[4], a);
+  a = fmaf(dpp_f0<kRowBcast31, 0xc>(a), ps[5], a);
   return a;
 }
 __device__ __forceinline__ void affine_steps(float p, float (&ps)[6]) {
@@ -165,7 +171,6 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
   }
   const float mdn = into_next(TR_MDIN, w), ddn = into_next(TR_DDIN, w);
   const float entry_p = P.entry_p;
-  const float *emit = P.f_emit + lane;
   const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = next_target(&db.counters[CNT_WORK_FWD], &slot);
@@ -180,12 +185,14 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
     float pM = 0.0f, pI = 0.0f, pD = 0.0f;   // previous row, left neighbour of the first cell
     float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
     int shift = 0, par = 0;
+    // row of residue a: a wave-uniform base (scalar address) and the lane
+    // as the only vector part of every read
     auto load = [&](float(&e)[2 * QW], int a) {
-      const float *er = emit + a * (2 * Q * kWave);
+      const float *em = P.f_emit + (size_t)a * (2 * Q * kWave) + q0 * kWave;
 #pragma unroll
       for (int q = 0; q < QW; q++) {
-        e[q] = er[(q0 + q) * kWave];
-        e[QW + q] = er[(Q + q0 + q) * kWave];
+        e[q] = em[q * kWave + lane];
+        e[QW + q] = em[(Q + q) * kWave + lane];
       }
     };
     auto row = [&](const float(&em)[2 * QW]) -> bool {
@@ -348,7 +355,6 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
     maxplus_steps_i(lanep, bs);
   }
   const int mdn = into_next(TR_MDIN, w), ddn = into_next(TR_DDIN, w);
-  const int *emit = P.v32_emit + lane;
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = next_target(&db.counters[CNT_WORK_OVF], &slot);
@@ -367,11 +373,11 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
     int T = -ej + 1;
     int par = 0;
     auto load = [&](int(&e)[2 * QW], int a) {
-      const int *er = emit + a * (2 * Q * kWave);
+      const int *em = P.v32_emit + (size_t)a * (2 * Q * kWave) + q0 * kWave;
 #pragma unroll
       for (int q = 0; q < QW; q++) {
-        e[q] = er[(q0 + q) * kWave];
-        e[QW + q] = er[(Q + q0 + q) * kWave];
+        e[q] = em[q * kWave + lane];
+        e[QW + q] = em[(Q + q) * kWave + lane];
       }
     };
     auto row = [&](const int(&em)[2 * QW]) -> bool {
