@@ -81,7 +81,7 @@ def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
     t, nres, nseq = run(stride)
     gcups = prof.M * nres / t / 1e9
     return {"value": round(gcups, 4), "unit": "GCUPS", "cores": threads, "kind": "oracle",
-            "sample": f"every {stride}th target of the same database ({nseq} targets, {nres} residues), "
+            "sample": f"one target in {stride} of the same database ({nseq} targets, {nres} residues), "
                       f"same cutoffs, oracle's own calibration; {t:.1f} s wall",
             "seconds": round(t, 2)}
 
