@@ -23,7 +23,12 @@ back to back on the search stream, between HIP events that the library
 records there, so the average launch lasts the stage's time divided by the
 launches.  `traffic` is the HBM bytes per MSV launch that rocprofv3's
 FETCH_SIZE and WRITE_SIZE counters measured for the same kernel source
-(scaled by a plain 1 GiB copy), beside the launch's algorithmic bytes.  `stage_roofline` gives the same
+(scaled by a plain 1 GiB copy), beside the launch's algorithmic bytes;
+`valu_issue` is the share of the chip's sustained VALU issue rate that the
+launch's counted VALU instructions took.  The MSV needs fewer instructions
+than 4 per cell (one packed add and one packed 3-way maximum per two
+cells, plus its running maxima), so its algorithmic fraction can pass 1
+while its issue fraction cannot.  `stage_roofline` gives the same
 fraction for every stage (Viterbi 18 ops/cell, rescore 17 int32 ops/cell
 against 39.32 Tops/s, Forward 18 flops/cell against 157.3 TFLOP/s).
 """
@@ -84,6 +89,17 @@ def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
             "sample": f"one target in {stride} of the same database ({nseq} targets, {nres} residues), "
                       f"same cutoffs, oracle's own calibration; {t:.1f} s wall",
             "seconds": round(t, 2)}
+
+
+def valu_issue(insts_per_launch, ms_per_launch, probe_ops_per_s):
+    """Share of the sustained VALU issue rate a launch used: its wave64 VALU
+    instructions (rocprofv3 SQ_INSTS_VALU, for the same kernel source) over
+    its duration times the chip's sustained rate of wave instructions (the
+    packed 16-bit probe's element-ops / 128: 64 lanes x 2 halves each).
+    Unlike the algorithmic fraction this cannot exceed 1."""
+    rate = probe_ops_per_s / 128.0
+    return {"insts_per_launch": insts_per_launch, "sustained_insts_per_s": round(rate, 1),
+            "frac": round(insts_per_launch / (ms_per_launch / 1e3 * rate), 4)}
 
 
 def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
@@ -292,7 +308,8 @@ def main():
         if (tr.get("workload") == w.name and tr.get("kernel_source_sha") == kernel_source_sha()
                 and tr.get("header_sha", kernel_source_sha("hmm_device.h")) == kernel_source_sha("hmm_device.h")
                 and tr.get("launches_per_search") == chunks):
-            traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"))
+            traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"),
+                       tr.get("valu_insts_per_launch"))
     if batched:
         wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
               f"against {D.n} synthetic sequences ({D.n_residues} residues, the C3 database)")
@@ -341,6 +358,8 @@ def main():
                      "algorithmic_bytes": traffic[1] if traffic else None,
                      "ms_per_launch": round(msv_ms / chunks, 4),
                      "peak_measured": round(probe_tops, 3), "frac_of_measured": round(achieved / probe_tops, 4),
+                     "valu_issue": (valu_issue(traffic[2], msv_ms / chunks, probe_ops)
+                                    if traffic and traffic[2] else None),
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
                      "msv_launches_per_search": chunks}
         if timed_stages else None,

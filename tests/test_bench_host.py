@@ -55,6 +55,17 @@ def test_counter_records_are_consistent(name):
         assert tr["bytes_per_search"] == 2 * tr["bytes_per_launch"]
         # the kernel reads every residue of its chunk at least once
         assert tr["bytes_per_launch"] >= tr["algorithmic_bytes_per_launch"]
+        # at least one VALU instruction per two cells of the launch's chunk
+        cells = 734 * tr["algorithmic_bytes_per_launch"] * 0.9
+        assert tr["valu_insts_per_launch"] * 64 * 2 >= cells
+
+
+def test_valu_issue_arithmetic():
+    # 1e9 wave instructions in 5 ms on a chip that sustains 128e12
+    # element-ops/s (1e12 wave instructions/s): 0.2 of the issue rate
+    out = bench.valu_issue(1e9, 5.0, 128e12)
+    assert out["sustained_insts_per_s"] == pytest.approx(1e12)
+    assert out["frac"] == pytest.approx(0.2)
 
 
 def test_kernel_source_sha_is_the_file_hash():
