@@ -121,7 +121,8 @@ def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
                        f"stage_ms holds their exposed time after the last MSV")
         return out
     out["viterbi"] = entry(VIT_OPS_PER_CELL * ran_cells["viterbi"], st_ms[1], round(PEAK_PK16_TOPS, 2),
-                           "Tops/s packed 16-bit, 18 ops/cell")
+                           "Tops/s packed 16-bit, 18 ops/cell, cells of the targets scored to their last row "
+                           "(int16 overflows, which stop early, left out: a lower bound)")
     out["rescore"] = entry(RESCORE_OPS_PER_CELL * ran_cells["rescore"], st_ms[2], round(PEAK_I32_TOPS, 2),
                            "Tops/s 32-bit, 17 ops/cell")
     # Forward runs beside the rescore; its figure here uses the time both take
@@ -277,13 +278,22 @@ def main():
     cells = sum(M_list) * sum(Dx.n_residues for Dx in Ds)
     gcups = cells / (ms_step / 1e3) / 1e9
     counts = np.zeros(4, np.int64)
-    ran = {"viterbi": 0, "rescore": 0, "forward": 0}
+    # cells each stage processed.  The int16 Viterbi pass (and MSV) stop at
+    # the row where a target overflows, so Viterbi counts only the targets
+    # it scored to the end (a lower bound of its work); the cells of the
+    # overflowed targets, whose rows past the overflow are never computed,
+    # are reported apart.
+    ran = {"viterbi": 0, "viterbi_overflow": 0, "msv_overflow": 0, "rescore": 0, "forward": 0}
     for (pi, di), out in zip(jobs, outs):
         p = profs[pi]
         lengths = np.diff(dbs[di].offsets)
         counts += out["counts"].cpu().numpy()
         fl = out["flags"].cpu().numpy()
-        ran["viterbi"] += p.M * int(lengths[(fl & hg.HMM_VIT_RAN) != 0].sum())
+        vit_ran = (fl & hg.HMM_VIT_RAN) != 0
+        vit_ovf = (fl & hg.HMM_VIT_OVF) != 0
+        ran["viterbi"] += p.M * int(lengths[vit_ran & ~vit_ovf].sum())
+        ran["viterbi_overflow"] += p.M * int(lengths[vit_ran & vit_ovf].sum())
+        ran["msv_overflow"] += p.M * int(lengths[(fl & hg.HMM_MSV_OVF) != 0].sum())
         ran["rescore"] += p.M * int(lengths[(fl & hg.HMM_VIT_OVF) != 0].sum())
         ran["forward"] += p.M * int(lengths[(fl & hg.HMM_FWD_RAN) != 0].sum())
     counts = counts.tolist()
@@ -347,7 +357,9 @@ def main():
                       "bias_pass": (int(sum(int(((o["flags"].cpu().numpy() & hg.HMM_BIAS_PASS) != 0).sum())
                                             for o in outs)) if args.bias else None),
                       "vit_overflow": counts[1], "vit_pass": counts[2],
-                      "fwd_pass": counts[3], "viterbi_cells": ran["viterbi"], "rescore_cells": ran["rescore"],
+                      "fwd_pass": counts[3], "viterbi_cells": ran["viterbi"],
+                      "viterbi_overflow_cells": ran["viterbi_overflow"], "msv_overflow_cells": ran["msv_overflow"],
+                      "rescore_cells": ran["rescore"],
                       "forward_cells": ran["forward"]},
         "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
                      "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
