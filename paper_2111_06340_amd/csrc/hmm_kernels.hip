@@ -851,6 +851,15 @@ __global__ void reset_ovf(int32_t *c) {
 // registers rather than to scratch memory.
 template <int Q>
 constexpr int kThreads16 = Q >= 16 ? 256 : 512;
+// Instances whose transition planes, all but D->D, are read from LDS every
+// row instead of being held in registers (D->D, which the lazy delete
+// propagation also reads, stays in registers): 120 fewer registers at 20
+// vectors per lane, so that two waves share a SIMD and hide each other's
+// waits.
+template <int Q>
+constexpr bool kTrLds16 = Q == 16 || Q == 20;
+template <int Q>
+constexpr int kMinWaves16 = kTrLds16<Q> ? 2 : 1;
 // Threads per block of the one-wave rescore and Forward kernels.
 constexpr int kThreads32 = 512;
 
@@ -860,10 +869,10 @@ struct VitResult {
 };
 
 
-template <int Q>
+template <int Q, bool TRL = false>
 __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ emit, const uint32_t (&tr)[TR_N][Q],
                                                   const DevProfile &P, const uint8_t *x, int L,
-                                                  const LenParams &lp, int lane) {
+                                                  const LenParams &lp, int lane, const uint32_t *ltr = nullptr) {
   uint32_t M[Q], I[Q], D[Q];
 #pragma unroll
   for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNegNeg;
@@ -883,17 +892,24 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
   };
   auto row = [&](const uint32_t(&em)[2 * Q]) -> bool {
+    // LDS planes: an offset the compiler cannot see through keeps their
+    // reads inside the row (loop-invariant reads would be hoisted back
+    // into registers)
+    int off = 0;
+    if (TRL) asm volatile("" : "+v"(off));
+    auto trv = [&](int k, int q) -> uint32_t { return TRL ? ltr[off + (k * Q + q) * kWave] : tr[k][q]; };
     const uint32_t msh = slot_up16(M[Q - 1]);
     const uint32_t ish = slot_up16(I[Q - 1]);
     const uint32_t dsh = slot_up16(D[Q - 1]);
 #pragma unroll
     for (int q = Q - 1; q >= 0; q--) {
       const uint32_t pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-      uint32_t m = i16_max(xbe2, i16_adds(pm, tr[TR_MMIN][q]));
-      m = i16_max(m, i16_adds(pi, tr[TR_IMIN][q]));
-      m = i16_max(m, i16_adds(pd, tr[TR_DMIN][q]));
+      uint32_t m = i16_max(xbe2, i16_adds(pm, trv(TR_MMIN, q)));
+      m = i16_max(m, i16_adds(pi, trv(TR_IMIN, q)));
+      m = i16_max(m, i16_adds(pd, trv(TR_DMIN, q)));
       const uint32_t mn = i16_adds(m, em[q]);
-      const uint32_t in = i16_adds(i16_max(i16_adds(M[q], tr[TR_MI][q]), i16_adds(I[q], tr[TR_II][q])), em[Q + q]);
+      const uint32_t in =
+          i16_adds(i16_max(i16_adds(M[q], trv(TR_MI, q)), i16_adds(I[q], trv(TR_II, q))), em[Q + q]);
       accM = i16_max(accM, mn);
       accI = i16_max(accI, in);
       M[q] = mn;
@@ -903,7 +919,7 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     const uint32_t din = slot_up16(M[Q - 1]);
 #pragma unroll
     for (int q = 0; q < Q; q++) {
-      D[q] = i16_max(i16_max(i16_adds(q ? M[q - 1] : din, tr[TR_MDIN][q]), i16_adds(dc, tr[TR_DDIN][q])), tau2);
+      D[q] = i16_max(i16_max(i16_adds(q ? M[q - 1] : din, trv(TR_MDIN, q)), i16_adds(dc, tr[TR_DDIN][q])), tau2);
       dc = D[q];
     }
     // A chain can cross into the next slot only from a slot whose last
@@ -953,13 +969,16 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
 }
 
 template <int Q, bool EMIT_LDS>
-__global__ void __launch_bounds__(kThreads16<Q>) vit16_kernel(DevProfile P, DevDb db, DevOut out) {
+__global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ uint32_t lds[];
+  constexpr bool TRL = kTrLds16<Q>;
+  static_assert(!(TRL && EMIT_LDS), "one LDS table per instance");
   const int lane = threadIdx.x & 63;
-  if (EMIT_LDS) {
-    const uint4 *src = (const uint4 *)P.vit_emit;
+  if (EMIT_LDS || TRL) {
+    const uint4 *src = (const uint4 *)(EMIT_LDS ? P.vit_emit : P.vit_tr);
+    const int n4 = (EMIT_LDS ? kAlpha * 2 : TR_N) * Q * kWave / 4;
     uint4 *dst = (uint4 *)lds;
-    for (int i = threadIdx.x; i < kAlpha * 2 * Q * kWave / 4; i += blockDim.x) dst[i] = src[i];
+    for (int i = threadIdx.x; i < n4; i += blockDim.x) dst[i] = src[i];
     __syncthreads();
   }
   const uint32_t *emit = (EMIT_LDS ? (const uint32_t *)lds : P.vit_emit) + lane;
@@ -967,7 +986,8 @@ __global__ void __launch_bounds__(kThreads16<Q>) vit16_kernel(DevProfile P, DevD
 #pragma unroll
   for (int k = 0; k < TR_N; k++)
 #pragma unroll
-    for (int q = 0; q < Q; q++) tr[k][q] = P.vit_tr[(k * Q + q) * kWave + lane];
+    for (int q = 0; q < Q; q++)
+      tr[k][q] = (!TRL || k == TR_DDIN) ? P.vit_tr[(k * Q + q) * kWave + lane] : 0u;
   const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_VIT], 1);
@@ -975,7 +995,7 @@ __global__ void __launch_bounds__(kThreads16<Q>) vit16_kernel(DevProfile P, DevD
     const int t = uni(db.list_vit[idx]);
     const int L = uni(db.len[t]);
     const LenParams lp = db.lp[L];
-    const VitResult r = vit16_target<Q>(emit, tr, P, db.res + db.start[t], L, lp, lane);
+    const VitResult r = vit16_target<Q, TRL>(emit, tr, P, db.res + db.start[t], L, lp, lane, (const uint32_t *)lds + lane);
     const bool pass = r.ovf || r.raw >= lp.thr16;
     const uint8_t fl =
         (uint8_t)(uni(db.flags_sorted[t]) | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0));
@@ -1317,7 +1337,7 @@ template <int Q>
 hipError_t launch_vit16(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
   constexpr bool kLds = Q <= 8;
   const int threads = kThreads16<Q>;
-  const size_t lds = kLds ? (size_t)kAlpha * 2 * Q * kWave * 4 : 0;
+  const size_t lds = kLds ? (size_t)kAlpha * 2 * Q * kWave * 4 : kTrLds16<Q> ? (size_t)TR_N * Q * kWave * 4 : 0;
   auto k = vit16_kernel<Q, kLds>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
