@@ -245,6 +245,18 @@ def test_random_transitions_exercise_insert_and_delete_paths(seed):
     announce(f"random transitions seed={seed} ok {compare(g, o, what='random-trans')}")
 
 
+@pytest.mark.parametrize("M", [1990, 2047, 2300, 2560])
+def test_random_transitions_long_profiles(M):
+    # 16 and 20 vectors per lane: the Viterbi instances that read their
+    # transition planes from LDS every row; per-node transitions, so that a
+    # plane or vector read at the wrong place changes some score
+    prof = random_profile(M, 90 + M, alpha=0.3, talpha=0.6)
+    res, off = _ragged_db(prof, M, lengths=[50, 300, 700, 1200, 90, 5, 333, 2600], homolog_every=2)
+    g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0))
+    announce(f"random transitions M={M} ok {compare(g, o, what='random-trans long')}")
+
+
 def _peaked(M, seed, p_top=0.81):
     rng = np.random.default_rng(seed)
     c = rng.integers(0, 19, size=M)
