@@ -204,11 +204,13 @@ def length_params(L: int, library=None) -> dict:
                 move8=l.orc_move8(L), move16=l.orc_move16(L))
 
 
-def thresholds(calib, F, L: int) -> tuple[int, int, float]:
+def thresholds(calib, F, L: int, library=None) -> tuple[int, int, float]:
+    """(THR8(L), THR16(L), Forward cutoff in nats) of orc_thresholds."""
     c = np.asarray(calib, np.float64)
     f = np.asarray(F, np.float64)
     t8, t16, ft = C.c_int32(0), C.c_int32(0), C.c_double(0)
-    lib().orc_thresholds(_ptr(c), _ptr(f), L, C.byref(t8), C.byref(t16), C.byref(ft))
+    (lib() if library is None else library).orc_thresholds(_ptr(c), _ptr(f), L, C.byref(t8), C.byref(t16),
+                                                           C.byref(ft))
     return int(t8.value), int(t16.value), float(ft.value)
 
 
@@ -232,10 +234,23 @@ def gumbel_mu(bits: np.ndarray, lam: float = LN2) -> float:
     return float(-math.log(np.mean(np.exp(-lam * b))) / lam)
 
 
+FWD_TAIL = 0.04     # tail mass the Forward location is fitted at
+
+
+def exp_tail_location(bits, tail: float = FWD_TAIL, lam: float = LN2) -> float:
+    """Location tau of an exponential tail P(S > x) = exp(-lam (x - tau))
+    that gives the (tail * n)-th largest of n scores the survival `tail`:
+    exp(-lam (x_c - tau)) = tail, so tau = x_c + ln(tail) / lam."""
+    b = np.sort(np.asarray(bits, np.float64))[::-1]
+    xc = b[int(round(tail * b.size)) - 1]
+    return float(xc + math.log(tail) / lam)
+
+
 def calibrate(p: OracleProfile, nthreads: int = 8, n: int = 200) -> tuple[float, float, float]:
     """(mu_msv, mu_vit, tau) in bits from oracle scores of i.i.d. background
     sequences: n of length 200 for the filters, n of length 100 for Forward;
-    tau puts a tail mass of 0.04 at the 8th-largest Forward score."""
+    tau puts a tail mass of 0.04 at the (0.04 n)-th largest Forward score
+    (the 8th at n = 200)."""
     from synth import gen
     db = gen.random_sequences(gen.SEED_CALIB_VIT, n, 200)
     r = search(p, db.residues, db.offsets, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0), nthreads)
@@ -243,10 +258,7 @@ def calibrate(p: OracleProfile, nthreads: int = 8, n: int = 200) -> tuple[float,
     mu_vit = gumbel_mu([vit_bits(int(v), 200) for v in r["vit"]])
     dbf = gen.random_sequences(gen.SEED_CALIB_FWD, n, 100)
     rf = search(p, dbf.residues, dbf.offsets, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0), nthreads)
-    fb = np.sort([fwd_bits(float(v), 100) for v in rf["fwd"]])[::-1]
-    tail = 0.04
-    xc = fb[int(round(tail * n)) - 1]
-    tau = float(xc + math.log(tail) / LN2)
+    tau = exp_tail_location([fwd_bits(float(v), 100) for v in rf["fwd"]])
     return mu_msv, mu_vit, tau
 
 

@@ -53,6 +53,13 @@ MUTANTS = {
     "bias_mean_not_divided": ("p->bias_lr[a] = log(m / (double)M / bg[a]);", "p->bias_lr[a] = log(m / bg[a]);"),
     "bias_switch_swapped": ("const double q = lse(aR + ls, aS + lt) + p->bias_lr[x[i]];",
                             "const double q = lse(aR + lt, aS + ls) + p->bias_lr[x[i]];"),
+    # Forward cutoff (P-value of the exponential tail below F3)
+    "fwd_cutoff_sign_of_ln_f3": ("*fwd_thr = (calib[2] - log(F[2]) / M_LN2) * M_LN2 + nul;",
+                                 "*fwd_thr = (calib[2] + log(F[2]) / M_LN2) * M_LN2 + nul;"),
+    "fwd_cutoff_without_null": ("*fwd_thr = (calib[2] - log(F[2]) / M_LN2) * M_LN2 + nul;",
+                                "*fwd_thr = (calib[2] - log(F[2]) / M_LN2) * M_LN2;"),
+    "fwd_cutoff_in_bits": ("*fwd_thr = (calib[2] - log(F[2]) / M_LN2) * M_LN2 + nul;",
+                           "*fwd_thr = (calib[2] - log(F[2]) / M_LN2) + nul;"),
     "regions_strict_rt2": ("if (!(pcore[i] >= rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
                            "    while (j < L && pcore[j] >= rt2)",
                            "if (!(pcore[i] > rt2)) { i++; continue; }\n    int j = i, hit = 0;\n"
@@ -89,6 +96,7 @@ def _battery(lib) -> list:
         lp = oracle.length_params(L, lib)
         check("move", lp["move8"] == mv8 and lp["move16"] == mv16)
     from synth import make_profile
+    from synth.gen import SEED_CALIB_FWD, random_sequences
     for M, e8, e16 in ((77, 35, -5776), (734, 54, -9021)):
         s = oracle.OracleProfile(make_profile(M, 7), lib).scalars()
         check("entry", s["entry8"] == e8 and s["entry16"] == e16)
@@ -129,6 +137,20 @@ def _battery(lib) -> list:
         prof = random_profile(7, seed, alpha=0.3)
         x = np.random.default_rng(seed + 10).integers(0, 20, L).astype(np.uint8)
         check("bias", math.isclose(oracle.bias(oracle.OracleProfile(prof, lib), x), bias_brute(prof, x), abs_tol=1e-9))
+    # Forward cutoff: with tau fitted at tail mass 0.04 on 2,000 background
+    # sequences, a fresh sample passes F3 = 0.05 at about that rate
+    fprof = make_profile(20, 3)
+    fop = oracle.OracleProfile(fprof, lib)
+    fcal = oracle.calibrate(fop, nthreads=8, n=2000)
+    fdb = random_sequences(SEED_CALIB_FWD + 97, 4000, 100)
+    fr = oracle.search(fop, fdb.residues, fdb.offsets, fcal, (1.0, 1.0, 0.05), nthreads=8)
+    frac = float(np.mean((fr["flags"] & oracle.F_FWD_PASS) != 0))
+    check("fwd_cutoff", 0.025 < frac < 0.075)
+    # ... and the exponential tail's survival at the cutoff is F3 itself
+    for L, tau, F3 in ((100, -3.9, 0.05), (300, -7.2, 1e-3), (30, 2.5, 0.5)):
+        thr = oracle.thresholds((0.0, 0.0, tau), (1.0, 1.0, F3), L, lib)[2]
+        x = (thr - oracle.length_params(L, lib)["null"]) / math.log(2.0)
+        check("fwd_cutoff_survival", math.isclose(math.exp(-math.log(2.0) * (x - tau)), F3, rel_tol=1e-9))
     core = np.array([0.05, 0.10, 0.2, 0.25, 0.099, 0.3, 0.24, 0.11, 0.09, 0.12, 0.2, 0.1, 0.5, 0.1])
     check("regions", oracle.regions(core, 0.25, 0.10, lib) == [(2, 4), (6, 8), (10, 14)])
     return fails
