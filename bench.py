@@ -47,6 +47,7 @@ sys.path.insert(0, ROOT)
 PEAK_PK16_TOPS = 256 * 64 * 2 * 2.4e9 / 1e12      # 78.64
 PEAK_I32_TOPS = 256 * 64 * 2.4e9 / 1e12           # 39.32
 PEAK_FP32_TFLOPS = 157.3                          # datasheet (packed fp32 FMA)
+PEAK_WAVE_INSTS = 256 * 2.4e9                     # VALU wave64 instructions per second (one per CU per clock)
 MSV_OPS_PER_CELL = 4
 VIT_OPS_PER_CELL = 18
 RESCORE_OPS_PER_CELL = 17
@@ -59,14 +60,39 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
+def host_cpus() -> dict:
+    """The host the CPU baseline runs on: logical CPUs, the CPUs this
+    process may use, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+def oracle_threads() -> int:
+    """Threads of the CPU baseline: the host CPUs allotted to this GPU
+    (OMP_NUM_THREADS where the job scheduler sets it, else 16), within the
+    CPUs this process may use."""
+    share = int(os.environ.get("OMP_NUM_THREADS") or 16)
+    return max(1, min(share, len(os.sched_getaffinity(0))))
+
+
+def cpu_baseline(profs, db, F, budget_s: float, threads: int) -> dict:
     """The CPU oracle (scalar C, threaded) on a stride sample of the same
-    database, sized to roughly `budget_s` seconds."""
+    database, every profile of the workload on the same sample, sized to
+    roughly `budget_s` seconds; GCUPS = sum over profiles of M x sampled
+    residues / seconds."""
     import numpy as np
 
     import oracle
-    op = oracle.OracleProfile(prof)
-    calib = oracle.calibrate(op, nthreads=threads)
+    ops = [oracle.OracleProfile(p) for p in profs]
+    calibs = [oracle.calibrate(op, nthreads=threads) for op in ops]
     lengths = np.diff(db.offsets)
 
     def run(stride):
@@ -76,19 +102,34 @@ def cpu_baseline(prof, db, F, budget_s: float, threads: int) -> dict:
         off[1:] = np.cumsum(lengths[idx])
         res = np.concatenate(seqs)
         t = time.perf_counter()
-        oracle.search(op, res, off, calib, F, nthreads=threads)
+        for op, calib in zip(ops, calibs):
+            oracle.search(op, res, off, calib, F, nthreads=threads)
         return time.perf_counter() - t, int(res.size), int(idx.size)
 
-    probe_stride = max(1, db.n // 2000)
+    probe_stride = max(1, db.n * len(profs) // 2000)
     t, nres, nseq = run(probe_stride)
     rate = nres / max(t, 1e-6)
     stride = max(1, int(math.ceil(db.n * float(lengths.mean()) / (rate * budget_s))))
     t, nres, nseq = run(stride)
-    gcups = prof.M * nres / t / 1e9
+    gcups = sum(p.M for p in profs) * nres / t / 1e9
+    what = "every profile on " if len(profs) > 1 else ""
     return {"value": round(gcups, 4), "unit": "GCUPS", "cores": threads, "kind": "oracle",
-            "sample": f"one target in {stride} of the same database ({nseq} targets, {nres} residues), "
-                      f"same cutoffs, oracle's own calibration; {t:.1f} s wall",
-            "seconds": round(t, 2)}
+            "sample": f"{what}one target in {stride} of the same database ({nseq} targets, {nres} residues), "
+                      f"same cutoffs, oracle's own calibration; {t:.1f} s wall on {threads} threads",
+            "seconds": round(t, 2), "host": host_cpus(),
+            "threads_note": "one oracle thread per host CPU allotted to this GPU (16 on a one-GPU share)"}
+
+
+def issue_roofline(insts_per_launch, ms_per_launch) -> dict:
+    """VALU issue of a launch against the datasheet: its wave64 VALU
+    instructions (rocprofv3 SQ_INSTS_VALU, same kernel source) over its
+    live duration, against one wave instruction per CU per clock (4 SIMD16
+    each issue a wave64 instruction per 4 clocks): 256 x 2.4e9 = 6.144e11
+    per second.  In packed 16-bit element-ops (x 128 per instruction) the
+    peak is 78.64 Tops/s.  Cannot exceed 1."""
+    rate = insts_per_launch / (ms_per_launch / 1e3)
+    return {"achieved": round(rate * 128 / 1e12, 3), "peak": round(PEAK_PK16_TOPS, 2),
+            "frac": round(rate / PEAK_WAVE_INSTS, 4), "insts_per_launch": insts_per_launch}
 
 
 def valu_issue(insts_per_launch, ms_per_launch, probe_ops_per_s):
@@ -113,7 +154,8 @@ def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
 
     def entry(ops, ms, peak, unit):
         ach = ops / (ms / 1e3) / 1e12 if ms > 0 else 0.0
-        return {"achieved": round(ach, 3), "peak": peak, "unit": unit, "frac": round(ach / peak, 4)}
+        return {"algorithmic_achieved": round(ach, 3), "peak": peak, "unit": unit,
+                "algorithmic_frac": round(ach / peak, 4)}
 
     out["msv"] = entry(msv_ops, st_ms[0], round(PEAK_PK16_TOPS, 2), "Tops/s packed 16-bit, 4 ops/cell")
     if chunks > 1:
@@ -320,6 +362,7 @@ def main():
                 and tr.get("launches_per_search") == chunks):
             traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"),
                        tr.get("valu_insts_per_launch"))
+    issue = issue_roofline(traffic[2], msv_ms / chunks) if traffic and traffic[2] and msv_ms > 0 else None
     if batched:
         wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
               f"against {D.n} synthetic sequences ({D.n_residues} residues, the C3 database)")
@@ -361,15 +404,28 @@ def main():
                       "viterbi_overflow_cells": ran["viterbi_overflow"], "msv_overflow_cells": ran["msv_overflow"],
                       "rescore_cells": ran["rescore"],
                       "forward_cells": ran["forward"]},
-        "roofline": {"bound": "alu", "kernel": "msv_kernel", "achieved": round(achieved, 3),
-                     "peak": round(PEAK_PK16_TOPS, 2), "unit": "Tops/s (packed 16-bit VALU element-ops)",
-                     "frac": round(achieved / PEAK_PK16_TOPS, 4), "traffic": traffic[0] if traffic else None,
+        "roofline": {"bound": "alu", "kernel": "msv_kernel",
+                     "achieved": issue["achieved"] if issue else None,
+                     "peak": round(PEAK_PK16_TOPS, 2),
+                     "unit": "Tops/s packed 16-bit VALU issue (SQ_INSTS_VALU x 128 per launch / launch time)",
+                     "frac": issue["frac"] if issue else None,
+                     "frac_note": ("wave64 VALU instructions per MSV launch (rocprofv3 counter record for this "
+                                   "kernel source) / live launch time / (256 CU x 2.4 GHz); null when the record "
+                                   "is for another source"),
+                     "valu_insts_per_launch": issue["insts_per_launch"] if issue else None,
+                     "algorithmic_achieved": round(achieved, 3),
+                     "algorithmic_frac": round(achieved / PEAK_PK16_TOPS, 4),
+                     "algorithmic_note": ("4 packed 16-bit ops per cell (max, saturating add, saturating subtract, "
+                                          "running max) x M x residues of a launch / launch time; the fp16 rewrite "
+                                          "needs fewer instructions than that, so this can pass 1"),
+                     "traffic": traffic[0] if traffic else None,
                      "traffic_note": ("HBM bytes per MSV launch (FETCH_SIZE + WRITE_SIZE, rocprofv3 counters "
                                       "scaled by a 1 GiB copy); algorithmic_bytes = residues of the launch's chunk "
                                       "+ 20 bytes of index and results per target"),
                      "algorithmic_bytes": traffic[1] if traffic else None,
                      "ms_per_launch": round(msv_ms / chunks, 4),
-                     "peak_measured": round(probe_tops, 3), "frac_of_measured": round(achieved / probe_tops, 4),
+                     "peak_measured": round(probe_tops, 3),
+                     "algorithmic_frac_of_measured": round(achieved / probe_tops, 4),
                      "valu_issue": (valu_issue(traffic[2], msv_ms / chunks, probe_ops)
                                     if traffic and traffic[2] else None),
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
@@ -396,10 +452,10 @@ def main():
         h.close()
     for Dx in Ds:
         Dx.close()
-    if not args.no_cpu_baseline and not batched and len(Ds) == 1:
-        threads = min(16, len(os.sched_getaffinity(0)))
+    if not args.no_cpu_baseline and len(Ds) == 1:
+        threads = oracle_threads()
         log(f"CPU oracle baseline on {threads} threads ...")
-        rec["cpu_baseline"] = cpu_baseline(profs[0], db, F, args.cpu_seconds, threads)
+        rec["cpu_baseline"] = cpu_baseline(profs, db, F, args.cpu_seconds, threads)
         log(f"CPU oracle: {rec['cpu_baseline']['value']} GCUPS")
     print(json.dumps(rec), flush=True)
 

@@ -7,6 +7,7 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -23,7 +24,8 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False, save_temps: str | None = None) -> str:
-    objs = []
+    """Compile every source (concurrently) and link the shared library."""
+    cmds, objs = [], []
     for src in SOURCES:
         obj = os.path.join(CSRC, src + ".o")
         cmd = [hipcc(), "-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
@@ -33,8 +35,12 @@ def build(verbose: bool = False, save_temps: str | None = None) -> str:
             cmd.insert(1, f"-save-temps={save_temps}")
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.check_call(cmd, cwd=save_temps or CSRC)
+        cmds.append(cmd)
         objs.append(obj)
+    jobs = max(1, min(len(cmds), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+    with ThreadPoolExecutor(jobs) as ex:
+        for f in [ex.submit(subprocess.check_call, c, cwd=save_temps or CSRC) for c in cmds]:
+            f.result()
     tmp = LIB + ".tmp"
     subprocess.check_call([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)

@@ -153,42 +153,95 @@ def sample_ids(db, n_random, n_planted, seed):
     return np.unique(np.concatenate([r, p]).astype(np.int64))
 
 
-@pytest.mark.parametrize("name,n_random,n_planted", [("C2", 400, 100), ("C3", 300, 80), ("C5", 200, 40)])
-def test_full_size_sampled(name, n_random, n_planted):
+def whole_db_properties(g, what=""):
+    """Properties of a full-database result that need no oracle."""
+    fl = g["flags"]
+    assert np.all((fl & hg.HMM_VIT_RAN != 0) == (fl & hg.HMM_MSV_PASS != 0)), what
+    assert np.all((fl & hg.HMM_FWD_RAN != 0) == (fl & hg.HMM_VIT_PASS != 0)), what
+    assert np.all(g["vit"][(fl & hg.HMM_VIT_RAN) == 0] == np.iinfo(np.int32).min), what
+    assert np.all(np.isnan(g["fwd"][(fl & hg.HMM_FWD_RAN) == 0])), what
+    return float(np.mean((fl & hg.HMM_MSV_PASS) != 0))
+
+
+@pytest.mark.parametrize("name,stride", [("C2", 1), ("C3", 1), ("C5", 50)])
+def test_full_size(name, stride):
+    """The whole workload database in the benchmark's launch configuration
+    (default pipeline); every target (C2, C3) or every 50th target in
+    caller order (C5, where the oracle would need about six minutes for
+    all 2M) compared with the oracle, element by element."""
     w = gen.WORKLOADS[name]
     prof, db = full_db(name)
     calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
     g = run_gpu(prof, db.residues, db.offsets, calib, w.F)
-    idx = sample_ids(db, n_random, n_planted, seed=w.index)
-    res, off = sub_db(db, idx)
     t = time.time()
-    o = oracle_search(prof, res, off, calib, w.F)
+    if stride == 1:
+        idx = np.arange(db.n, dtype=np.int64)
+        o = oracle_search(prof, db.residues, db.offsets, calib, w.F)
+    else:
+        idx = np.arange(0, db.n, stride, dtype=np.int64)
+        res, off = sub_db(db, idx)
+        o = oracle_search(prof, res, off, calib, w.F)
+    announce(f"{name} oracle on {idx.size} of {db.n} targets in {time.time() - t:.1f}s")
     st = compare(g, o, idx, what=name)
-    announce(f"{name} full n={db.n} sampled {idx.size} (oracle {time.time() - t:.1f}s) ok {st}")
-    # whole-DB properties that need no oracle
-    fl = g["flags"]
-    assert np.all((fl & hg.HMM_VIT_RAN != 0) == (fl & hg.HMM_MSV_PASS != 0))
-    assert np.all((fl & hg.HMM_FWD_RAN != 0) == (fl & hg.HMM_VIT_PASS != 0))
-    assert np.all(g["vit"][(fl & hg.HMM_VIT_RAN) == 0] == np.iinfo(np.int32).min)
-    assert np.all(np.isnan(g["fwd"][(fl & hg.HMM_FWD_RAN) == 0]))
-    msv_pass = np.mean((fl & hg.HMM_MSV_PASS) != 0)
+    announce(f"{name} full n={db.n}: {idx.size} targets compared ok {st}")
+    msv_pass = whole_db_properties(g, name)
     assert 0.005 < msv_pass < 0.06, msv_pass
 
 
-def test_c4_profiles_sampled():
-    prof3, db = full_db("C3")
+def test_c4_group_full_size():
+    """C4 exactly as the benchmark times it: one hmm_search_group call of
+    the 64 profiles (M 50-400) against the full C3 database, each through
+    its own handle, on the current stream.  The group MSV kernels then
+    score about 120 targets per wave.  For every profile 150 random and 30
+    planted targets are compared with the oracle; for one profile of each
+    group size (1, 2 and 3 vectors per lane) every target is compared, bit
+    for bit, with a single hmm_search of the same profile, whose MSV kernel
+    the whole-database C3 test checks against the oracle."""
+    import torch
+    _, db = full_db("C3")
     profiles = gen.c4_profiles()
     F = gen.WORKLOADS["C3"].F
-    for p_i, prof in enumerate(profiles):
-        if p_i % 8 != 0:
-            continue
-        calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
-        g = run_gpu(prof, db.residues, db.offsets, calib, F)
-        idx = sample_ids(db, 60, 20, seed=100 + p_i)
+    t = time.time()
+    calibs = [oracle.calibrate(oracle.OracleProfile(p), nthreads=NTHREADS) for p in profiles]
+    announce(f"C4: {len(profiles)} profiles calibrated by the oracle in {time.time() - t:.1f}s")
+    Ps = [hg.Profile(p, *c) for p, c in zip(profiles, calibs)]
+    D = hg.Database(db.residues, db.offsets)
+    handles = [D] + [D.share() for _ in profiles[1:]]
+    announce(f"C4 group search: {len(Ps)} profiles, n={D.n}, residues={D.n_residues}")
+    outs = hg.search_group(Ps, handles, F)
+    torch.cuda.synchronize()
+    firsts = {}
+    for i, p in enumerate(profiles):
+        firsts.setdefault((p.M + 127) // 128, i)
+    for i, (p, c, out) in enumerate(zip(profiles, calibs, outs)):
+        g = {k: v.cpu().numpy() for k, v in out.items()}
+        idx = sample_ids(db, 150, 30, seed=200 + i)
         res, off = sub_db(db, idx)
-        o = oracle_search(prof, res, off, calib, F)
-        st = compare(g, o, idx, what=f"C4 profile {p_i} M={prof.M}")
-        announce(f"C4 profile {p_i} M={prof.M} ok {st}")
+        o = oracle_search(p, res, off, c, F)
+        st = compare(g, o, idx, what=f"C4 group profile {i} M={p.M}")
+        whole_db_properties(g, f"C4 profile {i}")
+        counts = g["counts"]
+        fl = g["flags"]
+        assert counts[0] == np.sum((fl & hg.HMM_MSV_PASS) != 0)
+        assert counts[2] == np.sum((fl & hg.HMM_VIT_PASS) != 0)
+        if i in firsts.values():
+            single = hg.alloc_results(D.n)
+            H = D.share()
+            hg.search(Ps[i], H, F, single)
+            torch.cuda.synchronize()
+            H.close()
+            s1 = {k: v.cpu().numpy() for k, v in single.items()}
+            for k in ("msv", "vit", "flags", "counts"):
+                assert np.array_equal(g[k], s1[k]), f"C4 group vs single {k} differ, profile {i} M={p.M}"
+            ran = ~np.isnan(s1["fwd"])
+            assert np.array_equal(ran, ~np.isnan(g["fwd"]))
+            assert np.array_equal(g["fwd"][ran], s1["fwd"][ran])
+            announce(f"C4 profile {i} M={p.M}: all {D.n} targets equal the single search")
+        announce(f"C4 group profile {i} M={p.M} ok {st}")
+    for H in handles:
+        H.close()
+    for P in Ps:
+        P.close()
 
 
 # ------------------------------------------------------------ edge cases
@@ -695,6 +748,60 @@ def test_search_group_matches_oracle_and_single_searches():
             ref = oracle_search(p, res, off, c, Fs[i])
             st = compare(g, ref, what=f"group M={p.M}")
             announce(f"group round {rnd} profile {i} M={p.M} ok {st}")
+    for H in handles:
+        H.close()
+    for P in Ps:
+        P.close()
+
+
+def test_search_group_several_targets_per_wave():
+    """Every group size of the group MSV kernels (4, 3 and 2 profiles at 1,
+    2 and 3 vectors per lane, plus a profile left alone) against 60,000
+    targets: the launch keeps 8,192 waves resident, so each wave scores
+    about seven targets in turn (its next-target prefetch, per-target
+    state reset and table reuse).  Every target of every profile is
+    compared with the oracle, and with the single hmm_search."""
+    import torch
+    Ms = [50, 90, 127, 64, 100, 128, 200, 255, 256, 383]
+    profs = [random_profile(M, 6100 + M, alpha=0.3, talpha=0.5) if i % 4 == 1 else gen.make_profile(M, 6000 + M)
+             for i, M in enumerate(Ms)]
+    rng = np.random.default_rng(6200)
+    base = gen.make_database(60000, 6201, None, 0.0)
+    seqs = [base.seq(i) for i in range(base.n)]
+    for p in profs:                            # planted homologs of every profile
+        for h in gen.sample_homologs(rng, p, 4):
+            L = int(h.size + rng.integers(0, 150))
+            s = gen.background_residues(rng, L)
+            o = int(rng.integers(0, L - h.size + 1))
+            s[o:o + h.size] = h
+            seqs.append(s)
+    order = rng.permutation(len(seqs))
+    seqs = [seqs[i] for i in order]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([x.size for x in seqs])
+    res = np.concatenate(seqs)
+    calibs = [oracle.calibrate(oracle.OracleProfile(p), nthreads=NTHREADS, n=100) for p in profs]
+    Ps = [hg.Profile(p, *c) for p, c in zip(profs, calibs)]
+    D = hg.Database(res, off)
+    handles = [D] + [D.share() for _ in profs[1:]]
+    F = (0.05, 0.01, 1.0)
+    announce(f"group of {len(profs)} profiles M={Ms} against n={D.n} residues={D.n_residues}")
+    outs = hg.search_group(Ps, handles, F)
+    torch.cuda.synchronize()
+    for i, (p, c, o) in enumerate(zip(profs, calibs, outs)):
+        g = {k: v.cpu().numpy() for k, v in o.items()}
+        ref = oracle_search(p, res, off, c, F)
+        st = compare(g, ref, what=f"group/multi-target M={p.M}")
+        single = hg.alloc_results(D.n)
+        H = D.share()
+        hg.search(Ps[i], H, F, single)
+        torch.cuda.synchronize()
+        H.close()
+        s1 = {k: v.cpu().numpy() for k, v in single.items()}
+        for k in ("msv", "vit", "flags", "counts"):
+            assert np.array_equal(g[k], s1[k]), f"group vs single {k} differ, profile {i} M={p.M}"
+        assert st["msv_ovf"] >= 1
+        announce(f"group/multi-target profile {i} M={p.M} ok {st}")
     for H in handles:
         H.close()
     for P in Ps:
