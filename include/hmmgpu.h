@@ -279,6 +279,23 @@ typedef struct {
 int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask,
                const hmm_decode_out *out, hmm_stream stream);
 
+/* hmm_decode for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * arguments, outputs and results are hmm_decode's; the per-wave scratch is
+ * a fixed array of 512 MiB that the library holds on every device it runs
+ * on (one copy per device, from the first call on that device until the
+ * process ends), so the call allocates nothing.  Slots are sized for the
+ * database's longest target; as many waves run as slots fit (a multiple of
+ * four): M = 734 with targets up to 1,000 residues gives 80 waves, M = 2,500
+ * with targets up to 5,000 residues 4.  Every call on one device shares
+ * the array and keeps no state in it between calls (nothing in it needs to
+ * start at zero), so calls that overlap on one device -- on different
+ * streams, or from different threads -- race and give undefined results;
+ * calls serialised on one stream are safe.  Errors: those of hmm_decode
+ * (HMM_ENOMEM aside), and HMM_ERANGE when four slots exceed the array. */
+int hmm_decode_static(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask,
+                      const hmm_decode_out *out, hmm_stream stream);
+
 /* ---------------------------------------------------------------- iteration
  *
  * A jackhmmer search is iterated: the hits it accepts are aligned to the

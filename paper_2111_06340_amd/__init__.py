@@ -28,7 +28,7 @@ HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float
 
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
             "hmm_count", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables",
-            "hmm_decode", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
+            "hmm_decode", "hmm_decode_static", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
             "hmm_probe_pk16", "hmm_profile_upload", "hmm_search", "hmm_search_group", "hmm_strerror")
 
 
@@ -96,6 +96,8 @@ def lib():
         L.hmm_rebuild.argtypes = [C.POINTER(hmm_profile_desc), vp, C.c_double, C.c_double, vp, vp, vp]
         L.hmm_decode.restype = C.c_int
         L.hmm_decode.argtypes = [vp, vp, vp, C.c_uint8, C.POINTER(hmm_decode_out), vp]
+        L.hmm_decode_static.restype = C.c_int
+        L.hmm_decode_static.argtypes = [vp, vp, vp, C.c_uint8, C.POINTER(hmm_decode_out), vp]
         L.hmm_db_info.restype = C.c_int
         L.hmm_db_info.argtypes = [vp, C.POINTER(i64), C.POINTER(i64), C.POINTER(i32)]
         L.hmm_db_stage_timing.restype = C.c_int
@@ -247,18 +249,30 @@ def hmm_search_group(profiles, dbs, Fs, outs, stream=None, bias_filter=False) ->
     _check(lib().hmm_search_group(P, D, T, R, int(n), _stream_handle(stream)), "hmm_search_group")
 
 
-def hmm_decode(profile: int, db: int, flags, mask: int, out: dict, stream=None) -> None:
-    """Enqueue posterior decoding.  `flags`: device uint8 tensor (caller
-    order) or None (decode every target); `out` maps dom (int32 [max_dom, 9])
-    and n_dom (int32 [1]) and optionally exp_dom / pp / aln to device
-    tensors."""
+def _decode_args(flags, out: dict):
     def ptr(k):
         v = out.get(k)
         return v.data_ptr() if v is not None else None
     o = hmm_decode_out(ptr("dom"), int(out["dom"].shape[0]), ptr("n_dom"), ptr("exp_dom"), ptr("pp"), ptr("aln"))
     fp = C.c_void_p(flags.data_ptr()) if flags is not None else C.c_void_p(0)
+    return fp, o
+
+
+def hmm_decode(profile: int, db: int, flags, mask: int, out: dict, stream=None) -> None:
+    """Enqueue posterior decoding.  `flags`: device uint8 tensor (caller
+    order) or None (decode every target); `out` maps dom (int32 [max_dom, 9])
+    and n_dom (int32 [1]) and optionally exp_dom / pp / aln to device
+    tensors."""
+    fp, o = _decode_args(flags, out)
     _check(lib().hmm_decode(C.c_void_p(profile), C.c_void_p(db), fp, int(mask) & 0xff, C.byref(o),
                             _stream_handle(stream)), "hmm_decode")
+
+
+def hmm_decode_static(profile: int, db: int, flags, mask: int, out: dict, stream=None) -> None:
+    """hmm_decode on the library's fixed device scratch (allocates nothing)."""
+    fp, o = _decode_args(flags, out)
+    _check(lib().hmm_decode_static(C.c_void_p(profile), C.c_void_p(db), fp, int(mask) & 0xff, C.byref(o),
+                                   _stream_handle(stream)), "hmm_decode_static")
 
 
 def _desc(prof, mu_msv=0.0, mu_vit=0.0, tau=0.0):
@@ -386,13 +400,14 @@ def search_group(profiles, dbs, F, outs=None, stream=None, bias_filter=False) ->
 
 
 def decode(profile: Profile, db: Database, flags=None, mask: int = HMM_FWD_PASS, max_dom: int | None = None,
-           pp: bool = False, aln: bool = False, stream=None) -> dict:
+           pp: bool = False, aln: bool = False, stream=None, static: bool = False) -> dict:
     """Posterior decoding of the targets whose flags hold `mask` (all targets
     when flags is None) on the current torch stream (or `stream`).  Returns
     device tensors: dom int32 [max_dom, 9] (fields DOMAIN_FIELDS; score and
     nexp are float32 bit patterns), n_dom int32 [1], exp_dom float32 [n]
     (NaN where not decoded), and pp float32 / aln int16 [n_residues] when
-    asked for (caller residue layout)."""
+    asked for (caller residue layout).  static=True runs hmm_decode_static
+    (the library's fixed device scratch; no device allocation)."""
     import torch
     if max_dom is None:
         max_dom = max(16, 4 * db.n)
@@ -406,7 +421,7 @@ def decode(profile: Profile, db: Database, flags=None, mask: int = HMM_FWD_PASS,
         out["aln"] = torch.full((db.n_residues,), -32768, dtype=torch.int16, device=dev)
     if stream is None:
         stream = torch.cuda.current_stream()
-    hmm_decode(profile.handle, db.handle, flags, mask, out, stream)
+    (hmm_decode_static if static else hmm_decode)(profile.handle, db.handle, flags, mask, out, stream)
     return out
 
 

@@ -33,11 +33,37 @@
 #include <algorithm>
 #include <climits>
 #include <cmath>
+#include <mutex>
 
 #include "hmm_device.h"
 #include "hmm_internal.h"
 
+// Decode scratch of hmm_decode_static: one copy per device, never freed.
+// Host code must not pass this name to a kernel (on the host it is only a
+// stand-in for the symbol); kernels get the address static_decode_scratch
+// looked up for the current device.
+static __device__ __align__(256) float scratch[hmmgpu::kStaticDecodeBytes / sizeof(float)];
+
 namespace hmmgpu {
+
+hipError_t static_decode_scratch(float **ptr) {
+  static std::mutex mu;
+  static float *addr[256] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 256) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = (float *)p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
+
 namespace {
 
 constexpr float kNegInf = -__builtin_inff();

@@ -1016,11 +1016,35 @@ int hmm_rebuild(const hmm_profile_desc *prior, const uint32_t *counts, double A,
   return HMM_OK;
 }
 
-int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask, const hmm_decode_out *out,
-               hmm_stream stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared body of hmm_decode and hmm_decode_static.  With `fixed` set the
+// wave slots live in the file-scope scratch array (kStaticDecodeBytes) and
+// nothing is allocated; otherwise in the database's decode scratch, grown
+// on demand.
+int decode_impl(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask, const hmm_decode_out *out,
+                hmm_stream stream, bool fixed) {
   if (!p || !db || !out) return fail(HMM_EINVAL, "NULL profile, db or out");
   if (!out->dom || !out->n_dom) return fail(HMM_EINVAL, "NULL dom or n_dom");
   if (out->max_dom < 0) return fail(HMM_EINVAL, "max_dom = %d", out->max_dom);
+  // one scratch slot per resident wave, four per workgroup
+  const int64_t slot_dw = decode_slot_dw(p->dev.Q32, db->max_len);
+  const size_t slot_bytes = (size_t)slot_dw * 4;
+  const size_t budget = fixed ? kStaticDecodeBytes : kDecodeScratchMax;
+  int64_t nslots = decode_max_waves(p->dev);
+  nslots = std::min<int64_t>(nslots, (int64_t)(budget / slot_bytes));
+  nslots = std::min<int64_t>(nslots, (db->n + 3) / 4 * 4);
+  nslots = nslots / 4 * 4;
+  if (db->n > 0 && nslots < 4) {
+    if (fixed)
+      return fail(HMM_ERANGE, "hmm_decode_static: 4 waves of %zu bytes (M = %d, longest target %d) exceed the "
+                  "%zu-byte static scratch", slot_bytes, p->dev.M, db->max_len, kStaticDecodeBytes);
+    return fail(HMM_ENOMEM, "decode scratch: %zu bytes per wave exceed the budget", slot_bytes);
+  }
+  float *base = nullptr;
+  if (fixed && db->n > 0) HIP_TRY(static_decode_scratch(&base), "hipGetSymbolAddress(scratch)");
   hipStream_t s = (hipStream_t)stream;
   // serialise with the searches on this database (lists, counters, scratch)
   if (db->searched) HIP_TRY(hipStreamWaitEvent(s, db->done, 0), "hipStreamWaitEvent");
@@ -1047,27 +1071,22 @@ int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t m
       db->lp_serial = p->serial;
       db->lp_F[0] = db->lp_F[1] = db->lp_F[2] = 1.0;
     }
-    // one scratch slot per resident wave, within the scratch budget
-    const int64_t slot_dw = decode_slot_dw(p->dev.Q32, db->max_len);
-    const size_t slot_bytes = (size_t)slot_dw * 4;
-    int64_t nslots = decode_max_waves(p->dev);
-    nslots = std::min<int64_t>(nslots, (int64_t)(kDecodeScratchMax / slot_bytes));
-    nslots = std::min<int64_t>(nslots, (db->n + 3) / 4 * 4);
-    nslots = nslots / 4 * 4;
-    if (nslots < 4) return fail(HMM_ENOMEM, "decode scratch: %zu bytes per wave exceed the budget", slot_bytes);
-    const size_t need = (size_t)nslots * slot_bytes;
-    if (need > db->dec_bytes) {
-      if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
-      if (db->dec_mem) HIP_TRY(hipFree(db->dec_mem), "hipFree(decode scratch)");
-      db->dec_mem = nullptr;
-      db->dec_bytes = 0;
-      hipError_t e = hipMalloc(&db->dec_mem, need);
-      if (e != hipSuccess)
-        return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "decode scratch of %zu bytes", need)
-                                        : fail_hip(e, "hipMalloc(decode scratch)");
-      db->dec_bytes = need;
+    if (!fixed) {
+      const size_t need = (size_t)nslots * slot_bytes;
+      if (need > db->dec_bytes) {
+        if (db->searched) HIP_TRY(hipEventSynchronize(db->done), "hipEventSynchronize");
+        if (db->dec_mem) HIP_TRY(hipFree(db->dec_mem), "hipFree(decode scratch)");
+        db->dec_mem = nullptr;
+        db->dec_bytes = 0;
+        hipError_t e = hipMalloc(&db->dec_mem, need);
+        if (e != hipSuccess)
+          return e == hipErrorOutOfMemory ? fail(HMM_ENOMEM, "decode scratch of %zu bytes", need)
+                                          : fail_hip(e, "hipMalloc(decode scratch)");
+        db->dec_bytes = need;
+      }
+      base = (float *)db->dec_mem;
     }
-    d.scratch = (float *)db->dec_mem;
+    d.scratch = base;
     d.slot_dw = slot_dw;
     d.nslots = (int32_t)nslots;
   }
@@ -1075,6 +1094,20 @@ int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t m
   HIP_TRY(hipEventRecord(db->done, s), "hipEventRecord");
   db->searched = true;
   return HMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hmm_decode(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask, const hmm_decode_out *out,
+               hmm_stream stream) {
+  return decode_impl(p, db, flags, mask, out, stream, false);
+}
+
+int hmm_decode_static(const hmm_profile *p, hmm_db *db, const uint8_t *flags, uint8_t mask,
+                      const hmm_decode_out *out, hmm_stream stream) {
+  return decode_impl(p, db, flags, mask, out, stream, true);
 }
 
 }  // extern "C"

@@ -130,6 +130,14 @@ int decode_max_waves(const DevProfile &p);
 // Enqueue the decode of the selected targets on `stream` (d.nslots waves).
 hipError_t launch_decode(const DevProfile &p, const DevDb &db, const DevDecode &d, hipStream_t stream);
 
+// Bytes of the decode scratch held in a file-scope device array, for the
+// entry point that allocates nothing (hmm_decode_static).
+constexpr size_t kStaticDecodeBytes = (size_t)512 << 20;
+
+// Device address of that array on the current device: looked up once per
+// device (hipGetSymbolAddress) and kept for the life of the process.
+hipError_t static_decode_scratch(float **ptr);
+
 // Forward and int32 rescore of long profiles with one workgroup of several
 // waves per target (hmm_coop.hip): coop_instance(Q) tells whether vectors
 // per lane Q have such an instance.
