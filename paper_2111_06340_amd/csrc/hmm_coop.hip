@@ -279,9 +279,8 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
       const bool pass = f > lp.fthr;
       const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
-      const int c = uni(db.perm[t]);
-      out.fwd[c] = f;
-      out.flags[c] = fl;
+      db.flags_sorted[t] = fl;
+      out.fwd[uni(db.perm[t])] = f;
       if (pass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
     }
   }

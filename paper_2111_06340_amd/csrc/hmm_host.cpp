@@ -536,7 +536,9 @@ static int attach_scratch(hmm_db *db) {
   const size_t n = (size_t)db->n;
   const size_t sz_u8 = al(n + 1), sz_i32 = al(n * 4 + 4);
   const size_t sz_lp = al(sizeof(LenParams) * ((size_t)db->max_len + 1));
-  const size_t o_flags = 0, o_lv = o_flags + sz_u8, o_lo = o_lv + sz_i32, o_lf = o_lo + sz_i32;
+  const size_t sz_i16 = al(n * 2 + 2);
+  const size_t o_flags = 0, o_msv = o_flags + sz_u8, o_lv = o_msv + sz_i16, o_lo = o_lv + sz_i32,
+               o_lf = o_lo + sz_i32;
   const size_t o_cnt = o_lf + sz_i32, o_lp = o_cnt + al(kMaxChunks * CNT_N * 4), total = o_lp + sz_lp;
   hipError_t e = hipMalloc(&db->smem, total);
   if (e != hipSuccess) {
@@ -561,6 +563,7 @@ static int attach_scratch(hmm_db *db) {
   uint8_t *b = (uint8_t *)db->smem;
   DevDb &dv = db->dev;
   dv.flags_sorted = b + o_flags;
+  dv.msv_sorted = (int16_t *)(b + o_msv);
   dv.list_vit = (int32_t *)(b + o_lv);
   dv.list_ovf = (int32_t *)(b + o_lo);
   dv.list_fwd = (int32_t *)(b + o_lf);

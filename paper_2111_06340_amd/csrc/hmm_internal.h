@@ -79,7 +79,8 @@ struct DevDb {
   const int64_t *start;         // [n] byte offset of each target (sorted order)
   const int32_t *len;           // [n]
   const int32_t *perm;          // [n] sorted index -> caller index
-  uint8_t *flags_sorted;        // [n] scratch
+  uint8_t *flags_sorted;        // [n] scratch: every stage's flags, sorted order
+  int16_t *msv_sorted;          // [n] scratch: MSV scores, sorted order
   int32_t *list_vit;            // [n] MSV survivors (sorted indices)
   int32_t *list_ovf;            // [n] int16 Viterbi overflows
   int32_t *list_fwd;            // [n] Viterbi survivors
@@ -172,6 +173,7 @@ inline DevDb chunk_of(const DevDb &d, int64_t a, int64_t b, int k) {
   c.perm += a;
   c.coff += a;
   c.flags_sorted += a;
+  c.msv_sorted += a;
   c.list_vit += a;
   c.list_ovf += a;
   c.list_fwd += a;

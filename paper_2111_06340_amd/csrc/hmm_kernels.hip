@@ -329,10 +329,21 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
       xJt = max(xJt, max(m - exit8, 0));
       return min(max(max(base, max(xJt - mv, 0)) - entry8, 0), ovf_line);
     };
+    // running maximum: a tree of 3-way maxima where Q allows (depth 2 at
+    // Q = 6 instead of a chain of 3), the same instruction count
     auto fold = [&](h16x2 &acc) {
+      if constexpr (Q % 3 == 0) {
+        h16x2 p[Q / 3];
 #pragma unroll
-      for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
-      if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
+        for (int j = 0; j < Q / 3; j++) p[j] = h2_max3(w[3 * j], w[3 * j + 1], w[3 * j + 2]);
+#pragma unroll
+        for (int j = 0; j + 1 < Q / 3; j += 2) acc = h2_max3(acc, p[j], p[j + 1]);
+        if ((Q / 3) & 1) acc = __builtin_elementwise_maximum(acc, p[Q / 3 - 1]);
+      } else {
+#pragma unroll
+        for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
+        if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
+      }
     };
     auto fired = [&]() { return any_lane(as_u(h2_max3(acc_o, as_h2(thr), acc_e)) != thr); };
     // byte offset of the next load's row inside the residue's table row:
@@ -353,11 +364,14 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
     };
     auto step = [&](int n) { lofs += 4 * n; };
     auto row = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int kind) -> bool {
+      // every add, then every maximum: no maximum waits on the add just
+      // before it (a dependent packed op needs a wait state on gfx950)
+      h16x2 t[Q];
 #pragma unroll
-      for (int q = 0; q < Q; q++) {
-        const h16x2 e = as_h2(c[q]);
-        w[q] = h2_max3(w[q] + e, e, as_h2(nbx));
-      }
+      for (int q = 0; q < Q; q++) t[q] = w[q] + as_h2(c[q]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < Q; q++) w[q] = h2_max3(t[q], as_h2(c[q]), as_h2(nbx));
       fold(kind == 1 ? acc_o : acc_e);
       pin();
       lds_wait(next);
@@ -462,7 +476,6 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   for (; t < n; t += nw) {
     const int L = Lnext;
     const uint8_t *x = db.res + snext;
-    const int cperm = db.perm[t];  // read now, used at the end
     const LenParams lp = db.lp[L];
     MsvResult res;
     if constexpr (DIAG) {
@@ -544,12 +557,10 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     }
     const bool pass = ovf || raw >= lp.thr8;
     const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
-    const int c = uni(cperm);
+    // sorted order: neighbouring waves score neighbouring targets, so these
+    // stores fill whole cache lines; results_kernel writes the caller's order
     db.flags_sorted[t] = fl;
-    out.flags[c] = fl;
-    out.msv[c] = (int16_t)raw;
-    out.vit[c] = INT32_MIN;
-    out.fwd[c] = __builtin_nanf("");
+    db.msv_sorted[t] = (int16_t)raw;
     // with the composition-bias filter on, MSV passes go to the filter's
     // list (the overflow list, unused until Viterbi) instead of Viterbi's
     if (pass) {
@@ -622,7 +633,6 @@ msv_group_kernel(MsvGroup<G> A) {
   for (; t < n; t += nw) {
     const int L = Lnext;
     const uint8_t *x = D0.res + snext;
-    const int cperm = D0.perm[t];
     int mv[G], base[G], xJt[G], Bx[G], ovf_line[G];
     bool ovf[G];
     uint32_t nbx[G], thr[G];
@@ -676,13 +686,17 @@ msv_group_kernel(MsvGroup<G> A) {
     };
     auto step = [&](int n) { lofs += 4 * n; };
     auto row = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int kind) -> bool {
+      // every add, then every maximum (as in the single-profile kernel)
+      h16x2 tt[G][Q];
 #pragma unroll
       for (int g = 0; g < G; g++)
 #pragma unroll
-        for (int q = 0; q < Q; q++) {
-          const h16x2 e = as_h2(c[g * Q + q]);
-          w[g][q] = h2_max3(w[g][q] + e, e, as_h2(nbx[g]));
-        }
+        for (int q = 0; q < Q; q++) tt[g][q] = w[g][q] + as_h2(c[g * Q + q]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < G; g++)
+#pragma unroll
+        for (int q = 0; q < Q; q++) w[g][q] = h2_max3(tt[g][q], as_h2(c[g * Q + q]), as_h2(nbx[g]));
 #pragma unroll
       for (int g = 0; g < G; g++) fold(kind == 1 ? acc_o[g] : acc_e[g], w[g]);
       pin();
@@ -763,7 +777,6 @@ msv_group_kernel(MsvGroup<G> A) {
       Lnext = uni(D0.len[t + nw]);
       snext = D0.start[t + nw];
     }
-    const int c = uni(cperm);
 #pragma unroll
     for (int g = 0; g < G; g++) {
       int raw = 255;
@@ -776,10 +789,7 @@ msv_group_kernel(MsvGroup<G> A) {
       const bool pass = ovf[g] || raw >= Dg.lp[L].thr8;
       const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf[g] ? HMM_MSV_OVF : 0);
       Dg.flags_sorted[t] = fl;
-      Og.flags[c] = fl;
-      Og.msv[c] = (int16_t)raw;
-      Og.vit[c] = INT32_MIN;
-      Og.fwd[c] = __builtin_nanf("");
+      Dg.msv_sorted[t] = (int16_t)raw;
       if (pass) {
         const bool bf = Og.bias_filter != 0;
         (bf ? Dg.list_ovf : Dg.list_vit)[wave_fetch_add(&Dg.counters[bf ? CNT_OVF : CNT_VIT], 1)] = t;
@@ -802,13 +812,11 @@ __global__ void __launch_bounds__(256) bias_kernel(DevProfile P, DevDb db, DevOu
     const LenParams lp = db.lp[L];
     const float beta = bias_score(P, db.res + db.start[t], L, lane);
     uint8_t fl = (uint8_t)uni(db.flags_sorted[t]);
-    const int c = uni(db.perm[t]);
-    const int raw = (int)out.msv[c];
+    const int raw = (int)uni((int)db.msv_sorted[t]);
     const bool go = (fl & HMM_MSV_OVF) || (float)raw - kS8f * fmaxf(beta, 0.0f) >= (float)lp.thr8;
     if (go) fl |= HMM_BIAS_PASS;
     db.flags_sorted[t] = fl;
-    out.flags[c] = fl;
-    if (out.bias) out.bias[c] = beta;
+    if (out.bias) out.bias[uni(db.perm[t])] = beta;
     if (go) db.list_vit[wave_fetch_add(&db.counters[CNT_VIT], 1)] = t;
   }
 }
@@ -999,10 +1007,8 @@ __global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(De
     const bool pass = r.ovf || r.raw >= lp.thr16;
     const uint8_t fl =
         (uint8_t)(uni(db.flags_sorted[t]) | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) | (r.ovf ? HMM_VIT_OVF : 0));
-    const int c = uni(db.perm[t]);
     db.flags_sorted[t] = fl;
-    out.flags[c] = fl;
-    out.vit[c] = r.raw;
+    out.vit[uni(db.perm[t])] = r.raw;
     if (r.ovf) db.list_ovf[wave_fetch_add(&db.counters[CNT_OVF], 1)] = t;
     if (pass) db.list_fwd[wave_fetch_add(&db.counters[CNT_FWD], 1)] = t;
   }
@@ -1241,9 +1247,8 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
     const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
     const bool pass = f > lp.fthr;
     const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
-    const int c = uni(db.perm[t]);
-    out.fwd[c] = f;
-    out.flags[c] = fl;
+    db.flags_sorted[t] = fl;
+    out.fwd[uni(db.perm[t])] = f;
     if (pass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
   }
 }
@@ -1266,6 +1271,23 @@ __global__ void export_counts(const int32_t *c, int nblocks, int64_t *counts) {
     }
     for (int i = 0; i < 4; i++) counts[i] = v[i];
   }
+}
+
+// Results in the caller's order, once every stage of a search is done: each
+// thread takes one caller index c and its sorted index iperm[c]; the flags
+// and MSV score come from the sorted arrays the stages wrote, and Viterbi
+// and Forward scores, written in caller order by those stages for the
+// targets they scored, get INT32_MIN and NaN where the stage did not run.
+// Reads of iperm and writes of every output are contiguous.
+__global__ void __launch_bounds__(256) results_kernel(DevDb db, DevOut out) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= db.n) return;
+  const int t = db.iperm[c];
+  const uint8_t fl = db.flags_sorted[t];
+  out.flags[c] = fl;
+  out.msv[c] = db.msv_sorted[t];
+  if (!(fl & HMM_VIT_RAN)) out.vit[c] = INT32_MIN;
+  if (!(fl & HMM_FWD_RAN)) out.fwd[c] = __builtin_nanf("");
 }
 
 // ============================================================================ launcher
@@ -1544,6 +1566,15 @@ hipError_t launch_tail(const DevProfile &P, const DevDb *chunk, int K, const Dev
     ok(hipStreamWaitEvent(s, y.tail_done, 0));
   if (e == hipSuccess && o.counts) {
     hipLaunchKernelGGL(export_counts, dim3(1), dim3(64), 0, s, (const int32_t *)chunk[0].counters, K, o.counts);
+    ok(hipGetLastError());
+  }
+  // chunk 0 starts at sorted index 0: its sorted arrays are the whole
+  // database's
+  DevDb all = chunk[0];
+  all.n = 0;
+  for (int k = 0; k < K; k++) all.n += chunk[k].n;
+  if (e == hipSuccess && all.n > 0) {
+    hipLaunchKernelGGL(results_kernel, dim3((unsigned)((all.n + 255) / 256)), dim3(256), 0, s, all, o);
     ok(hipGetLastError());
   }
   mark(4, s);
