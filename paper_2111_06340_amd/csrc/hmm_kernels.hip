@@ -243,14 +243,14 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
       load(RowK<1>{}, bb, code(w, 1));
       row(ba, bb, 0);
       load(RowK<2>{}, ba, code(w, 2));
-      if (row(bb, ba, 1)) {
+      if (__builtin_expect(row(bb, ba, 1), 0)) {
         stop = c0 + 4 * j + 1;
         return true;
       }
       load(RowK<3>{}, bb, code(w, 3));
       row(ba, bb, 0);
       load(RowK<4>{}, ba, code(wn, 0));
-      if (row(bb, ba, 1)) {
+      if (__builtin_expect(row(bb, ba, 1), 0)) {
         stop = c0 + 4 * j + 3;
         return true;
       }
@@ -295,10 +295,23 @@ struct MsvResult {
   bool ovf;
 };
 
-// Diagonal-layout MSV of one target.  Rows come in pairs and the trigger
-// test runs once per pair, on two running maxima (even rows, odd rows).
-// When a pair fires and its first row already reached the trigger, the
-// second row was computed with the old Bx; since xB only grows and
+// Diagonal-layout MSV of one target, in two passes.
+//
+// Fast pass: every row with the entry value of the first row and no test
+// at all; at the end, one test of the running maximum against the first
+// trigger value T (the smallest cell value that could change xB or
+// overflow).  If no cell reached T, xB never changed and no cell came near
+// the overflow line, so the pass is exactly the recurrence and its maximum
+// gives the score.  Background targets reach T with probability ~2^-19
+// (about 19 bits above the score distribution's location); homologs and
+// other high scorers do, and take the exact pass from the start.  Cells
+// past T may lose fp16 exactness or saturate to +inf in the fast pass:
+// rounding is monotone, so the maximum still compares at or above T.
+//
+// Exact pass: rows come in pairs and the trigger test runs once per pair,
+// on two running maxima (even rows, odd rows).  When a pair fires and its
+// first row already reached the trigger, the second row was computed with
+// the old Bx; since xB only grows and
 //   v'_k = max(v_{k-1} + E, Bx' + E, 0) = max(v_k, Bx' + E)   (Bx' >= Bx),
 // that row is corrected in place from its own table entries: in units of
 // the new Bx, w' = max(w + Bx - Bx', E).  Then the second row is tested
@@ -363,19 +376,64 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
       pin();
     };
     auto step = [&](int n) { lofs += 4 * n; };
-    auto row = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int kind) -> bool {
-      // every add, then every maximum: no maximum waits on the add just
-      // before it (a dependent packed op needs a wait state on gfx950)
+    // the rows' arithmetic: every add, then every maximum, so that no
+    // maximum waits on the add just before it (a dependent packed op needs
+    // a wait state on gfx950)
+    auto advance = [&](const uint32_t(&c)[Q]) {
       h16x2 t[Q];
 #pragma unroll
       for (int q = 0; q < Q; q++) t[q] = w[q] + as_h2(c[q]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int q = 0; q < Q; q++) w[q] = h2_max3(t[q], as_h2(c[q]), as_h2(nbx));
+    };
+    // at the end of every phase of P/2 rows the halves of each state dword
+    // swap diagonals
+    auto next_phase = [&](int stop) -> int {
+      const int r = stop + 1;
+      lofs = 4 * (r % kHalf);
+      if (lofs == 0) {
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+          const uint32_t u = as_u(w[q]);
+          w[q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
+        }
+      }
+      return r;
+    };
+    // ---- fast pass
+    bool exact = false;
+    {
+      auto frow = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int) -> bool {
+        advance(c);
+        fold(acc_e);
+        pin();
+        lds_wait(next);
+        return false;
+      };
+      int r = 0;
+      for (;;) {
+        int stop = 0;
+        const int limit = (r / kHalf + 1) * kHalf;
+        if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, step, frow)) break;
+        r = next_phase(stop);
+        if (r >= L) break;
+      }
+      exact = any_lane(as_u(__builtin_elementwise_maximum(acc_e, as_h2(thr))) != thr);
+    }
+    // ---- exact pass, from the first row again
+    if (__builtin_expect(exact, 0)) {
+#pragma unroll
+      for (int q = 0; q < Q; q++) w[q] = as_h2(nbx);
+      acc_e = acc_o = as_h2(nbx);
+      lofs = 0;
+    }
+    auto row = [&](const uint32_t(&c)[Q], uint32_t(&next)[Q], int kind) -> bool {
+      advance(c);
       fold(kind == 1 ? acc_o : acc_e);
       pin();
       lds_wait(next);
-      if (kind == 0 || !fired()) return false;
+      if (__builtin_expect(kind == 0 || !fired(), 1)) return false;
       if (kind == 2 || !any_lane(as_u(__builtin_elementwise_maximum(acc_e, as_h2(thr))) != thr)) return true;
       // the pair's first row reached the trigger: settle it, correct the second row
       const int m = wave_max_i32(h2_hmax(acc_e)) + Bx;
@@ -397,8 +455,7 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
       thr = trigger_thr();
       return fired();
     };
-    int r = 0;
-    for (;;) {
+    for (int r = 0; exact;) {
       int stop = 0;
       const int limit = (r / kHalf + 1) * kHalf;   // end of the current phase
       if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, step, row)) break;
@@ -419,16 +476,8 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
         nbx = splat(-Bx);
       }
       thr = trigger_thr();
-      r = stop + 1;
+      r = next_phase(stop);
       if (r >= L) break;
-      lofs = 4 * (r % kHalf);
-      if (lofs == 0) {  // the halves of every state dword swap diagonals
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          const uint32_t u = as_u(w[q]);
-          w[q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
-        }
-      }
     }
   }
   MsvResult res{255, ovf};
@@ -501,10 +550,7 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
 #pragma unroll
           for (int q = 0; q < Q; q++) c[q] = row[q * kWave];
         };
-        // One row.  Only w and the running maximum change here, on every row:
-        // a trigger stops the row driver; the caller then updates xJ and xB,
-        // re-bases w, and resumes at the next row.
-        auto row = [&](const uint32_t(&c)[Q]) -> bool {
+        auto advance = [&](const uint32_t(&c)[Q]) {
           const uint32_t sh = slot_up16(as_u(w[Q - 1]));
 #pragma unroll
           for (int q = Q - 1; q >= 0; q--) {
@@ -514,11 +560,34 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
 #pragma unroll
           for (int q = 0; q + 1 < Q; q += 2) acc = h2_max3(acc, w[q], w[q + 1]);
           if (Q & 1) acc = __builtin_elementwise_maximum(acc, w[Q - 1]);
-          return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr);
         };
+        auto fired = [&]() { return any_lane(as_u(__builtin_elementwise_maximum(acc, as_h2(thr))) != thr); };
         uint32_t ca[Q], cb[Q];
+        // Fast pass, as in the diagonal layout: no test until the end; if
+        // no cell reached the first trigger value, the pass is exact.
+        {
+          auto frow = [&](const uint32_t(&c)[Q]) -> bool {
+            advance(c);
+            return false;
+          };
+          int stop = 0;
+          (void)drive_rows(x, L, 0, 0, stop, lane, ca, cb, load, frow);
+        }
+        const bool exact = fired();
+        if (__builtin_expect(exact, 0)) {   // exact pass from the first row again
+#pragma unroll
+          for (int q = 0; q < Q; q++) w[q] = as_h2(nbx);
+          acc = as_h2(nbx);
+        }
+        // One row of the exact pass.  Only w and the running maximum change
+        // here, on every row: a trigger stops the row driver; the caller then
+        // updates xJ and xB, re-bases w, and resumes at the next row.
+        auto row = [&](const uint32_t(&c)[Q]) -> bool {
+          advance(c);
+          return __builtin_expect(fired(), 0);
+        };
         int r = 0;
-        for (;;) {
+        for (; exact;) {
           int stop = 0;
           if (!drive_rows(x, L, r, 0, stop, lane, ca, cb, load, row)) break;
           const int m = wave_max_i32(h2_hmax(acc)) + Bx;      // largest cell so far
@@ -685,8 +754,8 @@ msv_group_kernel(MsvGroup<G> A) {
       pin();
     };
     auto step = [&](int n) { lofs += 4 * n; };
-    auto row = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int kind) -> bool {
-      // every add, then every maximum (as in the single-profile kernel)
+    // every add, then every maximum (as in the single-profile kernel)
+    auto advance = [&](const uint32_t(&c)[G * Q]) {
       h16x2 tt[G][Q];
 #pragma unroll
       for (int g = 0; g < G; g++)
@@ -697,6 +766,60 @@ msv_group_kernel(MsvGroup<G> A) {
       for (int g = 0; g < G; g++)
 #pragma unroll
         for (int q = 0; q < Q; q++) w[g][q] = h2_max3(tt[g][q], as_h2(c[g * Q + q]), as_h2(nbx[g]));
+    };
+    auto next_phase = [&](int stop) -> int {
+      const int r = stop + 1;
+      lofs = 4 * (r % kHalf);
+      if (lofs == 0) {  // the halves of every state dword swap diagonals
+#pragma unroll
+        for (int g = 0; g < G; g++)
+#pragma unroll
+          for (int q = 0; q < Q; q++) {
+            const uint32_t u = as_u(w[g][q]);
+            w[g][q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
+          }
+      }
+      return r;
+    };
+    bool all_ovf0 = true;
+#pragma unroll
+    for (int g = 0; g < G; g++) all_ovf0 = all_ovf0 && ovf[g];
+    // Fast pass (as in msv_target_diag): every profile without tests; if
+    // none reached its first trigger value, the pass is exact for all.
+    bool exact = false;
+    if (!all_ovf0) {
+      auto frow = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int) -> bool {
+        advance(c);
+#pragma unroll
+        for (int g = 0; g < G; g++) fold(acc_e[g], w[g]);
+        pin();
+        lds_wait(next);
+        return false;
+      };
+      for (int r = 0;;) {
+        int stop = 0;
+        const int limit = (r / kHalf + 1) * kHalf;
+        if (!drive_pairs(x, L, r, limit, stop, lane, ca, cb, load, step, frow)) break;
+        r = next_phase(stop);
+        if (r >= L) break;
+      }
+      uint64_t any = 0;
+#pragma unroll
+      for (int g = 0; g < G; g++)
+        any |= __builtin_amdgcn_ballot_w64(as_u(__builtin_elementwise_maximum(acc_e[g], as_h2(thr[g]))) != thr[g]);
+      exact = any != 0;
+    }
+    if (__builtin_expect(exact, 0)) {   // exact pass for every profile, from the first row again
+#pragma unroll
+      for (int g = 0; g < G; g++) {
+#pragma unroll
+        for (int q = 0; q < Q; q++) w[g][q] = as_h2(nbx[g]);
+        acc_e[g] = acc_o[g] = as_h2(nbx[g]);
+      }
+      lofs = 0;
+    }
+    auto row = [&](const uint32_t(&c)[G * Q], uint32_t(&next)[G * Q], int kind) -> bool {
+      advance(c);
 #pragma unroll
       for (int g = 0; g < G; g++) fold(kind == 1 ? acc_o[g] : acc_e[g], w[g]);
       pin();
@@ -706,7 +829,7 @@ msv_group_kernel(MsvGroup<G> A) {
 #pragma unroll
       for (int g = 0; g < G; g++)
         any |= __builtin_amdgcn_ballot_w64(as_u(h2_max3(acc_o[g], as_h2(thr[g]), acc_e[g])) != thr[g]);
-      if (!any) return false;
+      if (__builtin_expect(!any, 1)) return false;
       bool stop = false;
 #pragma unroll
       for (int g = 0; g < G; g++) {
@@ -738,8 +861,7 @@ msv_group_kernel(MsvGroup<G> A) {
       }
       return stop;
     };
-    int r = 0;
-    for (;;) {
+    for (int r = 0; exact;) {
       bool all_ovf = true;
 #pragma unroll
       for (int g = 0; g < G; g++) all_ovf = all_ovf && ovf[g];
@@ -760,18 +882,8 @@ msv_group_kernel(MsvGroup<G> A) {
         if (nBx != Bx[g]) rebase(g, nBx);
         thr[g] = trigger_thr(g);
       }
-      r = stop + 1;
+      r = next_phase(stop);
       if (r >= L) break;
-      lofs = 4 * (r % kHalf);
-      if (lofs == 0) {  // the halves of every state dword swap diagonals
-#pragma unroll
-        for (int g = 0; g < G; g++)
-#pragma unroll
-          for (int q = 0; q < Q; q++) {
-            const uint32_t u = as_u(w[g][q]);
-            w[g][q] = as_h2(__builtin_amdgcn_alignbit(u, u, 16));
-          }
-      }
     }
     if (t + nw < n) {
       Lnext = uni(D0.len[t + nw]);
