@@ -375,7 +375,7 @@ __device__ __forceinline__ MsvResult msv_target_diag(const DevProfile &P, const 
       lds_load_tid<4 * decltype(k)::v>(c, a * kRowB, uni(lofs));
       pin();
     };
-    auto step = [&](int n) { lofs += 4 * n; };
+    auto step = [&](int n) { lofs = uni(lofs + 4 * n); };   // kept uniform: an SGPR
     // the rows' arithmetic: every add, then every maximum, so that no
     // maximum waits on the add just before it (a dependent packed op needs
     // a wait state on gfx950)
@@ -753,7 +753,7 @@ msv_group_kernel(MsvGroup<G> A) {
       lds_load_group<4 * decltype(k)::v, Q, G>(c, a * (G * kRowB), uni(lofs));
       pin();
     };
-    auto step = [&](int n) { lofs += 4 * n; };
+    auto step = [&](int n) { lofs = uni(lofs + 4 * n); };   // kept uniform: an SGPR
     // every add, then every maximum (as in the single-profile kernel)
     auto advance = [&](const uint32_t(&c)[G * Q]) {
       h16x2 tt[G][Q];
@@ -1037,9 +1037,12 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     }
     uint32_t dc = kNegNeg;
     const uint32_t din = slot_up16(M[Q - 1]);
+    // the floor joins the M->D term, which does not depend on the chain:
+    // the chain itself is one add and one maximum per vector
 #pragma unroll
     for (int q = 0; q < Q; q++) {
-      D[q] = i16_max(i16_max(i16_adds(q ? M[q - 1] : din, trv(TR_MDIN, q)), i16_adds(dc, tr[TR_DDIN][q])), tau2);
+      const uint32_t md = i16_max(i16_adds(q ? M[q - 1] : din, trv(TR_MDIN, q)), tau2);
+      D[q] = i16_max(md, i16_adds(dc, tr[TR_DDIN][q]));
       dc = D[q];
     }
     // A chain can cross into the next slot only from a slot whose last
@@ -1061,7 +1064,7 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
         if (!moved) break;
       }
     }
-    if (any_lane(i16_max(accM, tm1) != tm1)) {
+    if (__builtin_expect(any_lane(i16_max(accM, tm1) != tm1), 0)) {
       const int m = wave_max_i32(hmax16(accM));
       if (m >= 32767) return true;
       xJt = max(xJt, sat16(m + ej));
