@@ -18,13 +18,15 @@
 //       when nothing enters its own first cell (last cell's M through M->D
 //       and A through D->D into that cell);
 //   ml, il, al: its last cell's M, I and A;
-//   Forward: es, the sum of its M + A (its part of E);
+//   Forward: once per wave, the sum of its cells' M g over every lane (its
+//   part of E; the exit weight g of a cell carries the deletes it reaches,
+//   see hmm_profile_upload);
 //   rescore: its running maximum if it crossed the trigger line.
 // After the barrier every wave composes its lane's W segment maps
 // (x_out = xo + p x_in: affine for Forward, max-plus for the rescore), chains
 // the lanes with a DPP prefix scan, and so knows the value x_j entering every
 // segment j of its lane.  Its own delete cells are then D_q = A_q (+) P_q
-// x_w; Forward's E is the wave sum of sum_j (es_j + S_j x_j); the left
+// x_w; Forward's E is the sum of the W published parts; the left
 // neighbour of its first cell for the next row (segment w-1 of the lane, or
 // segment W-1 of the previous lane through a DPP shift) is (ml, il,
 // al (+) P_last x).  All waves hold the same special states and take the
@@ -124,7 +126,7 @@ __device__ __forceinline__ int next_target(int32_t *work, int *slot) {
 template <int QW, int W>
 __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db, DevOut out) {
   constexpr int Q = QW * W;
-  __shared__ float sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave], ses[2][W][kWave];
+  __shared__ float sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave], ses[2][W];
   __shared__ int slot;
   const int lane = threadIdx.x & 63;
   const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -143,10 +145,15 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
     if (j + 1 < W) return trg[(plane * Q + (j + 1) * QW) * kWave];
     return lane + 1 < kWave ? trg[plane * Q * kWave + 1] : 0.0f;
   };
+  // exit weights of this wave's cells: a row's E = sum over cells of M g
+  // (the delete cells' part included through g)
+  float gx[QW];
+#pragma unroll
+  for (int q = 0; q < QW; q++) gx[q] = trg[(TR_EXIT * Q + q0 + q) * kWave];
   // pre[q]: product of DD over this wave's cells 1..q; per segment j of the
   // lane: pl[j] the product over its cells 1..QW-1, pj[j] = pl[j] DD' (its
-  // map's slope), sj[j] the sum of its pre[q]; the lane map slope's scan steps
-  float pre[QW], pl[W], pj[W], sj[W], ps[6];
+  // map's slope); the lane map slope's scan steps
+  float pre[QW], pl[W], pj[W], ps[6];
   {
     float acc = 1.0f;
 #pragma unroll
@@ -157,14 +164,10 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
     float lanep = 1.0f;
 #pragma unroll
     for (int j = 0; j < W; j++) {
-      float a = 1.0f, sum = 0.0f;
-      for (int q = 0; q < QW; q++) {
-        if (q) a *= trg[(TR_DDIN * Q + j * QW + q) * kWave];
-        sum += a;
-      }
+      float a = 1.0f;
+      for (int q = 1; q < QW; q++) a *= trg[(TR_DDIN * Q + j * QW + q) * kWave];
       pl[j] = a;
       pj[j] = a * into_next(TR_DDIN, j);
-      sj[j] = sum;
       lanep *= pj[j];
     }
     affine_steps(lanep, ps);
@@ -205,31 +208,34 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
         M[q] = em[q] * sm;
         I[q] = em[QW + q] * si;
       }
-      // delete chain with nothing entering the segment (A), and its sums
-      float es = M[0];
+      // this wave's part of E (every lane's segment), reduced before the
+      // barrier: it needs no delete value, so its cross-lane sum overlaps
+      // the delete chain below instead of following the barrier
+      float es = 0.0f;
+#pragma unroll
+      for (int q = 0; q < QW; q++) es = fmaf(M[q], gx[q], es);
+      es = wave_sum_f(es);
+      // delete chain with nothing entering the segment (A)
       D[0] = 0.0f;
 #pragma unroll
-      for (int q = 1; q < QW; q++) {
-        D[q] = fmaf(M[q - 1], tr[TR_MDIN][q], D[q - 1] * tr[TR_DDIN][q]);
-        es += M[q] + D[q];
-      }
+      for (int q = 1; q < QW; q++) D[q] = fmaf(M[q - 1], tr[TR_MDIN][q], D[q - 1] * tr[TR_DDIN][q]);
       sxo[par][w][lane] = fmaf(M[QW - 1], mdn, D[QW - 1] * ddn);
       sml[par][w][lane] = M[QW - 1];
       sil[par][w][lane] = I[QW - 1];
       sal[par][w][lane] = D[QW - 1];
-      ses[par][w][lane] = es;
+      if (lane == 0) ses[par][w] = es;
       __syncthreads();
       // the values entering the lane's segments
       float a = 0.0f;
 #pragma unroll
       for (int j = 0; j < W; j++) a = fmaf(pj[j], a, sxo[par][j][lane]);
       float x = lane_up_f(affine_scan(a, ps));
-      float xw = 0.0f, xn = 0.0f, e = 0.0f;
+      float xw = 0.0f, xn = 0.0f, E = 0.0f;
 #pragma unroll
       for (int j = 0; j < W; j++) {
         if (j == w) xw = x;
         if (j == nb) xn = x;
-        e += fmaf(sj[j], x, ses[par][j][lane]);
+        E += ses[par][j];
         x = fmaf(pj[j], x, sxo[par][j][lane]);
       }
 #pragma unroll
@@ -244,7 +250,7 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
         pD = lane_up_f(pD);
       }
       par ^= 1;
-      const float E = wave_sum_f(e);
+      E = __builtin_bit_cast(float, uni(__builtin_bit_cast(int, E)));
       J = fmaf(J, loop, 0.5f * E);
       C = fmaf(C, loop, 0.5f * E);
       N = N * loop;
@@ -380,15 +386,18 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
       }
     };
     auto row = [&](const int(&em)[2 * QW]) -> bool {
-      // every state and table value is >= -2^30, so each add fits in int32
-      // and the floors inside a maximum merge into one; the value shifted
-      // into cell 0 is irrelevant, as every transition into it is kNeg32
+      // saturating adds and two floors, as in the one-wave kernel: a match
+      // or insert value below -2^30 only meets maxima with a term >= -2^30
+      // (xBe, the insert floor, tau); the value shifted into cell 0 is
+      // irrelevant, as every transition into it is kNeg32
 #pragma unroll
       for (int q = QW - 1; q >= 0; q--) {
         const int pm = q ? M[q - 1] : pM, pi = q ? I[q - 1] : pI, pd = q ? D[q - 1] : pD;
-        const int m = max(max(xbe, pm + tr[TR_MMIN][q]), max(pi + tr[TR_IMIN][q], pd + tr[TR_DMIN][q]));
-        const int mn = fl32(m + em[q]);
-        const int in = fl32(max(max(M[q] + tr[TR_MI][q], I[q] + tr[TR_II][q]), kNeg32) + em[QW + q]);
+        const int m = max(max(xbe, sadd32(pm, tr[TR_MMIN][q])),
+                          max(sadd32(pi, tr[TR_IMIN][q]), sadd32(pd, tr[TR_DMIN][q])));
+        const int mn = sadd32(m, em[q]);
+        const int in =
+            sadd32(max(max(sadd32(M[q], tr[TR_MI][q]), sadd32(I[q], tr[TR_II][q])), kNeg32), em[QW + q]);
         accM = max(accM, mn);
         M[q] = mn;
         I[q] = in;
@@ -396,8 +405,9 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
       // delete chain with only the floor entering the segment
       D[0] = tau;
 #pragma unroll
-      for (int q = 1; q < QW; q++) D[q] = max(max(M[q - 1] + tr[TR_MDIN][q], D[q - 1] + tr[TR_DDIN][q]), tau);
-      sxo[par][w][lane] = max(max(M[QW - 1] + mdn, D[QW - 1] + ddn), tau);
+      for (int q = 1; q < QW; q++)
+        D[q] = max(max(sadd32(M[q - 1], tr[TR_MDIN][q]), D[q - 1] + tr[TR_DDIN][q]), tau);
+      sxo[par][w][lane] = max(max(sadd32(M[QW - 1], mdn), D[QW - 1] + ddn), tau);
       sml[par][w][lane] = M[QW - 1];
       sil[par][w][lane] = I[QW - 1];
       sal[par][w][lane] = D[QW - 1];

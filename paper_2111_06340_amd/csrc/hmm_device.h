@@ -17,6 +17,8 @@ typedef short i16x2 __attribute__((ext_vector_type(2)));
 constexpr uint32_t kNegNeg = 0x80008000u;  // two int16 -32768
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+// Saturating int32 add (one v_add_i32 with clamp): no sum can wrap.
+__device__ __forceinline__ int sadd32(int a, int b) { return __builtin_elementwise_add_sat(a, b); }
 
 // Control flow in these kernels is wave-uniform by construction, and the
 // cross-lane operations (DPP, readlane, ballot, bpermute) rely on every lane

@@ -292,7 +292,7 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
   const size_t n_vtr = (size_t)TR_N * Q8 * kWave;
   const size_t n_w32emit = (size_t)kAlpha * 2 * Q32 * kWave;
   const size_t n_w32tr = (size_t)TR_N * Q32 * kWave;
-  const size_t n_ftr = (size_t)(TR_N + 2) * Q32 * kWave;
+  const size_t n_ftr = (size_t)(TR_N + 3) * Q32 * kWave;
   const size_t total = n_msv + n_vemit + n_vtr + n_w32emit + n_w32tr + n_w32emit + n_ftr;
   std::vector<uint32_t> h(total, 0);
   uint32_t *h_msv = h.data();
@@ -402,6 +402,23 @@ int hmm_profile_upload(const hmm_profile_desc *d, hmm_stream stream, hmm_profile
     for (int q = Q32 - 1; q >= 0; q--) {
       h_ftr[(size_t)TR_SUF * Q32 * kWave + pk_index(q, l)] = (float)acc;
       acc *= tr_prob(TR_DDIN, w_cell(Q32, q, l));
+    }
+  }
+
+  // Exit weights.  A row's delete cells are sums over the same row's match
+  // cells: D_c = sum_{j<c} M_j MDIN(j+1) DDIN(j+2) ... DDIN(c), so the row's
+  // E = sum_c (M_c + D_c) = sum_j M_j g_j with
+  //   g_j = 1 + MDIN(j+1) S_{j+1},  S_k = 1 + DDIN(k+1) S_{k+1},
+  // the total probability of leaving M_j for E directly or through the
+  // delete states it reaches (zero transitions past the last node end the
+  // sums).  fp64, cells P-1 down to 0.
+  {
+    const int P32 = Q32 * kWave;
+    double S = 1.0;   // S_{c+1} while cell c is visited
+    for (int c = P32 - 1; c >= 0; c--) {
+      const double g = 1.0 + (c + 1 < P32 ? tr_prob(TR_MDIN, c + 1) * S : 0.0);
+      h_ftr[(size_t)TR_EXIT * Q32 * kWave + pk_index(c % Q32, c / Q32)] = c < M ? (float)g : 0.0f;
+      S = 1.0 + (c + 1 < P32 ? tr_prob(TR_DDIN, c + 1) * S : 0.0);
     }
   }
 

@@ -58,12 +58,14 @@ struct DevProfile {
   const int32_t *v32_emit;      // [20][2][Q32][64]
   const int32_t *v32_tr;        // [TR_N][Q32][64]
   const float *f_emit;          // [20][2][Q32][64] odds e/f, i/f
-  // [TR_N + 2][Q32][64]: probabilities; plane TR_PRE: D-chain products
+  // [TR_N + 3][Q32][64]: probabilities; plane TR_PRE: D-chain products
   // prod_{j<=q} DDIN(lane*Q + j); plane TR_SUF: prod_{j=q+1}^{Q} DDIN(lane*Q + j)
-  // (the last factor belongs to the next lane's first cell; 0 past the end)
+  // (the last factor belongs to the next lane's first cell; 0 past the end);
+  // plane TR_EXIT: exit weight g_c of cell c (see hmm_profile_upload), so
+  // that a row's E = sum_c M_c g_c
   const float *f_tr;
 };
-enum { TR_PRE = TR_N, TR_SUF = TR_N + 1 };
+enum { TR_PRE = TR_N, TR_SUF = TR_N + 1, TR_EXIT = TR_N + 2 };
 
 // Counters in the database scratch (device int32).
 enum {

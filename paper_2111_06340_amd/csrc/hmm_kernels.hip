@@ -1179,16 +1179,21 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
       const int msh = lane_up_i(M[Q - 1]);
       const int ish = lane_up_i(I[Q - 1]);
       const int dsh = lane_up_i(D[Q - 1]);
-      // Every state and table value is >= -2^30, so each add fits in int32,
-      // and the floor of every add inside a maximum is one floor of the
-      // maximum: max(fl32(a), fl32(b)) = max(a, b, -2^30).  The M maximum
-      // includes xBe >= -2^30 and needs no floor at all.
+      // The oracle floors every add at -2^30.  Here every add saturates
+      // (v_add_i32 clamp), so no sum wraps, and only two floors remain: the
+      // insert maximum's -2^30 and the delete floor tau.  A value below
+      // -2^30 (after an impossible emission or transition) reaches only
+      // maxima that hold a term >= -2^30 -- the match maximum includes xBe,
+      // the insert maximum -2^30, the delete maximum tau -- so it is dropped
+      // there exactly as the oracle's floored -2^30 is, and every state
+      // that is not below -2^30 equals the oracle's.
 #pragma unroll
       for (int q = Q - 1; q >= 0; q--) {
         const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-        const int m = max(max(xbe, pm + TR(TR_MMIN, q)), max(pi + TR(TR_IMIN, q), pd + TR(TR_DMIN, q)));
-        const int mn = fl32(m + em[q]);
-        const int in = fl32(max(max(M[q] + TR(TR_MI, q), I[q] + TR(TR_II, q)), kNeg32) + em[Q + q]);
+        const int m = max(max(xbe, sadd32(pm, TR(TR_MMIN, q))),
+                          max(sadd32(pi, TR(TR_IMIN, q)), sadd32(pd, TR(TR_DMIN, q))));
+        const int mn = sadd32(m, em[q]);
+        const int in = sadd32(max(max(sadd32(M[q], TR(TR_MI, q)), sadd32(I[q], TR(TR_II, q))), kNeg32), em[Q + q]);
         accM = max(accM, mn);
         M[q] = mn;
         I[q] = in;
@@ -1197,7 +1202,7 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
       const int din = lane_up_i(M[Q - 1]);
 #pragma unroll
       for (int q = 0; q < Q; q++) {
-        D[q] = max(max((q ? M[q - 1] : din) + TR(TR_MDIN, q), dc + TR(TR_DDIN, q)), tau);
+        D[q] = max(max(sadd32(q ? M[q - 1] : din, TR(TR_MDIN, q)), sadd32(dc, TR(TR_DDIN, q))), tau);
         dc = D[q];
       }
       for (int it = 0; it < kWave; it++) {
@@ -1257,11 +1262,13 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
   __syncthreads();
   const float *emit = (const float *)ldsf + lane;
   const float *trp = P.f_tr + lane;
-  float tr[TR_N + 1][Q];
+  float tr[TR_N + 1][Q], gx[Q];
 #pragma unroll
   for (int k = 0; k <= TR_N; k++)
 #pragma unroll
     for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
+#pragma unroll
+  for (int q = 0; q < Q; q++) gx[q] = trp[(TR_EXIT * Q + q) * kWave];   // exit weights: E = sum M g
   auto TR = [&](int k, int q) -> float { return tr[k][q]; };
   // P part of the delete-chain scan: the lane's P before each of the six steps
   float pstep[6];
@@ -1302,6 +1309,7 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
       const float ish = lane_up_f(I[Q - 1]);
       const float dsh = lane_up_f(D[Q - 1]);
       const float bent = B * entry_p;
+      float part = 0.0f;   // this lane's part of E: sum of M g (deletes included through g)
 #pragma unroll
       for (int q = Q - 1; q >= 0; q--) {
         const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
@@ -1309,6 +1317,7 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
         const float si = fmaf(M[q], TR(TR_MI, q), I[q] * TR(TR_II, q));
         M[q] = em[q] * sm;
         I[q] = em[Q + q] * si;
+        part = fmaf(M[q], gx[q], part);
       }
       const float din = lane_up_f(M[Q - 1]);
       float dc = 0.0f;
@@ -1325,12 +1334,8 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
       sa = fmaf(pstep[4], dpp_f<kRowBcast15, 0xa>(sa, 0.0f), sa);
       sa = fmaf(pstep[5], dpp_f<kRowBcast31, 0xc>(sa, 0.0f), sa);
       const float carry = lane_up_f(sa);
-      float part = 0.0f;
 #pragma unroll
-      for (int q = 0; q < Q; q++) {
-        D[q] = fmaf(carry, TR(TR_N, q), D[q]);
-        part += M[q] + D[q];
-      }
+      for (int q = 0; q < Q; q++) D[q] = fmaf(carry, TR(TR_N, q), D[q]);
       const float E = wave_sum_f(part);
       J = fmaf(J, loop, 0.5f * E);
       C = fmaf(C, loop, 0.5f * E);

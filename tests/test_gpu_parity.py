@@ -446,6 +446,44 @@ def test_degenerate_and_extreme_profiles():
     assert rng is not None
 
 
+@pytest.mark.parametrize("M", [734, 1000, 2500])
+def test_zero_probabilities_in_long_profiles(M):
+    """Impossible insert emissions (probability exactly 0: score minus
+    infinity), zero transitions and near-impossible match emissions
+    (1e-30; a match probability of 0 is rejected at upload) in profiles of
+    12, 16 and 40 vectors per lane (the one-wave int32 rescore and Forward,
+    and the cooperative ones), against homologs that overflow int16 and
+    targets full of the rare residue: the int32 rescore meets insert values
+    far below its -2^30 floor and must still equal the oracle."""
+    rng = np.random.default_rng(M)
+    prof = gen.make_profile(M, 3100 + M)
+    match, insert, trans = prof.match.copy(), prof.insert.copy(), prof.trans.copy()
+    for k in rng.choice(M, size=M // 5, replace=False):       # residue 0 near-impossible at a fifth of the nodes
+        match[k, 0] = 1e-30
+        match[k] /= match[k].sum()
+    for k in rng.choice(M - 1, size=M // 10, replace=False):  # inserts that emit one residue only
+        insert[k] = 0.0
+        insert[k, int(rng.integers(1, 20))] = 1.0
+    for k in rng.choice(M - 1, size=M // 10, replace=False):  # no M->D, no I->I, no D->D at some nodes
+        trans[k] = [0.9, 0.1, 0.0, 1.0, 0.0, 1.0, 0.0]
+    prof = gen.Profile(M, prof.bg, match, insert, trans)
+    homs = gen.sample_homologs(rng, prof, 4)
+    seqs = [np.concatenate([gen.background_residues(rng, 30), h, gen.background_residues(rng, 20)]) for h in homs]
+    seqs += [np.zeros(400, np.uint8), gen.background_residues(rng, 900)]
+    mixed = gen.background_residues(rng, 1500)
+    mixed[::3] = 0
+    seqs.append(mixed)
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([x.size for x in seqs])
+    res = np.concatenate(seqs)
+    F = (1.0, 1.0, 1.0)
+    g = run_gpu(prof, res, off, (0.0, 0.0, 0.0), F)
+    o = oracle_search(prof, res, off, (0.0, 0.0, 0.0), F)
+    st = compare(g, o, what=f"zero probabilities M={M}")
+    assert st["vit_ovf"] >= 1
+    announce(f"zero probabilities M={M} ok {st}")
+
+
 def _rare_residue_profile(M, seed):
     """Residue 0 has background frequency 1e-9 and match probability 1/2 at
     every node: each match of it scores about 14,400 units (1/500 bit), so
