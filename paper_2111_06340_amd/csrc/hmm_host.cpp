@@ -680,7 +680,9 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   // next MSV and more chunks only add MSV launches.  On a 707M-residue one
   // (M = 2500) four chunks beat two by 2.5 %: its long targets' rescore and
   // Forward run with one workgroup per target and leave room beside MSV.
-  db->chunks = n_res >= ((int64_t)512 << 20) ? 4 : n_res >= ((int64_t)8 << 20) ? 2 : 1;
+  // Below about 128 Mi residues one chunk is better (69M residues, M = 256:
+  // 2.55 against 2.63 ms): the MSV kernels are too short to hide a tail.
+  db->chunks = n_res >= ((int64_t)512 << 20) ? 4 : n_res >= ((int64_t)128 << 20) ? 2 : 1;
   db->data = new (std::nothrow) hmm_db_data();
   if (!db->data) {
     delete db;
