@@ -357,10 +357,12 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
       // where the registers are better spent on the row itself.
       constexpr bool kPrefetch = Q <= 12;
       float enx[kPrefetch ? 2 * Q : 1], fnx[kPrefetch ? 2 * Q : 1];
+      float snx = 0.0f;   // special values of the next row (lanes 0..3)
       if constexpr (kPrefetch) {
 #pragma unroll
         for (int q = 0; q < 2 * Q; q++) enx[q] = 0.0f;   // row L uses no emissions
         loadF(fnx, L);
+        if (L >= 1) snx = spec[(L - 1) * 8 + (lane & 7)];
       }
       for (int i = L; i >= 0; i--) {
         if (TR_LDS) asm volatile("" : "+v"(trofs));
@@ -370,19 +372,23 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
           // ---- Backward row i from row i+1 (ec: emissions of x_{i+1}, fc: kept Forward row i)
           const bool last = i == L;
           float ec[2 * Q], fc[2 * Q];
+          float sv;
           if constexpr (kPrefetch) {
 #pragma unroll
             for (int q = 0; q < 2 * Q; q++) {
               ec[q] = enx[q];
               fc[q] = fnx[q];
             }
+            sv = snx;
             if (i >= 2) {
               loadE(enx, res_at(i - 1));   // residue x_i, used by row i-1
               loadF(fnx, i - 1);
+              snx = spec[(i - 2) * 8 + (lane & 7)];
             }
           } else {
             if (!last) loadE(ec, res_at(i));
             loadF(fc, i);
+            sv = spec[(i - 1) * 8 + (lane & 7)];
           }
           // u_k = e_k(x_{i+1}) bM_k(i+1), w_k = i_k(x_{i+1}) bI_k(i+1)
           float u[Q], w[Q];
@@ -438,7 +444,6 @@ __global__ void __launch_bounds__(kDecThreads) decode_kernel(DevProfile P, DevDb
             pi[q] = fc[Q + q] * bI[q];
             part2 += pm[q] + pi[q];
           }
-          const float sv = spec[(i - 1) * 8 + (lane & 7)];
           const float fN = readlane_f(sv, 0), fJl = readlane_f(sv, 1), fCl = readlane_f(sv, 2),
                       fE = readlane_f(sv, 3);
           const float Zc = wave_sum_f(part2);
@@ -728,11 +733,16 @@ __global__ void decode_export(const int32_t *c, int32_t *n_dom) {
 }
 
 // Tables of the decode kernel: emissions in LDS up to 12 vectors per lane,
-// transitions in registers up to 16, else in LDS.
+// transitions in registers up to 16, else in LDS.  (Both tables in LDS with
+// workgroups of 8 waves, two waves per SIMD at 256 registers, was measured
+// slower at 12 vectors: the per-row LDS reads and recomputed gates cost more
+// than the second wave hides.)
 template <int Q>
 constexpr bool kDecEmitLds = Q <= 12;
 template <int Q>
 constexpr bool kDecTrLds = Q > 16;
+template <int Q>
+constexpr auto decode_fn = decode_kernel<Q, kDecEmitLds<Q>, kDecTrLds<Q>>;
 
 template <int Q>
 size_t decode_lds() {
@@ -742,7 +752,7 @@ size_t decode_lds() {
 
 template <int Q>
 int decode_waves_q() {
-  auto k = decode_kernel<Q, kDecEmitLds<Q>, kDecTrLds<Q>>;
+  auto k = decode_fn<Q>;
   const size_t lds = decode_lds<Q>();
   if (lds > 64 * 1024)
     (void)hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -757,13 +767,15 @@ int decode_waves_q() {
 
 template <int Q>
 hipError_t launch_decode_q(const DevDb &db, const DevProfile &P, const DevDecode &d, hipStream_t s) {
-  auto k = decode_kernel<Q, kDecEmitLds<Q>, kDecTrLds<Q>>;
+  auto k = decode_fn<Q>;
   const size_t lds = decode_lds<Q>();
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  const int blocks = d.nslots / (kDecThreads / kWave);
+  // waves past the last slot return at once (after the table load)
+  constexpr int wpb = kDecThreads / kWave;
+  const int blocks = (d.nslots + wpb - 1) / wpb;
   hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(kDecThreads), lds, s, P, db, d);
   return hipGetLastError();
 }
