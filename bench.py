@@ -14,23 +14,29 @@ against the C3 database; one step searches all 64, reported as aggregate
 GCUPS and queries/hour), --cutoffs F1,F2,F3 (e.g. 1,1e-3,1 runs Viterbi on
 every target).
 
-Roofline of the dominant kernel (MSV): plain packed-int16 VALU arithmetic,
-4 element-ops per cell (max, saturating add, saturating subtract, max), so
-achieved = 4 x cells per launch / (average MSV launch duration), against
-the MI355X packed 16-bit VALU peak 256 CU x 64 lanes x 2 elements x 2.4 GHz
-= 78.64 Tops/s.  The MSV launches of a search (one per pipelined chunk) run
-back to back on the search stream, between HIP events that the library
-records there, so the average launch lasts the stage's time divided by the
-launches.  `traffic` is the HBM bytes per MSV launch that rocprofv3's
-FETCH_SIZE and WRITE_SIZE counters measured for the same kernel source
-(scaled by a plain 1 GiB copy), beside the launch's algorithmic bytes;
-`valu_issue` is the share of the chip's sustained VALU issue rate that the
-launch's counted VALU instructions took.  The MSV needs fewer instructions
-than 4 per cell (one packed add and one packed 3-way maximum per two
-cells, plus its running maxima), so its algorithmic fraction can pass 1
-while its issue fraction cannot.  `stage_roofline` gives the same
-fraction for every stage (Viterbi 18 ops/cell, rescore 17 int32 ops/cell
-against 39.32 Tops/s, Forward 18 flops/cell against 157.3 TFLOP/s).
+Roofline of the dominant kernel (MSV): plain packed 16-bit VALU work, bound
+by instruction issue.  `frac` is the launch's VALU issue against the
+datasheet: the wave64 VALU instructions of one MSV launch (rocprofv3
+SQ_INSTS_VALU, recorded in profiles/msv_traffic_C3.json for the same
+kernel source) over the launch's live duration, against one wave
+instruction per CU per clock (256 x 2.4 GHz); `achieved` and `peak` are the
+same rate in packed 16-bit element-ops (x 128 per instruction, peak 256 CU x
+64 lanes x 2 elements x 2.4 GHz = 78.64 Tops/s).  The MSV launches of a
+search (one per pipelined chunk) run back to back on the search stream,
+between HIP events that the library records there, so the live launch
+duration is the stage's time divided by the launches.  Beside it,
+`algorithmic_frac` counts the nominal 4 element-ops per cell (max,
+saturating add, saturating subtract, running max) over the same time; the
+fp16 rewrite needs fewer instructions than that (one packed add and one
+packed 3-way maximum per two cells, plus its running maximum), so that
+figure can pass 1 while the issue fraction cannot.  `traffic` is the HBM
+bytes per MSV launch that rocprofv3's FETCH_SIZE and WRITE_SIZE counters
+measured for the same kernel source (scaled by a plain 1 GiB copy), beside
+the launch's algorithmic bytes; `valu_issue` is the same instruction count
+against the sustained rate a probe kernel measures in the run.
+`stage_roofline` gives the algorithmic fraction of every stage (Viterbi 18
+ops/cell, rescore 17 int32 ops/cell against 39.32 Tops/s, Forward 18
+flops/cell against 157.3 TFLOP/s).
 """
 from __future__ import annotations
 
@@ -421,7 +427,7 @@ def main():
                      "traffic": traffic[0] if traffic else None,
                      "traffic_note": ("HBM bytes per MSV launch (FETCH_SIZE + WRITE_SIZE, rocprofv3 counters "
                                       "scaled by a 1 GiB copy); algorithmic_bytes = residues of the launch's chunk "
-                                      "+ 20 bytes of index and results per target"),
+                                      "+ 15 bytes of index and results per target"),
                      "algorithmic_bytes": traffic[1] if traffic else None,
                      "ms_per_launch": round(msv_ms / chunks, 4),
                      "peak_measured": round(probe_tops, 3),
