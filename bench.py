@@ -367,7 +367,7 @@ def main():
                 and tr.get("header_sha", kernel_source_sha("hmm_device.h")) == kernel_source_sha("hmm_device.h")
                 and tr.get("launches_per_search") == chunks):
             traffic = (tr.get("bytes_per_launch"), tr.get("algorithmic_bytes_per_launch"),
-                       tr.get("valu_insts_per_launch"))
+                       tr.get("valu_insts_per_launch"), tr.get("kernel_source_sha"))
     issue = issue_roofline(traffic[2], msv_ms / chunks) if traffic and traffic[2] and msv_ms > 0 else None
     if batched:
         wl = (f"C4: {len(profs)} Plan7 profiles, M {min(M_list)}-{max(M_list)} (sum {sum(M_list)}), each searched "
@@ -415,10 +415,12 @@ def main():
                      "peak": round(PEAK_PK16_TOPS, 2),
                      "unit": "Tops/s packed 16-bit VALU issue (SQ_INSTS_VALU x 128 per launch / launch time)",
                      "frac": issue["frac"] if issue else None,
-                     "frac_note": ("wave64 VALU instructions per MSV launch (rocprofv3 counter record for this "
-                                   "kernel source) / live launch time / (256 CU x 2.4 GHz); null when the record "
-                                   "is for another source"),
+                     "frac_note": ("wave64 VALU instructions per MSV launch (rocprofv3 counter record of the "
+                                   "kernel source whose sha256[:16] is counter_source_sha, the one built here) / "
+                                   "live launch time / (256 CU x 2.4 GHz); null when the record is for another "
+                                   "source"),
                      "valu_insts_per_launch": issue["insts_per_launch"] if issue else None,
+                     "counter_source_sha": traffic[3] if traffic else None,
                      "algorithmic_achieved": round(achieved, 3),
                      "algorithmic_frac": round(achieved / PEAK_PK16_TOPS, 4),
                      "algorithmic_note": ("4 packed 16-bit ops per cell (max, saturating add, saturating subtract, "
