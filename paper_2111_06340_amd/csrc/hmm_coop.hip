@@ -123,15 +123,58 @@ __device__ __forceinline__ int next_target(int32_t *work, int *slot) {
 }
 
 // ============================================================================ Forward
-template <int QW, int W>
-__global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db, DevOut out) {
+// A row's lane scan as one DPP multiply-add per step (x <- x + P x_src, a
+// lane without a source reading 0; rows outside the row mask keep x), and
+// the wave sum's two row-broadcast steps as one DPP add each.  Each step
+// states the two wait states a DPP read needs after the VALU write of its
+// source.
+__device__ __forceinline__ float affine_scan_fused(float a, const float (&ps)[6]) {
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[0]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[1]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[2]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[3]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf"
+               : "+v"(a) : "v"(ps[4]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf"
+               : "+v"(a) : "v"(ps[5]));
+  return a;
+}
+__device__ __forceinline__ float wave_sum_fused(float v) {
+  v += dpp_f<kRowShr1, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr2, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr4, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr8, 0xf>(v, 0.0f);
+  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf" : "+v"(v));
+  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf" : "+v"(v));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+template <int W>
+struct FwdCoopLds {
+  float xo[2][W][kWave], ml[2][W][kWave], il[2][W][kWave], al[2][W][kWave], es[2][W];
+  int slot;
+};
+
+// The work of wave WI of a Forward workgroup (its segment index a
+// constant): every wave runs its own instance, and all instances take the
+// same barriers in the same order.
+template <int QW, int W, int WI>
+__device__ __forceinline__ void fwd_coop_wave(const DevProfile &P, const DevDb &db, const DevOut &out,
+                                              FwdCoopLds<W> &sh) {
   constexpr int Q = QW * W;
-  __shared__ float sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave], ses[2][W];
-  __shared__ int slot;
+  constexpr int w = WI;
+  constexpr int q0 = w * QW;
+  constexpr int nb = w > 0 ? w - 1 : W - 1;   // segment of the first cell's left neighbour
+  auto &sxo = sh.xo;
+  auto &sml = sh.ml;
+  auto &sil = sh.il;
+  auto &sal = sh.al;
+  auto &ses = sh.es;
   const int lane = threadIdx.x & 63;
-  const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int q0 = w * QW;
-  const int nb = w > 0 ? w - 1 : W - 1;   // segment of the first cell's left neighbour
   const float *trg = P.f_tr + lane;
   // transition planes of this wave's cells, registers
   float tr[TR_N][QW];
@@ -176,7 +219,7 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
   const float entry_p = P.entry_p;
   const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
   for (;;) {
-    const int idx = next_target(&db.counters[CNT_WORK_FWD], &slot);
+    const int idx = next_target(&db.counters[CNT_WORK_FWD], &sh.slot);
     if (idx >= count) break;
     const int t = uni(db.list_fwd[idx]);
     const int L = uni(db.len[t]);
@@ -214,7 +257,7 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       float es = 0.0f;
 #pragma unroll
       for (int q = 0; q < QW; q++) es = fmaf(M[q], gx[q], es);
-      es = wave_sum_f(es);
+      es = wave_sum_fused(es);
       // delete chain with nothing entering the segment (A)
       D[0] = 0.0f;
 #pragma unroll
@@ -226,17 +269,17 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       if (lane == 0) ses[par][w] = es;
       __syncthreads();
       // the values entering the lane's segments
-      float a = 0.0f;
+      float a = sxo[par][0][lane];
 #pragma unroll
-      for (int j = 0; j < W; j++) a = fmaf(pj[j], a, sxo[par][j][lane]);
-      float x = lane_up_f(affine_scan(a, ps));
-      float xw = 0.0f, xn = 0.0f, E = 0.0f;
+      for (int j = 1; j < W; j++) a = fmaf(pj[j], a, sxo[par][j][lane]);
+      float x = lane_up_f(affine_scan_fused(a, ps));
+      float xw = x, xn = x, E = ses[par][0];
 #pragma unroll
       for (int j = 0; j < W; j++) {
         if (j == w) xw = x;
         if (j == nb) xn = x;
-        E += ses[par][j];
-        x = fmaf(pj[j], x, sxo[par][j][lane]);
+        if (j) E += ses[par][j];
+        if (j + 1 < W) x = fmaf(pj[j], x, sxo[par][j][lane]);
       }
 #pragma unroll
       for (int q = 0; q < QW; q++) D[q] = fmaf(pre[q], xw, D[q]);
@@ -244,7 +287,7 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       pM = sml[par][nb][lane];
       pI = sil[par][nb][lane];
       pD = fmaf(pl[nb], xn, sal[par][nb][lane]);
-      if (w == 0) {
+      if constexpr (w == 0) {
         pM = lane_up_f(pM);
         pI = lane_up_f(pI);
         pD = lane_up_f(pD);
@@ -281,7 +324,7 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
     float ea[2 * QW], eb[2 * QW];
     int stop;
     (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
-    if (w == 0) {
+    if constexpr (w == 0) {
       const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
       const bool pass = f > lp.fthr;
       const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
@@ -289,6 +332,25 @@ __global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db
       out.fwd[uni(db.perm[t])] = f;
       if (pass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
     }
+  }
+}
+
+
+
+template <int QW, int W>
+__global__ void __launch_bounds__(64 * W) fwd_coop_kernel(DevProfile P, DevDb db, DevOut out) {
+  static_assert(W == 2 || W == 4, "two or four waves per target");
+  __shared__ FwdCoopLds<W> sh;
+  const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  if (w == 0) {
+    fwd_coop_wave<QW, W, 0>(P, db, out, sh);
+  } else if (w == 1) {
+    fwd_coop_wave<QW, W, 1>(P, db, out, sh);
+  } else if constexpr (W == 4) {
+    if (w == 2)
+      fwd_coop_wave<QW, W, 2>(P, db, out, sh);
+    else
+      fwd_coop_wave<QW, W, 3>(P, db, out, sh);
   }
 }
 
@@ -316,17 +378,29 @@ __device__ __forceinline__ int lane_up_fill(int v, int fill) {
   return __builtin_amdgcn_update_dpp(fill, v, 0x138 /* wave_shr:1 */, 0xf, 0xf, false);
 }
 
-template <int QW, int W>
-__global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb db, DevOut out) {
+template <int W>
+struct VitCoopLds {
+  int xo[2][W][kWave], ml[2][W][kWave], il[2][W][kWave], al[2][W][kWave];
+  int xs[2][W];   // per wave: its maximum when it crossed the trigger line, else kNeg32
+  int fin[W];
+  int slot;
+};
+
+// The work of wave WI of a rescore workgroup, as in the Forward kernel.
+template <int QW, int W, int WI>
+__device__ __forceinline__ void vit32_coop_wave(const DevProfile &P, const DevDb &db, const DevOut &out,
+                                                VitCoopLds<W> &sh) {
   constexpr int Q = QW * W;
-  __shared__ int sxo[2][W][kWave], sml[2][W][kWave], sil[2][W][kWave], sal[2][W][kWave];
-  __shared__ int sxs[2][W];    // per wave: its maximum when it crossed the trigger line, else kNeg32
-  __shared__ int fin[W];
-  __shared__ int slot;
+  constexpr int w = WI;
+  constexpr int q0 = w * QW;
+  constexpr int nb = w > 0 ? w - 1 : W - 1;
+  auto &sxo = sh.xo;
+  auto &sml = sh.ml;
+  auto &sil = sh.il;
+  auto &sal = sh.al;
+  auto &sxs = sh.xs;
+  auto &fin = sh.fin;
   const int lane = threadIdx.x & 63;
-  const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int q0 = w * QW;
-  const int nb = w > 0 ? w - 1 : W - 1;
   const int *trg = P.v32_tr + lane;
   int tr[TR_N][QW];
 #pragma unroll
@@ -362,7 +436,7 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
   const int mdn = into_next(TR_MDIN, w), ddn = into_next(TR_DDIN, w);
   const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
-    const int idx = next_target(&db.counters[CNT_WORK_OVF], &slot);
+    const int idx = next_target(&db.counters[CNT_WORK_OVF], &sh.slot);
     if (idx >= count) break;
     const int t = uni(db.list_ovf[idx]);
     const int L = uni(db.len[t]);
@@ -420,19 +494,19 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
 #pragma unroll
       for (int j = 1; j < W; j++) a = max(sxo[par][j][lane], a + pj[j]);
       int x = lane_up_fill(maxplus_scan_i(a, bs), tau);
-      int xw = tau, xn = tau;
+      int xw = x, xn = x;
 #pragma unroll
       for (int j = 0; j < W; j++) {
         if (j == w) xw = x;
         if (j == nb) xn = x;
-        x = max(sxo[par][j][lane], x + pj[j]);
+        if (j + 1 < W) x = max(sxo[par][j][lane], x + pj[j]);
       }
 #pragma unroll
       for (int q = 0; q < QW; q++) D[q] = max(D[q], xw + pre[q]);
       pM = sml[par][nb][lane];
       pI = sil[par][nb][lane];
       pD = max(sal[par][nb][lane], xn + pl[nb]);
-      if (w == 0) {
+      if constexpr (w == 0) {
         pM = lane_up_fill(pM, kNeg32);
         pI = lane_up_fill(pI, kNeg32);
         pD = lane_up_fill(pD, kNeg32);
@@ -461,8 +535,25 @@ __global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb 
       int m = kNeg32;
 #pragma unroll
       for (int j = 0; j < W; j++) m = max(m, fin[j]);
-      if (w == 0) out.vit[uni(db.perm[t])] = fl32(fl32(m + ej) + mv);
+      if constexpr (w == 0) out.vit[uni(db.perm[t])] = fl32(fl32(m + ej) + mv);
     }
+  }
+}
+
+template <int QW, int W>
+__global__ void __launch_bounds__(64 * W) vit32_coop_kernel(DevProfile P, DevDb db, DevOut out) {
+  static_assert(W == 2 || W == 4, "two or four waves per target");
+  __shared__ VitCoopLds<W> sh;
+  const int w = (int)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  if (w == 0) {
+    vit32_coop_wave<QW, W, 0>(P, db, out, sh);
+  } else if (w == 1) {
+    vit32_coop_wave<QW, W, 1>(P, db, out, sh);
+  } else if constexpr (W == 4) {
+    if (w == 2)
+      vit32_coop_wave<QW, W, 2>(P, db, out, sh);
+    else
+      vit32_coop_wave<QW, W, 3>(P, db, out, sh);
   }
 }
 
