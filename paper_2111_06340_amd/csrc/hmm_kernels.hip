@@ -1097,6 +1097,9 @@ __global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(De
   constexpr bool TRL = kTrLds16<Q>;
   static_assert(!(TRL && EMIT_LDS), "one LDS table per instance");
   const int lane = threadIdx.x & 63;
+  // a launch with no target returns before staging its table
+  const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
+  if (count == 0) return;
   if (EMIT_LDS || TRL) {
     const uint4 *src = (const uint4 *)(EMIT_LDS ? P.vit_emit : P.vit_tr);
     const int n4 = (EMIT_LDS ? kAlpha * 2 : TR_N) * Q * kWave / 4;
@@ -1111,7 +1114,6 @@ __global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(De
 #pragma unroll
     for (int q = 0; q < Q; q++)
       tr[k][q] = (!TRL || k == TR_DDIN) ? P.vit_tr[(k * Q + q) * kWave + lane] : 0u;
-  const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_VIT], 1);
     if (idx >= count) break;
@@ -1143,6 +1145,9 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
   extern __shared__ int32_t lds32[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;   // dwords
+  // a launch with no target (no int16 overflow) returns before staging its table
+  const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
+  if (count == 0) return;
   for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_emit)[i];
   __syncthreads();
   const int *emit = (const int *)lds32 + lane;
@@ -1153,7 +1158,6 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
 #pragma unroll
     for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
   auto TR = [&](int k, int q) -> int { return tr[k][q]; };
-  const int count = uni(__atomic_load_n(&db.counters[CNT_OVF], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
     if (idx >= count) break;
@@ -1258,6 +1262,9 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
   extern __shared__ float ldsf[];
   const int lane = threadIdx.x & 63;
   constexpr int kEmit = kAlpha * 2 * Q * kWave;
+  // a launch with no target returns before staging its table
+  const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
+  if (count == 0) return;
   for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_emit)[i];
   __syncthreads();
   const float *emit = (const float *)ldsf + lane;
@@ -1286,7 +1293,6 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
 #undef HMM_PSTEP
   }
   const float entry_p = P.entry_p;
-  const int count = uni(__atomic_load_n(&db.counters[CNT_FWD], __ATOMIC_RELAXED));
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_FWD], 1);
     if (idx >= count) break;
