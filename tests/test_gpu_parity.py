@@ -597,6 +597,39 @@ def test_repeated_searches_streams_and_threshold_changes():
     D.close()
 
 
+def test_stages_that_receive_no_target():
+    """Searches whose later stages get no target -- nothing passes MSV; then
+    MSV passes but none passes Viterbi or overflows int16 -- between full
+    searches on the same handle: the empty Viterbi, rescore and Forward
+    launches return before staging their tables, the counters of the
+    previous search do not leak, and every result equals the oracle's."""
+    import torch
+    prof = gen.make_profile(200, 31)
+    db = gen.random_sequences(4321, 3000, 300)
+    calib = oracle.calibrate(oracle.OracleProfile(prof), nthreads=NTHREADS)
+    P = hg.Profile(prof, *calib)
+    D = hg.Database(db.residues, db.offsets)
+    for F in ((1.0, 1.0, 1.0), (1e-30, 1.0, 1.0), (0.05, 1e-30, 1.0), (1.0, 1.0, 1.0)):
+        out = hg.alloc_results(D.n)
+        hg.search(P, D, F, out)
+        torch.cuda.synchronize()
+        g = {k: v.cpu().numpy() for k, v in out.items()}
+        o = oracle_search(prof, db.residues, db.offsets, calib, F)
+        st = compare(g, o, what=f"empty stages F={F}")
+        fl = o["flags"]
+        counts = out["counts"].cpu().numpy()
+        assert counts[0] == np.sum((fl & hg.HMM_MSV_PASS) != 0)
+        assert counts[1] == np.sum((fl & hg.HMM_VIT_OVF) != 0)
+        assert counts[2] == np.sum((fl & hg.HMM_VIT_PASS) != 0)
+        if F[0] < 1e-20:
+            assert counts[0] == 0 and np.all(g["vit"] == np.iinfo(np.int32).min) and np.all(np.isnan(g["fwd"]))
+        if F[1] < 1e-20:
+            assert counts[0] > 0 and counts[1] == 0 and counts[2] == 0 and np.all(np.isnan(g["fwd"]))
+        announce(f"empty stages F={F} ok {st} counts={counts.tolist()}")
+    P.close()
+    D.close()
+
+
 def test_concurrent_searches_on_shared_database_handles():
     """hmm_db_share: four profiles searched at once on four streams through
     four handles of one uploaded database; every result equals the oracle's,
