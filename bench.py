@@ -149,12 +149,14 @@ def valu_issue(insts_per_launch, ms_per_launch, probe_ops_per_s):
             "frac": round(insts_per_launch / (ms_per_launch / 1e3 * rate), 4)}
 
 
-def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
+def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1, fused=False):
     """Per-stage fractions of the relevant VALU peak: algorithmic ops of the
     cells each stage processed, over its measured time (HIP events).  With
     a pipelined search (chunks > 1) the later stages overlap the MSV of the
     next chunk and only their exposed time is measured, so only MSV's
-    fraction is given (run with --pipeline 1 for the others)."""
+    fraction is given (run with --pipeline 1 for the others).  With the
+    fused tail (Viterbi, rescore and Forward as one kernel) the three have
+    one time, given as `tail` (run with --tail 1 for the separate ones)."""
     msv_ops = MSV_OPS_PER_CELL * sum(M * res_total for M in M_list)
     out = {}
 
@@ -167,6 +169,11 @@ def stage_roofline(M_list, res_total, ran_cells, st_ms, chunks=1):
     if chunks > 1:
         out["note"] = (f"{chunks} pipelined chunks: Viterbi, rescore and Forward overlap the next chunk's MSV; "
                        f"stage_ms holds their exposed time after the last MSV")
+        return out
+    if fused:
+        out["tail"] = {"ms": round(st_ms[1], 4),
+                       "note": "Viterbi, rescore and Forward as one kernel (hmm_db_fused_tail mode 2): one time "
+                               "for the three stages; --tail 1 times them one by one"}
         return out
     out["viterbi"] = entry(VIT_OPS_PER_CELL * ran_cells["viterbi"], st_ms[1], round(PEAK_PK16_TOPS, 2),
                            "Tops/s packed 16-bit, 18 ops/cell, cells of the targets scored to their last row "
@@ -207,6 +214,10 @@ def main():
                     help="chunks a search is pipelined in (hmm_db_pipeline; 0 = the library's default, "
                          "1 = sequential stages, whose per-stage times give per-stage roofline fractions; "
                          "-1 = 1 for C4, whose 64 searches overlap through --streams, else the default)")
+    ap.add_argument("--tail", type=int, default=0, choices=[0, 1, 2, 3],
+                    help="stages after MSV (hmm_db_fused_tail): 1 = one kernel per stage, 2 = one fused kernel "
+                         "for profiles of up to 384 nodes, 3 = fused when the Viterbi cutoff is 1, "
+                         "0 = the library's default (3)")
     ap.add_argument("--group", type=int, default=-1,
                     help="C4: searches per hmm_search_group call, each through its own database handle "
                          "(default: all 64 in one call; 0: separate hmm_search calls spread over --streams)")
@@ -269,6 +280,7 @@ def main():
     Ds = [hg.Database(d.residues, d.offsets) for d in dbs]
     D = Ds[0]
     chunks = [hg.hmm_db_pipeline(Dx.handle, args.pipeline) for Dx in Ds][0]
+    tail_mode = [hg.hmm_db_fused_tail(Dx.handle, args.tail) for Dx in Ds][0]   # shared handles inherit it
     upload_s = time.perf_counter() - t
     log(f"database(s) packed and uploaded in {upload_s:.2f}s (host buffers, PCIe included; not timed below)")
     # search jobs (profile, database) spread round-robin over `streams` lanes;
@@ -349,6 +361,9 @@ def main():
     st_ms = [float(v) for v in
              (stages.reshape(-1, len(Ps), 4).sum(axis=1).mean(axis=0) if stages.size else np.zeros(4))]
     msv_ms = float(st_ms[0])
+    # the fused tail has instances for profiles of up to 384 nodes (3 int16
+    # vectors per lane); longer ones run the staged kernels in either mode
+    tail_fused = (tail_mode == 2 or (tail_mode == 3 and F[1] >= 1.0)) and max(M_list) <= 384
     achieved = MSV_OPS_PER_CELL * cells / (msv_ms / 1e3) / 1e12 if msv_ms > 0 else 0.0
     log(f"{ms_step:.3f} ms/step, {gcups:.1f} GCUPS; stages ms: MSV {st_ms[0]:.3f} Viterbi {st_ms[1]:.3f} "
         f"rescore {st_ms[2]:.3f} (concurrent with) Forward {st_ms[3]:.3f}; counts {counts}")
@@ -399,7 +414,8 @@ def main():
         "config": {"workload": wl, "M": M_list if batched else M_list[0], "n_seqs": D.n,
                    "residues": D.n_residues, "cutoffs": list(F), "databases": len(Ds), "streams": S},
         # rescore and Forward run concurrently after Viterbi: both are timed
-        # from Viterbi's end, Forward until both are done
+        # from Viterbi's end, Forward until both are done (with the fused
+        # tail, "viterbi" holds all three)
         "stage_ms": {"msv": round(float(st_ms[0]), 4), "viterbi": round(float(st_ms[1]), 4),
                      "rescore": round(float(st_ms[2]), 4), "forward_and_rescore": round(float(st_ms[3]), 4)},
         "survivors": {"msv_pass": counts[0],
@@ -439,8 +455,10 @@ def main():
                      "ops_per_cell": MSV_OPS_PER_CELL, "cells_per_search": cells // len(jobs),
                      "msv_launches_per_search": chunks}
         if timed_stages else None,
-        "stage_roofline": stage_roofline(M_list, D.n_residues, ran, st_ms, chunks) if timed_stages else None,
+        "stage_roofline": (stage_roofline(M_list, D.n_residues, ran, st_ms, chunks, fused=tail_fused)
+                           if timed_stages else None),
         "pipeline_chunks": chunks,
+        "tail_mode": tail_mode,
         "upload_s": round(upload_s, 3),
         "calib": list(calibs[0]),
     }

@@ -370,6 +370,21 @@ int hmm_probe_pk16(hmm_stream stream, double *ops_per_s, float *ms);
  * Errors: HMM_EINVAL (NULL db, chunks outside 0..8). */
 int hmm_db_pipeline(hmm_db *db, int32_t chunks, int32_t *current);
 
+/* Tuning hook: how a search on this handle runs the stages after MSV.
+ * mode 1: one kernel per stage (int16 Viterbi over every MSV survivor, then
+ * the int32 rescore of its overflows beside Forward over its passes).
+ * mode 2: for profiles of at most 384 nodes, one kernel in which a wave
+ * takes each MSV survivor through its Viterbi, rescore (if it overflowed)
+ * and Forward (if it passed) before its next target, so that no stage
+ * waits for the longest target of the one before it; longer profiles run
+ * the staged kernels.  mode 3 (the default): mode 2 for searches whose
+ * Viterbi cutoff F2 is 1 (every target that reaches Viterbi reaches
+ * Forward), mode 1 otherwise.  Results do not depend on it.  When the fused
+ * kernel runs, hmm_db_stage_times reports it as the Viterbi stage.  mode 0
+ * changes nothing; *current (if non-NULL) receives the mode in force.
+ * Errors: HMM_EINVAL (NULL db, mode outside 0..3). */
+int hmm_db_fused_tail(hmm_db *db, int32_t mode, int32_t *current);
+
 /* Database properties: number of targets, total residues, longest target. */
 int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t *max_len);
 

@@ -27,7 +27,8 @@ HMM_MSV_PASS, HMM_MSV_OVF, HMM_VIT_RAN, HMM_VIT_PASS, HMM_VIT_OVF, HMM_FWD_RAN, 
 HMM_RT1, HMM_RT2 = 0.25, 0.10   # region thresholds on the core posterior (float32 in the library)
 
 EXPORTED = ("hmm_db_free", "hmm_db_info", "hmm_db_stage_times", "hmm_db_stage_timing", "hmm_db_upload",
-            "hmm_count", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params", "hmm_debug_tables",
+            "hmm_count", "hmm_db_fused_tail", "hmm_db_pipeline", "hmm_db_share", "hmm_debug_length_params",
+            "hmm_debug_tables",
             "hmm_decode", "hmm_decode_static", "hmm_last_error", "hmm_profile_free", "hmm_rebuild",
             "hmm_probe_pk16", "hmm_profile_upload", "hmm_search", "hmm_search_group", "hmm_strerror")
 
@@ -82,6 +83,8 @@ def lib():
         L.hmm_db_free.argtypes = [vp]
         L.hmm_db_pipeline.restype = C.c_int
         L.hmm_db_pipeline.argtypes = [vp, i32, C.POINTER(i32)]
+        L.hmm_db_fused_tail.restype = C.c_int
+        L.hmm_db_fused_tail.argtypes = [vp, i32, C.POINTER(i32)]
         L.hmm_db_share.restype = C.c_int
         L.hmm_db_share.argtypes = [vp, C.POINTER(vp)]
         L.hmm_search.restype = C.c_int
@@ -177,6 +180,13 @@ def hmm_db_pipeline(handle: int, chunks: int = 0) -> int:
     """Set (chunks > 0) and return the number of pipelined chunks of a search."""
     cur = C.c_int32(0)
     _check(lib().hmm_db_pipeline(C.c_void_p(handle), int(chunks), C.byref(cur)), "hmm_db_pipeline")
+    return cur.value
+
+
+def hmm_db_fused_tail(handle: int, mode: int = 0) -> int:
+    """Set (mode 1 staged, 2 fused, 3 fused when F2 = 1) and return how the stages after MSV run."""
+    cur = C.c_int32(0)
+    _check(lib().hmm_db_fused_tail(C.c_void_p(handle), int(mode), C.byref(cur)), "hmm_db_fused_tail")
     return cur.value
 
 

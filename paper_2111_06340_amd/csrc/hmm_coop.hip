@@ -123,36 +123,6 @@ __device__ __forceinline__ int next_target(int32_t *work, int *slot) {
 }
 
 // ============================================================================ Forward
-// A row's lane scan as one DPP multiply-add per step (x <- x + P x_src, a
-// lane without a source reading 0; rows outside the row mask keep x), and
-// the wave sum's two row-broadcast steps as one DPP add each.  Each step
-// states the two wait states a DPP read needs after the VALU write of its
-// source.
-__device__ __forceinline__ float affine_scan_fused(float a, const float (&ps)[6]) {
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-               : "+v"(a) : "v"(ps[0]));
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-               : "+v"(a) : "v"(ps[1]));
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-               : "+v"(a) : "v"(ps[2]));
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1"
-               : "+v"(a) : "v"(ps[3]));
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf"
-               : "+v"(a) : "v"(ps[4]));
-  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf"
-               : "+v"(a) : "v"(ps[5]));
-  return a;
-}
-__device__ __forceinline__ float wave_sum_fused(float v) {
-  v += dpp_f<kRowShr1, 0xf>(v, 0.0f);
-  v += dpp_f<kRowShr2, 0xf>(v, 0.0f);
-  v += dpp_f<kRowShr4, 0xf>(v, 0.0f);
-  v += dpp_f<kRowShr8, 0xf>(v, 0.0f);
-  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf" : "+v"(v));
-  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf" : "+v"(v));
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
-}
-
 template <int W>
 struct FwdCoopLds {
   float xo[2][W][kWave], ml[2][W][kWave], il[2][W][kWave], al[2][W][kWave], es[2][W];

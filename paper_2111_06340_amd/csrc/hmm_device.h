@@ -119,6 +119,74 @@ __device__ __forceinline__ float wave_sum_f(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
+// A row's lane scan as one DPP multiply-add per step (x <- x + P x_src, a
+// lane without a source reading 0; rows outside the row mask keep x), and
+// the wave sum's two row-broadcast steps as one DPP add each.  Each step
+// states the two wait states a DPP read needs after the VALU write of its
+// source.
+__device__ __forceinline__ float affine_scan_fused(float a, const float (&ps)[6]) {
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[0]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[1]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[2]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "+v"(a) : "v"(ps[3]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:15 row_mask:0xa bank_mask:0xf"
+               : "+v"(a) : "v"(ps[4]));
+  asm volatile("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 row_bcast:31 row_mask:0xc bank_mask:0xf"
+               : "+v"(a) : "v"(ps[5]));
+  return a;
+}
+__device__ __forceinline__ float wave_sum_fused(float v) {
+  v += dpp_f<kRowShr1, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr2, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr4, 0xf>(v, 0.0f);
+  v += dpp_f<kRowShr8, 0xf>(v, 0.0f);
+  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf" : "+v"(v));
+  asm volatile("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf" : "+v"(v));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+// Fused lane shifts: the previous lane's value (0 in lane 0, DPP wave_shr:1
+// with bound_ctrl) enters a multiply-add or a product directly, without a
+// separate move.  Each form first waits the two wait states a DPP read
+// needs after the VALU write of its source.
+//   acc += up(s0) t0; acc += up(s1) t1; acc += up(s2) t2   (in this order)
+__device__ __forceinline__ void fmac_up3(float &acc, float s0, float t0, float s1, float t1, float s2, float t2) {
+  asm volatile(
+      "s_nop 1\n\t"
+      "v_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+      "v_fmac_f32_dpp %0, %3, %4 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+      "v_fmac_f32_dpp %0, %5, %6 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "+v"(acc)
+      : "v"(s0), "v"(t0), "v"(s1), "v"(t1), "v"(s2), "v"(t2));
+}
+//   up(s) t
+__device__ __forceinline__ float mul_up(float s, float t) {
+  float d;
+  asm volatile("s_nop 1\n\tv_mul_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+               : "=v"(d)
+               : "v"(s), "v"(t));
+  return d;
+}
+
+// Issue priority of a wave by the length of its target against the
+// database's longest (lmax): a stage ends with its longest targets, so when
+// the waves of a SIMD compete for issue, those rows go first and the
+// shorter targets' waves fill the gaps.
+__device__ __forceinline__ void length_priority(int L, int lmax) {
+  if (4 * L > 3 * lmax)
+    __builtin_amdgcn_s_setprio(3);
+  else if (2 * L > lmax)
+    __builtin_amdgcn_s_setprio(2);
+  else if (4 * L > lmax)
+    __builtin_amdgcn_s_setprio(1);
+  else
+    __builtin_amdgcn_s_setprio(0);
+}
+
 // Row driver.  The residues of one target arrive 256 at a time: lane j of
 // `cur` holds dword j of the current 256-byte chunk, `nxt` the next chunk
 // (loaded a chunk ahead).  Rows are processed four per dword with two table

@@ -124,6 +124,10 @@ struct hmm_db {
   // [chunk_at[chunks][k], chunk_at[chunks][k+1]), of about equal residues.
   SearchSync sync;
   int chunks = 1;
+  // the stages after MSV: 1 staged kernels, 2 one fused kernel where the
+  // profile has an instance, 3 fused when the Viterbi cutoff passes every
+  // target (hmm_db_fused_tail)
+  int fused_tail = 3;
   int64_t chunk_at[kMaxChunks + 1][kMaxChunks + 1] = {};
   // posterior-decoding scratch (allocated by the first hmm_decode)
   void *dec_mem = nullptr;
@@ -770,6 +774,7 @@ int hmm_db_share(const hmm_db *src, hmm_db **out) {
   db->data = src->data;
   db->data->refs.fetch_add(1);
   db->chunks = src->chunks;
+  db->fused_tail = src->fused_tail;
   memcpy(db->chunk_at, src->chunk_at, sizeof db->chunk_at);
   db->dev = src->dev;   // shared residues and index arrays; attach_scratch replaces the rest
   const int rc = attach_scratch(db);
@@ -887,6 +892,14 @@ int hmm_db_pipeline(hmm_db *db, int32_t chunks, int32_t *current) {
   return HMM_OK;
 }
 
+int hmm_db_fused_tail(hmm_db *db, int32_t mode, int32_t *current) {
+  if (!db) return fail(HMM_EINVAL, "db is NULL");
+  if (mode < 0 || mode > 3) return fail(HMM_EINVAL, "mode = %d; need 0..3", mode);
+  if (mode > 0) db->fused_tail = mode;   // searches on a handle are serialised on the GPU
+  if (current) *current = db->fused_tail;
+  return HMM_OK;
+}
+
 int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t *max_len) {
   if (!db) return fail(HMM_EINVAL, "db is NULL");
   if (n_seqs) *n_seqs = db->n;
@@ -894,6 +907,15 @@ int hmm_db_info(const hmm_db *db, int64_t *n_seqs, int64_t *n_residues, int32_t 
   if (max_len) *max_len = db->max_len;
   return HMM_OK;
 }
+
+// Whether a search runs its stages after MSV as one kernel (mode of
+// hmm_db_fused_tail).  In mode 3 it does when the Viterbi cutoff passes every
+// target: then every target that reaches Viterbi also reaches Forward, and a
+// wave that takes each through all its stages saves two stage boundaries.
+// With a Viterbi filter most targets stop there, and the staged int16
+// kernel, at twice the waves per SIMD (the fused kernel's registers are set
+// by its Forward), is the faster one.
+static int fuse_tail(int mode, const hmm_thresholds &t) { return mode == 2 || (mode == 3 && t.F2 >= 1.0); }
 
 // Every transition score is <= 0 and a path emits at most once per residue,
 // so no Viterbi value of a target of length L exceeds L * s_max.  The int32
@@ -932,7 +954,8 @@ int hmm_search(const hmm_profile *p, hmm_db *db, const hmm_thresholds *t, const 
     db->lp_F[1] = t->F2;
     db->lp_F[2] = t->F3;
   }
-  DevOut o{out->msv, out->vit, out->fwd, out->flags, out->counts, out->bias, t->bias_filter};
+  DevOut o{out->msv,  out->vit,       out->fwd, out->flags, out->counts,
+           out->bias, t->bias_filter, fuse_tail(db->fused_tail, *t)};
   hipEvent_t *ev = nullptr;
   if (db->tcap > 0) ev = &db->tev[(size_t)(db->trec++ % db->tcap) * 5];
   DevDb chunk[kMaxChunks];
@@ -988,7 +1011,8 @@ int hmm_search_group(const hmm_profile *const *p, hmm_db *const *db, const hmm_t
     }
     P[i] = p[i]->dev;
     D[i] = chunk_of(d->dev, 0, d->n, 0);
-    O[i] = DevOut{out[i].msv, out[i].vit, out[i].fwd, out[i].flags, out[i].counts, out[i].bias, t[i].bias_filter};
+    O[i] = DevOut{out[i].msv,    out[i].vit,  out[i].fwd,        out[i].flags,
+                  out[i].counts, out[i].bias, t[i].bias_filter, fuse_tail(d->fused_tail, t[i])};
     Y[i] = &d->sync;
   }
   HIP_TRY(launch_search_group(P.data(), D.data(), O.data(), n, s, Y.data()), "kernel launch");

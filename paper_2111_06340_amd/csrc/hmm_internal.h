@@ -90,6 +90,7 @@ struct DevDb {
   const LenParams *lp;          // [max_len + 1]
   const int64_t *coff;          // [n] offset of each target in the caller's residue array
   const int32_t *iperm;         // [n] caller index -> sorted index
+  int32_t prio_by_len;          // 1: the later stages' waves take issue priority by target length
 };
 
 struct DevOut {
@@ -100,6 +101,7 @@ struct DevOut {
   int64_t *counts;
   float *bias;                  // optional bias scores
   int32_t bias_filter;          // 1: composition-bias filter between MSV and Viterbi
+  int32_t fused_tail;           // 1: the stages after MSV as one kernel where an instance exists
 };
 
 // Posterior decoding (hmm_decode): outputs and per-wave scratch.

@@ -1119,6 +1119,7 @@ __global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(De
     if (idx >= count) break;
     const int t = uni(db.list_vit[idx]);
     const int L = uni(db.len[t]);
+    if (db.prio_by_len) length_priority(L, db.max_len);
     const LenParams lp = db.lp[L];
     const VitResult r = vit16_target<Q, TRL>(emit, tr, P, db.res + db.start[t], L, lp, lane, (const uint32_t *)lds + lane);
     const bool pass = r.ovf || r.raw >= lp.thr16;
@@ -1140,6 +1141,96 @@ __global__ void __launch_bounds__(kThreads16<Q>, kMinWaves16<Q>) vit16_kernel(De
 
 __device__ __forceinline__ int fl32(int v) { return max(v, kNeg32); }
 
+// One target's int32 Viterbi score (raw, before the null model), emission
+// rows from `emit` (lane's column of [20][2][Q][64]), transitions `tr`.
+template <int Q>
+__device__ __forceinline__ int vit32_target(const int *emit, const int (&tr)[TR_N][Q], const DevProfile &P,
+                                            const uint8_t *x, int L, const LenParams &lp, int lane) {
+  auto TR = [&](int k, int q) -> int { return tr[k][q]; };
+  const int mv = lp.move16, ej = P.ej16, entry = P.entry16;
+  int M[Q], I[Q], D[Q];
+#pragma unroll
+  for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNeg32;
+  int accM = kNeg32;
+  int xJt = kNeg32;
+  int xB = fl32(mv);
+  int xbe = fl32(xB + entry);
+  int tau = xbe - P.dm_max32;   // delete floor (as in the int16 kernel); >= xbe >= -2^30
+  int T = -ej + 1;
+  auto load = [&](int(&e)[2 * Q], int a) {
+    const int *er = emit + a * (2 * Q * kWave);
+#pragma unroll
+    for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+  };
+  auto row = [&](const int(&em)[2 * Q]) -> bool {
+    const int msh = lane_up_i(M[Q - 1]);
+    const int ish = lane_up_i(I[Q - 1]);
+    const int dsh = lane_up_i(D[Q - 1]);
+    // The oracle floors every add at -2^30.  Here every add saturates
+    // (v_add_i32 clamp), so no sum wraps, and only two floors remain: the
+    // insert maximum's -2^30 and the delete floor tau.  A value below
+    // -2^30 (after an impossible emission or transition) reaches only
+    // maxima that hold a term >= -2^30 -- the match maximum includes xBe,
+    // the insert maximum -2^30, the delete maximum tau -- so it is dropped
+    // there exactly as the oracle's floored -2^30 is, and every state
+    // that is not below -2^30 equals the oracle's.
+#pragma unroll
+    for (int q = Q - 1; q >= 0; q--) {
+      const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
+      const int m = max(max(xbe, sadd32(pm, TR(TR_MMIN, q))),
+                        max(sadd32(pi, TR(TR_IMIN, q)), sadd32(pd, TR(TR_DMIN, q))));
+      const int mn = sadd32(m, em[q]);
+      const int in = sadd32(max(max(sadd32(M[q], TR(TR_MI, q)), sadd32(I[q], TR(TR_II, q))), kNeg32), em[Q + q]);
+      accM = max(accM, mn);
+      M[q] = mn;
+      I[q] = in;
+    }
+    int dc = kNeg32;
+    const int din = lane_up_i(M[Q - 1]);
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+      D[q] = max(max(sadd32(q ? M[q - 1] : din, TR(TR_MDIN, q)), sadd32(dc, TR(TR_DDIN, q))), tau);
+      dc = D[q];
+    }
+    for (int it = 0; it < kWave; it++) {
+      dc = lane_up_i(D[Q - 1]);
+      bool moved = true;
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        if (moved) {
+          const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= tau >= -2^30 already
+          moved = any_lane(nd != D[q]);
+          D[q] = nd;
+          dc = nd;
+        }
+      }
+      if (!moved) break;
+    }
+    if (any_lane(accM >= T)) {
+      const int m = wave_max_i32(accM);
+      xJt = max(xJt, fl32(m + ej));
+      xB = max(fl32(mv), fl32(xJt + mv));
+      xbe = fl32(xB + entry);
+      tau = xbe - P.dm_max32;
+      T = max(xJt, 0) - ej + 1;
+    }
+    return false;
+  };
+  int ea[2 * Q], eb[2 * Q];
+  int stop;
+  (void)drive_rows(x, L, 0, 0, stop, lane, ea, eb, load, row);
+  const int m = wave_max_i32(accM);
+  return fl32(fl32(m + ej) + mv);
+}
+
+template <int Q>
+__device__ __forceinline__ void load_tr32(const DevProfile &P, int lane, int (&tr)[TR_N][Q]) {
+#pragma unroll
+  for (int k = 0; k < TR_N; k++)
+#pragma unroll
+    for (int q = 0; q < Q; q++) tr[k][q] = P.v32_tr[(k * Q + q) * kWave + lane];
+}
+
 template <int Q>
 __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ int32_t lds32[];
@@ -1151,94 +1242,16 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
   for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((int4 *)lds32)[i] = ((const int4 *)P.v32_emit)[i];
   __syncthreads();
   const int *emit = (const int *)lds32 + lane;
-  const int *trp = P.v32_tr + lane;
   int tr[TR_N][Q];
-#pragma unroll
-  for (int k = 0; k < TR_N; k++)
-#pragma unroll
-    for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
-  auto TR = [&](int k, int q) -> int { return tr[k][q]; };
+  load_tr32<Q>(P, lane, tr);
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_OVF], 1);
     if (idx >= count) break;
     const int t = uni(db.list_ovf[idx]);
     const int L = uni(db.len[t]);
+    if (db.prio_by_len) length_priority(L, db.max_len);
     const LenParams lp = db.lp[L];
-    const int mv = lp.move16, ej = P.ej16, entry = P.entry16;
-    int M[Q], I[Q], D[Q];
-#pragma unroll
-    for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = kNeg32;
-    int accM = kNeg32;
-    int xJt = kNeg32;
-    int xB = fl32(mv);
-    int xbe = fl32(xB + entry);
-    int tau = xbe - P.dm_max32;   // delete floor (as in the int16 kernel); >= xbe >= -2^30
-    int T = -ej + 1;
-    auto load = [&](int(&e)[2 * Q], int a) {
-      const int *er = emit + a * (2 * Q * kWave);
-#pragma unroll
-      for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
-    };
-    auto row = [&](const int(&em)[2 * Q]) -> bool {
-      const int msh = lane_up_i(M[Q - 1]);
-      const int ish = lane_up_i(I[Q - 1]);
-      const int dsh = lane_up_i(D[Q - 1]);
-      // The oracle floors every add at -2^30.  Here every add saturates
-      // (v_add_i32 clamp), so no sum wraps, and only two floors remain: the
-      // insert maximum's -2^30 and the delete floor tau.  A value below
-      // -2^30 (after an impossible emission or transition) reaches only
-      // maxima that hold a term >= -2^30 -- the match maximum includes xBe,
-      // the insert maximum -2^30, the delete maximum tau -- so it is dropped
-      // there exactly as the oracle's floored -2^30 is, and every state
-      // that is not below -2^30 equals the oracle's.
-#pragma unroll
-      for (int q = Q - 1; q >= 0; q--) {
-        const int pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-        const int m = max(max(xbe, sadd32(pm, TR(TR_MMIN, q))),
-                          max(sadd32(pi, TR(TR_IMIN, q)), sadd32(pd, TR(TR_DMIN, q))));
-        const int mn = sadd32(m, em[q]);
-        const int in = sadd32(max(max(sadd32(M[q], TR(TR_MI, q)), sadd32(I[q], TR(TR_II, q))), kNeg32), em[Q + q]);
-        accM = max(accM, mn);
-        M[q] = mn;
-        I[q] = in;
-      }
-      int dc = kNeg32;
-      const int din = lane_up_i(M[Q - 1]);
-#pragma unroll
-      for (int q = 0; q < Q; q++) {
-        D[q] = max(max(sadd32(q ? M[q - 1] : din, TR(TR_MDIN, q)), sadd32(dc, TR(TR_DDIN, q))), tau);
-        dc = D[q];
-      }
-      for (int it = 0; it < kWave; it++) {
-        dc = lane_up_i(D[Q - 1]);
-        bool moved = true;
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          if (moved) {
-            const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= tau >= -2^30 already
-            moved = any_lane(nd != D[q]);
-            D[q] = nd;
-            dc = nd;
-          }
-        }
-        if (!moved) break;
-      }
-      if (any_lane(accM >= T)) {
-        const int m = wave_max_i32(accM);
-        xJt = max(xJt, fl32(m + ej));
-        xB = max(fl32(mv), fl32(xJt + mv));
-        xbe = fl32(xB + entry);
-        tau = xbe - P.dm_max32;
-        T = max(xJt, 0) - ej + 1;
-      }
-      return false;
-    };
-    int ea[2 * Q], eb[2 * Q];
-    int stop;
-    (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
-    const int m = wave_max_i32(accM);
-    const int v = fl32(fl32(m + ej) + mv);
-    out.vit[uni(db.perm[t])] = v;
+    out.vit[uni(db.perm[t])] = vit32_target<Q>(emit, tr, P, db.res + db.start[t], L, lp, lane);
   }
 }
 
@@ -1257,6 +1270,112 @@ __global__ void __launch_bounds__(kThreads32) vit32_kernel(DevProfile P, DevDb d
 // of two whenever the largest special value leaves [2^-40, 2^40]; the removed
 // exponents are summed.  Result: ln(C move) + (sum of exponents) ln 2, nats.
 
+// Per-profile register state of the one-wave Forward: transitions, exit
+// weights and the P part of the delete-chain scan (the lane's P before each
+// of the six steps).
+template <int Q>
+struct FwdRegs {
+  float tr[TR_N + 1][Q], gx[Q], pstep[6];
+};
+
+template <int Q>
+__device__ __forceinline__ void load_fwd_regs(const DevProfile &P, int lane, FwdRegs<Q> &R) {
+  const float *trp = P.f_tr + lane;
+#pragma unroll
+  for (int k = 0; k <= TR_N; k++)
+#pragma unroll
+    for (int q = 0; q < Q; q++) R.tr[k][q] = trp[(k * Q + q) * kWave];
+#pragma unroll
+  for (int q = 0; q < Q; q++) R.gx[q] = trp[(TR_EXIT * Q + q) * kWave];   // exit weights: E = sum M g
+  float p = P.f_tr[(TR_N * Q + Q - 1) * kWave + lane];
+#define HMM_PSTEP(I, CTRL, MASK) \
+  R.pstep[I] = p;                \
+  p = p * dpp_f<CTRL, MASK>(p, 1.0f);
+  HMM_PSTEP(0, kRowShr1, 0xf)
+  HMM_PSTEP(1, kRowShr2, 0xf)
+  HMM_PSTEP(2, kRowShr4, 0xf)
+  HMM_PSTEP(3, kRowShr8, 0xf)
+  HMM_PSTEP(4, kRowBcast15, 0xa)
+  HMM_PSTEP(5, kRowBcast31, 0xc)
+#undef HMM_PSTEP
+}
+
+// One target's Forward score in nats (before the null model), emission
+// rows from `emit` (lane's column of [20][2][Q][64]).
+template <int Q>
+__device__ __forceinline__ float fwd_target(const float *emit, const FwdRegs<Q> &R, const DevProfile &P,
+                                            const uint8_t *x, int L, const LenParams &lp, int lane) {
+  auto TR = [&](int k, int q) -> float { return R.tr[k][q]; };
+  const float(&gx)[Q] = R.gx;
+  const float(&pstep)[6] = R.pstep;
+  const float entry_p = P.entry_p;
+  const float loop = lp.loop_p, move = lp.move_p;
+  float M[Q], I[Q], D[Q];
+#pragma unroll
+  for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = 0.0f;
+  float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
+  int shift = 0;
+  auto load = [&](float(&e)[2 * Q], int a) {
+    const float *er = emit + a * (2 * Q * kWave);
+#pragma unroll
+    for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
+  };
+  auto row = [&](const float(&em)[2 * Q]) -> bool {
+    const float bent = B * entry_p;
+    // the first cell's predecessors are the previous lane's last cells
+    // (none in lane 0), read through the lane shift of each multiply-add
+    float sm0 = bent;
+    fmac_up3(sm0, D[Q - 1], TR(TR_DMIN, 0), I[Q - 1], TR(TR_IMIN, 0), M[Q - 1], TR(TR_MMIN, 0));
+    float part = 0.0f;   // this lane's part of E: sum of M g (deletes included through g)
+#pragma unroll
+    for (int q = Q - 1; q >= 0; q--) {
+      const float sm =
+          q ? fmaf(M[q - 1], TR(TR_MMIN, q), fmaf(I[q - 1], TR(TR_IMIN, q), fmaf(D[q - 1], TR(TR_DMIN, q), bent)))
+            : sm0;
+      const float si = fmaf(M[q], TR(TR_MI, q), I[q] * TR(TR_II, q));
+      M[q] = em[q] * sm;
+      I[q] = em[Q + q] * si;
+      part = fmaf(M[q], gx[q], part);
+    }
+    // delete chain inside the lane from a zero entry (the first cell's M
+    // predecessor is the previous lane's new last M)
+    D[0] = mul_up(M[Q - 1], TR(TR_MDIN, 0));
+#pragma unroll
+    for (int q = 1; q < Q; q++) D[q] = fmaf(M[q - 1], TR(TR_MDIN, q), D[q - 1] * TR(TR_DDIN, q));
+    const float carry = lane_up_f(affine_scan_fused(D[Q - 1], pstep));
+#pragma unroll
+    for (int q = 0; q < Q; q++) D[q] = fmaf(carry, TR(TR_N, q), D[q]);
+    const float E = wave_sum_fused(part);
+    J = fmaf(J, loop, 0.5f * E);
+    C = fmaf(C, loop, 0.5f * E);
+    N = N * loop;
+    B = (N + J) * move;
+    const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
+    if (big > 0x1p40f || big < 0x1p-40f) {
+      int ex;
+      (void)frexpf(big, &ex);
+      ex = uni(ex);
+      const float s = ldexpf(1.0f, -ex);
+#pragma unroll
+      for (int q = 0; q < Q; q++) {
+        M[q] *= s;
+        I[q] *= s;
+        D[q] *= s;
+      }
+      J *= s;
+      C *= s;
+      N *= s;
+      B *= s;
+      shift += ex;
+    }
+    return false;
+  };
+  float ea[2 * Q], eb[2 * Q];
+  int stop;
+  (void)drive_rows(x, L, 0, 0, stop, lane, ea, eb, load, row);
+  return (float)(log((double)C * (double)move) + (double)shift * M_LN2);
+}
+
 template <int Q>
 __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db, DevOut out) {
   extern __shared__ float ldsf[];
@@ -1268,114 +1387,102 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
   for (int i = threadIdx.x; i < kEmit / 4; i += blockDim.x) ((float4 *)ldsf)[i] = ((const float4 *)P.f_emit)[i];
   __syncthreads();
   const float *emit = (const float *)ldsf + lane;
-  const float *trp = P.f_tr + lane;
-  float tr[TR_N + 1][Q], gx[Q];
-#pragma unroll
-  for (int k = 0; k <= TR_N; k++)
-#pragma unroll
-    for (int q = 0; q < Q; q++) tr[k][q] = trp[(k * Q + q) * kWave];
-#pragma unroll
-  for (int q = 0; q < Q; q++) gx[q] = trp[(TR_EXIT * Q + q) * kWave];   // exit weights: E = sum M g
-  auto TR = [&](int k, int q) -> float { return tr[k][q]; };
-  // P part of the delete-chain scan: the lane's P before each of the six steps
-  float pstep[6];
-  {
-    float p = P.f_tr[(TR_N * Q + Q - 1) * kWave + lane];
-#define HMM_PSTEP(I, CTRL, MASK)           \
-  pstep[I] = p;                            \
-  p = p * dpp_f<CTRL, MASK>(p, 1.0f);
-    HMM_PSTEP(0, kRowShr1, 0xf)
-    HMM_PSTEP(1, kRowShr2, 0xf)
-    HMM_PSTEP(2, kRowShr4, 0xf)
-    HMM_PSTEP(3, kRowShr8, 0xf)
-    HMM_PSTEP(4, kRowBcast15, 0xa)
-    HMM_PSTEP(5, kRowBcast31, 0xc)
-#undef HMM_PSTEP
-  }
-  const float entry_p = P.entry_p;
+  FwdRegs<Q> R;
+  load_fwd_regs<Q>(P, lane, R);
   for (;;) {
     const int idx = wave_fetch_add(&db.counters[CNT_WORK_FWD], 1);
     if (idx >= count) break;
     const int t = uni(db.list_fwd[idx]);
     const int L = uni(db.len[t]);
+    if (db.prio_by_len) length_priority(L, db.max_len);
     const LenParams lp = db.lp[L];
-    const float loop = lp.loop_p, move = lp.move_p;
-    float M[Q], I[Q], D[Q];
-#pragma unroll
-    for (int q = 0; q < Q; q++) M[q] = I[q] = D[q] = 0.0f;
-    float N = 1.0f, B = move, J = 0.0f, C = 0.0f;
-    int shift = 0;
-    auto load = [&](float(&e)[2 * Q], int a) {
-      const float *er = emit + a * (2 * Q * kWave);
-#pragma unroll
-      for (int q = 0; q < 2 * Q; q++) e[q] = er[q * kWave];
-    };
-    auto row = [&](const float(&em)[2 * Q]) -> bool {
-      const float msh = lane_up_f(M[Q - 1]);
-      const float ish = lane_up_f(I[Q - 1]);
-      const float dsh = lane_up_f(D[Q - 1]);
-      const float bent = B * entry_p;
-      float part = 0.0f;   // this lane's part of E: sum of M g (deletes included through g)
-#pragma unroll
-      for (int q = Q - 1; q >= 0; q--) {
-        const float pm = q ? M[q - 1] : msh, pi = q ? I[q - 1] : ish, pd = q ? D[q - 1] : dsh;
-        const float sm = fmaf(pm, TR(TR_MMIN, q), fmaf(pi, TR(TR_IMIN, q), fmaf(pd, TR(TR_DMIN, q), bent)));
-        const float si = fmaf(M[q], TR(TR_MI, q), I[q] * TR(TR_II, q));
-        M[q] = em[q] * sm;
-        I[q] = em[Q + q] * si;
-        part = fmaf(M[q], gx[q], part);
-      }
-      const float din = lane_up_f(M[Q - 1]);
-      float dc = 0.0f;
-#pragma unroll
-      for (int q = 0; q < Q; q++) {
-        D[q] = fmaf(q ? M[q - 1] : din, TR(TR_MDIN, q), dc * TR(TR_DDIN, q));
-        dc = D[q];
-      }
-      float sa = D[Q - 1];
-      sa = fmaf(pstep[0], dpp_f<kRowShr1, 0xf>(sa, 0.0f), sa);
-      sa = fmaf(pstep[1], dpp_f<kRowShr2, 0xf>(sa, 0.0f), sa);
-      sa = fmaf(pstep[2], dpp_f<kRowShr4, 0xf>(sa, 0.0f), sa);
-      sa = fmaf(pstep[3], dpp_f<kRowShr8, 0xf>(sa, 0.0f), sa);
-      sa = fmaf(pstep[4], dpp_f<kRowBcast15, 0xa>(sa, 0.0f), sa);
-      sa = fmaf(pstep[5], dpp_f<kRowBcast31, 0xc>(sa, 0.0f), sa);
-      const float carry = lane_up_f(sa);
-#pragma unroll
-      for (int q = 0; q < Q; q++) D[q] = fmaf(carry, TR(TR_N, q), D[q]);
-      const float E = wave_sum_f(part);
-      J = fmaf(J, loop, 0.5f * E);
-      C = fmaf(C, loop, 0.5f * E);
-      N = N * loop;
-      B = (N + J) * move;
-      const float big = fmaxf(fmaxf(fmaxf(E, J), fmaxf(C, N)), B);
-      if (big > 0x1p40f || big < 0x1p-40f) {
-        int ex;
-        (void)frexpf(big, &ex);
-        ex = uni(ex);
-        const float s = ldexpf(1.0f, -ex);
-#pragma unroll
-        for (int q = 0; q < Q; q++) {
-          M[q] *= s;
-          I[q] *= s;
-          D[q] *= s;
-        }
-        J *= s;
-        C *= s;
-        N *= s;
-        B *= s;
-        shift += ex;
-      }
-      return false;
-    };
-    float ea[2 * Q], eb[2 * Q];
-    int stop;
-    (void)drive_rows(db.res + db.start[t], L, 0, 0, stop, lane, ea, eb, load, row);
-    const float f = (float)(log((double)C * (double)move) + (double)shift * M_LN2);
+    const float f = fwd_target<Q>(emit, R, P, db.res + db.start[t], L, lp, lane);
     const bool pass = f > lp.fthr;
     const uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_FWD_RAN | (pass ? HMM_FWD_PASS : 0));
     db.flags_sorted[t] = fl;
     out.fwd[uni(db.perm[t])] = f;
     if (pass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
+  }
+}
+
+// ============================================================================ fused tail
+//
+// For profiles of up to 384 nodes (3 int16 vectors per lane) the three
+// stages after MSV run as one kernel: a wave takes an MSV survivor, scores
+// it with the int16 Viterbi, rescores it in int32 at once if it overflowed,
+// and runs Forward on it at once if it passed.  The staged kernels each wait
+// for the longest target of the stage before them; here a target's stages
+// follow each other without waiting for any other target, and a launch ends
+// when its last wave's chain of stages does.  The three emission tables sit
+// in LDS side by side (10 KB per int16 vector, 20 KB per 32-bit vector,
+// twice); transitions are read per target and stage, so that no stage's
+// registers stay live through the others.  Results, flags and counts are
+// the staged kernels' (the survivor lists between the stages are not
+// written).
+template <int Q8>
+constexpr int kThreadsTail = Q8 <= 2 ? 1024 : 512;
+
+template <int Q8, int Q32>
+__global__ void __launch_bounds__(kThreadsTail<Q8>) tail_kernel(DevProfile P, DevDb db, DevOut out) {
+  extern __shared__ uint32_t ldst[];
+  const int lane = threadIdx.x & 63;
+  constexpr int n16 = kAlpha * 2 * Q8 * kWave, n32 = kAlpha * 2 * Q32 * kWave;   // dwords
+  // a launch with no target returns before staging its tables
+  const int count = uni(__atomic_load_n(&db.counters[CNT_VIT], __ATOMIC_RELAXED));
+  if (count == 0) return;
+  for (int i = threadIdx.x; i < n16 / 4; i += blockDim.x) ((uint4 *)ldst)[i] = ((const uint4 *)P.vit_emit)[i];
+  for (int i = threadIdx.x; i < n32 / 4; i += blockDim.x) {
+    ((uint4 *)(ldst + n16))[i] = ((const uint4 *)P.v32_emit)[i];
+    ((uint4 *)(ldst + n16 + n32))[i] = ((const uint4 *)P.f_emit)[i];
+  }
+  __syncthreads();
+  const uint32_t *e16 = ldst + lane;
+  const int *e32 = (const int *)ldst + n16 + lane;
+  const float *ef = (const float *)ldst + n16 + n32 + lane;
+  for (;;) {
+    const int idx = wave_fetch_add(&db.counters[CNT_WORK_VIT], 1);
+    if (idx >= count) break;
+    const int t = uni(db.list_vit[idx]);
+    const int L = uni(db.len[t]);
+    if (db.prio_by_len) length_priority(L, db.max_len);
+    const LenParams lp = db.lp[L];
+    const uint8_t *x = db.res + db.start[t];
+    // the transition reads' lane offset, opaque to the compiler: otherwise
+    // it keeps every read's address live through the loop
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    VitResult r;
+    {
+      uint32_t tr[TR_N][Q8];
+#pragma unroll
+      for (int k = 0; k < TR_N; k++)
+#pragma unroll
+        for (int q = 0; q < Q8; q++) tr[k][q] = P.vit_tr[(k * Q8 + q) * kWave + ln];
+      r = vit16_target<Q8>(e16, tr, P, x, L, lp, lane);
+    }
+    const bool pass = r.ovf || r.raw >= lp.thr16;
+    int vit = r.raw;
+    if (r.ovf) {
+      (void)wave_fetch_add(&db.counters[CNT_OVF], 1);
+      int tr[TR_N][Q32];
+      load_tr32<Q32>(P, ln, tr);
+      vit = vit32_target<Q32>(e32, tr, P, x, L, lp, lane);
+    }
+    const int c = uni(db.perm[t]);
+    out.vit[c] = vit;
+    uint8_t fl = (uint8_t)(uni(db.flags_sorted[t]) | HMM_VIT_RAN | (pass ? HMM_VIT_PASS : 0) |
+                           (r.ovf ? HMM_VIT_OVF : 0));
+    if (pass) {
+      (void)wave_fetch_add(&db.counters[CNT_FWD], 1);
+      FwdRegs<Q32> R;
+      load_fwd_regs<Q32>(P, ln, R);
+      const float f = fwd_target<Q32>(ef, R, P, x, L, lp, lane);
+      const bool fpass = f > lp.fthr;
+      fl |= (uint8_t)(HMM_FWD_RAN | (fpass ? HMM_FWD_PASS : 0));
+      out.fwd[c] = f;
+      if (fpass) (void)wave_fetch_add(&db.counters[CNT_FWD_PASS], 1);
+    }
+    db.flags_sorted[t] = fl;
   }
 }
 
@@ -1535,6 +1642,29 @@ hipError_t launch_fwd(const DevProfile &P, const DevDb &db, const DevOut &o, hip
   return launch_list_kernel(fwd_kernel<Q>, kThreads32, bpc, lds, P, db, o, s);
 }
 
+// Fused tail (profiles of up to 3 int16 vectors per lane): the three
+// emission tables in LDS, as many blocks as fit, at most one wave per target.
+template <int Q8, int Q32>
+hipError_t launch_tail_fused(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+  const size_t lds = (size_t)kAlpha * 2 * kWave * 4 * (Q8 + 2 * Q32);
+  static int bpc = 0;
+  return launch_list_kernel(tail_kernel<Q8, Q32>, kThreadsTail<Q8>, bpc, lds, P, db, o, s);
+}
+
+// The int16 / 32-bit vector counts with a fused-tail instance.
+bool tail_fused_instance(const DevProfile &P) {
+  return (P.Q8 == 1 && P.Q32 <= 2) || (P.Q8 == 2 && (P.Q32 == 3 || P.Q32 == 4)) ||
+         (P.Q8 == 3 && (P.Q32 == 5 || P.Q32 == 6));
+}
+
+hipError_t dispatch_tail_fused(const DevProfile &P, const DevDb &db, const DevOut &o, hipStream_t s) {
+#define HMM_TAIL(a, b) \
+  if (P.Q8 == a && P.Q32 == b) return launch_tail_fused<a, b>(P, db, o, s);
+  HMM_TAIL(1, 1) HMM_TAIL(1, 2) HMM_TAIL(2, 3) HMM_TAIL(2, 4) HMM_TAIL(3, 5) HMM_TAIL(3, 6)
+#undef HMM_TAIL
+  return hipErrorInvalidValue;
+}
+
 #define HMM_Q8_CASES(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(10) X(12) X(14) X(16) X(20) X(24)
 // One-wave instances of the 32-bit kernels; 14 and more vectors per lane
 // (14, 16, 20, 24, 28, 32, 40, 48) run the cooperative ones.
@@ -1665,7 +1795,9 @@ hipError_t launch_search(const DevProfile &P, const DevDb *chunk, int K, const D
 // The rest of each chunk's cascade as soon as its MSV is done (event
 // y.msv_done[k] on the search stream).  An int16 overflow passes the
 // Viterbi filter whatever its exact score, so Forward needs nothing from
-// the rescore: the two run side by side.  The counts and the caller-order
+// the rescore: the two run side by side.  With `o.fused_tail` and a profile
+// that has a fused instance, one kernel takes all three stages instead (the
+// rescore stream then has nothing to run).  The counts and the caller-order
 // results follow on the tail stream, whose end (y.tail_done) the search
 // stream waits for when `join` is set (a group of searches joins them all
 // at its end instead).
@@ -1679,15 +1811,22 @@ hipError_t launch_tail(const DevProfile &P, const DevDb *chunk, int K, const Dev
   auto mark = [&](int i, hipStream_t st) {
     if (ev) ok(hipEventRecord(ev[i], st));
   };
+  const bool fused = o.fused_tail && tail_fused_instance(P);
   for (int k = 0; k < K && e == hipSuccess; k++) {
     const bool any = chunk[k].n > 0;
+    // the last chunk's stages end the search: their waves take issue
+    // priority by target length (an earlier chunk's share the CUs with the
+    // next chunk's MSV, which they would hold back)
+    DevDb ck = chunk[k];
+    ck.prio_by_len = k == K - 1;
     if (!ok(hipStreamWaitEvent(y.tail, y.msv_done[k], 0))) break;
-    if (any && !ok(dispatch_vit16(P, chunk[k], o, y.tail))) break;
+    if (any && !ok(fused ? dispatch_tail_fused(P, ck, o, y.tail) : dispatch_vit16(P, ck, o, y.tail))) break;
     if (!ok(hipEventRecord(y.vit_done[k], y.tail))) break;
     if (k == K - 1) mark(2, y.tail);
     if (!ok(hipStreamWaitEvent(y.aux, y.vit_done[k], 0))) break;
-    if (any && !ok(dispatch_vit32(P, chunk[k], o, y.aux))) break;
-    if (any && !ok(dispatch_fwd(P, chunk[k], o, y.tail))) break;
+    if (fused) continue;
+    if (any && !ok(dispatch_vit32(P, ck, o, y.aux))) break;
+    if (any && !ok(dispatch_fwd(P, ck, o, y.tail))) break;
   }
   mark(3, y.aux);
   if (ok(hipEventRecord(y.aux_done, y.aux))) ok(hipStreamWaitEvent(y.tail, y.aux_done, 0));

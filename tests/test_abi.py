@@ -118,6 +118,9 @@ def test_search_rejects_null_handles():
     assert hg.lib().hmm_search(None, None, C.byref(t), C.byref(r), None) == hg.HMM_EINVAL
     assert hg.lib().hmm_profile_free(None) == hg.HMM_OK
     assert hg.lib().hmm_db_free(None) == hg.HMM_OK
+    cur = C.c_int32(-7)
+    assert hg.lib().hmm_db_fused_tail(None, 2, C.byref(cur)) == hg.HMM_EINVAL and cur.value == -7
+    assert hg.lib().hmm_db_pipeline(None, 2, C.byref(cur)) == hg.HMM_EINVAL and cur.value == -7
 
 
 def _gpu_present():

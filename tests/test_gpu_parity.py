@@ -38,12 +38,13 @@ def gpu():
     return torch
 
 
-def run_gpu(prof, residues, offsets, calib, F, stream=None):
+def run_gpu(prof, residues, offsets, calib, F, stream=None, tail_mode=0):
     import torch
     P = hg.Profile(prof, *calib)
     D = hg.Database(residues, offsets)
     out = hg.alloc_results(D.n)
-    announce(f"search M={prof.M} n={D.n} residues={D.n_residues} max_len={D.max_len} F={F}")
+    mode = hg.hmm_db_fused_tail(D.handle, tail_mode)
+    announce(f"search M={prof.M} n={D.n} residues={D.n_residues} max_len={D.max_len} F={F} tail mode {mode}")
     hg.search(P, D, F, out, stream=stream)
     torch.cuda.synchronize()
     res = {k: v.cpu().numpy() for k, v in out.items()}
@@ -343,6 +344,57 @@ def test_overflow_and_rescore(M):
         st = compare(g, o, what=f"peaked M={M}")
         assert st["vit_ovf"] >= 1 and st["msv_ovf"] >= 1
         announce(f"overflow M={M} F={F} ok {st}")
+
+
+@pytest.mark.parametrize("M", [40, 64, 65, 77, 128, 129, 200, 256, 257, 320, 384, 385])
+def test_fused_and_staged_tails_agree(M):
+    """Profiles up to 384 nodes can run Viterbi, rescore and Forward as one
+    kernel (hmm_db_fused_tail mode 2; by default when F2 = 1); the staged
+    kernels (mode 1) must give the same results, bit for bit, and both the
+    oracle's.  A
+    peaked profile against its planted homologs (int16 overflows, several
+    hits), mutated copies and background, and a profile with random per-node
+    transitions; open cutoffs and the filter cutoffs; the counts as well."""
+    import torch
+    peaked, c = _peaked(M, 1000 + M)
+    rng = np.random.default_rng(M)
+    seqs = [c, np.concatenate([gen.background_residues(rng, 60), c, gen.background_residues(rng, 700)])]
+    for d in (0.1, 0.3, 0.5):
+        mut = c.copy()
+        m = rng.random(M) < d
+        mut[m] = rng.integers(0, 20, size=int(m.sum()))
+        seqs.append(mut)
+    seqs.append(np.concatenate([c[: M // 2], c[M // 3:]]))
+    seqs += [gen.background_residues(rng, int(n)) for n in rng.integers(1, 1500, size=40)]
+    off = np.zeros(len(seqs) + 1, np.int64)
+    off[1:] = np.cumsum([s.size for s in seqs])
+    res = np.concatenate(seqs)
+    rand = random_profile(M, 300 + M, alpha=0.3, talpha=0.6)
+    for prof, calib in ((peaked, (-8.0, -9.0, -4.0)), (rand, (0.0, 0.0, 0.0))):
+        for F in ((1.0, 1.0, 1.0), (0.02, 1e-3, 1.0)):
+            o = oracle_search(prof, res, off, calib, F)
+            got = {}
+            for mode in (1, 2):
+                P = hg.Profile(prof, *calib)
+                D = hg.Database(res, off)
+                assert hg.hmm_db_fused_tail(D.handle) == 3    # the default: fused when F2 = 1
+                assert hg.hmm_db_fused_tail(D.handle, mode) == mode
+                out = hg.alloc_results(D.n)
+                announce(f"tails M={M} mode={mode} F={F}")
+                hg.search(P, D, F, out)
+                torch.cuda.synchronize()
+                got[mode] = {k: v.cpu().numpy() for k, v in out.items()}
+                P.close()
+                D.close()
+                st = compare(got[mode], o, what=f"tail mode {mode} M={M} F={F}")
+                fl = o["flags"]
+                assert got[mode]["counts"][1] == np.sum((fl & hg.HMM_VIT_OVF) != 0)
+                assert got[mode]["counts"][2] == np.sum((fl & hg.HMM_VIT_PASS) != 0)
+                assert got[mode]["counts"][3] == np.sum((fl & hg.HMM_FWD_PASS) != 0)
+            for k in ("msv", "vit", "flags", "counts"):
+                assert np.array_equal(got[1][k], got[2][k]), k
+            assert np.array_equal(got[1]["fwd"].view(np.uint32), got[2]["fwd"].view(np.uint32))
+            announce(f"tails M={M} F={F} agree {st}")
 
 
 @pytest.mark.parametrize("M", [700, 900, 1500, 2600])
