@@ -71,6 +71,7 @@ enum { TR_PRE = TR_N, TR_SUF = TR_N + 1, TR_EXIT = TR_N + 2 };
 enum {
   CNT_VIT = 0, CNT_OVF, CNT_FWD, CNT_FWD_PASS, CNT_WORK_VIT, CNT_WORK_OVF, CNT_WORK_FWD,
   CNT_DEC, CNT_WORK_DEC, CNT_NDOM,   // posterior decoding: list size, work counter, domains found
+  CNT_WORK_MSV,                      // MSV: runs of targets taken
   CNT_N = 16
 };
 

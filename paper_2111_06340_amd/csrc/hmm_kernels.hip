@@ -290,6 +290,9 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
   }
 }
 
+// Targets per run an MSV wave takes from its launch's work counter.
+constexpr int kMsvRun = 8;
+
 struct MsvResult {
   int raw;
   bool ovf;
@@ -501,7 +504,6 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
   const int entry8 = P.entry8, exit8 = P.exit8;
   const int ovf_line = 255 - P.bias8;
   const uint32_t *tab = lds + lane;
@@ -512,17 +514,20 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   for (int q = 0; q < Q; q++) da[q] = dbuf[q] = 0;
   // packed fp16 pair (v, v) as a wave-uniform dword
   auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
-  // The next target's length and start are read during the current
+  // Targets come in runs of consecutive (sorted) targets from the launch's
+  // work counter, so that waves slowed by other kernels on their CU take
+  // fewer.  The next target's length and start are read during the current
   // target's epilogue, so a target starts with one round trip (its length
   // parameters and first residue chunks, in parallel) instead of three.
-  int t = wave_id();
+  int t = wave_fetch_add(&db.counters[CNT_WORK_MSV], 1) * kMsvRun;
+  int tend = min(t + kMsvRun, n);
   int Lnext = 0;
   int64_t snext = 0;
   if (t < n) {
     Lnext = uni(db.len[t]);
     snext = db.start[t];
   }
-  for (; t < n; t += nw) {
+  while (t < n) {
     const int L = Lnext;
     const uint8_t *x = db.res + snext;
     const LenParams lp = db.lp[L];
@@ -620,9 +625,14 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     }
     const bool ovf = res.ovf;
     const int raw = res.raw;
-    if (t + nw < n) {
-      Lnext = uni(db.len[t + nw]);
-      snext = db.start[t + nw];
+    int tn = t + 1;
+    if (tn >= tend) {
+      tn = wave_fetch_add(&db.counters[CNT_WORK_MSV], 1) * kMsvRun;
+      tend = min(tn + kMsvRun, n);
+    }
+    if (tn < n) {
+      Lnext = uni(db.len[tn]);
+      snext = db.start[tn];
     }
     const bool pass = ovf || raw >= lp.thr8;
     const uint8_t fl = (pass ? HMM_MSV_PASS : 0) | (ovf ? HMM_MSV_OVF : 0);
@@ -636,6 +646,7 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
       const bool bf = out.bias_filter != 0;
       (bf ? db.list_ovf : db.list_vit)[wave_fetch_add(&db.counters[bf ? CNT_OVF : CNT_VIT], 1)] = t;
     }
+    t = tn;
   }
 }
 
@@ -684,7 +695,6 @@ msv_group_kernel(MsvGroup<G> A) {
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
   const DevDb &D0 = A.db[0];
   const int n = (int)D0.n;
   auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
@@ -692,14 +702,18 @@ msv_group_kernel(MsvGroup<G> A) {
   uint32_t ca[G * Q], cb[G * Q];
 #pragma unroll
   for (int i = 0; i < G * Q; i++) ca[i] = cb[i] = 0;
-  int t = wave_id();
+  // runs of consecutive targets from the launch's work counter (the first
+  // profile's), as in the single-profile kernel
+  int32_t *work = &D0.counters[CNT_WORK_MSV];
+  int t = wave_fetch_add(work, 1) * kMsvRun;
+  int tend = min(t + kMsvRun, n);
   int Lnext = 0;
   int64_t snext = 0;
   if (t < n) {
     Lnext = uni(D0.len[t]);
     snext = D0.start[t];
   }
-  for (; t < n; t += nw) {
+  while (t < n) {
     const int L = Lnext;
     const uint8_t *x = D0.res + snext;
     int mv[G], base[G], xJt[G], Bx[G], ovf_line[G];
@@ -885,9 +899,14 @@ msv_group_kernel(MsvGroup<G> A) {
       r = next_phase(stop);
       if (r >= L) break;
     }
-    if (t + nw < n) {
-      Lnext = uni(D0.len[t + nw]);
-      snext = D0.start[t + nw];
+    int tn = t + 1;
+    if (tn >= tend) {
+      tn = wave_fetch_add(work, 1) * kMsvRun;
+      tend = min(tn + kMsvRun, n);
+    }
+    if (tn < n) {
+      Lnext = uni(D0.len[tn]);
+      snext = D0.start[tn];
     }
 #pragma unroll
     for (int g = 0; g < G; g++) {
@@ -907,6 +926,7 @@ msv_group_kernel(MsvGroup<G> A) {
         (bf ? Dg.list_ovf : Dg.list_vit)[wave_fetch_add(&Dg.counters[bf ? CNT_OVF : CNT_VIT], 1)] = t;
       }
     }
+    t = tn;
   }
 }
 
@@ -1867,6 +1887,13 @@ hipError_t launch_search_group(const DevProfile *P, const DevDb *db, const DevOu
     ok(hipGetLastError());
   }
   std::vector<int> done(n, 0);
+  // a search's composition-bias filter (if on) and its cascade tail, on its
+  // own handle's streams once its MSV (on `s`) is done
+  auto tail = [&](int i) {
+    if (o[i].bias_filter && db[i].n > 0) ok(launch_bias(P[i], db[i], o[i], s));
+    ok(hipEventRecord(y[i]->msv_done[0], s));
+    ok(launch_tail(P[i], &db[i], 1, o[i], s, *y[i], nullptr, false));
+  };
   for (int i = 0; i < n && e == hipSuccess; i++) {
     if (done[i] || db[i].n == 0) continue;
     const int gmax = P[i].msv_diag ? msv_group_max(P[i].Qm) : 1;
@@ -1888,14 +1915,11 @@ hipError_t launch_search_group(const DevProfile *P, const DevDb *db, const DevOu
       ok(dispatch_msv_group(gp, gd, go, (int)grp.size(), s));
     }
   }
-  // The tails start after every MSV launch: started earlier, they take
-  // CUs from the next MSV launches, whose waves each take a fixed share of
-  // the targets, and the whole group takes longer (C4: 412 against 378 ms).
-  for (int i = 0; i < n && e == hipSuccess; i++) {
-    if (o[i].bias_filter && db[i].n > 0) ok(launch_bias(P[i], db[i], o[i], s));
-    ok(hipEventRecord(y[i]->msv_done[0], s));
-  }
-  for (int i = 0; i < n && e == hipSuccess; i++) ok(launch_tail(P[i], &db[i], 1, o[i], s, *y[i], nullptr, false));
+  // The tails start after every MSV launch.  Started right after their own
+  // group's launch, they share the CUs with the later MSV launches, which
+  // absorb that (their waves take targets from a work counter), but the
+  // group still took longer (C4: 350.7 against 345.0 ms).
+  for (int i = 0; i < n && e == hipSuccess; i++) tail(i);
   // every search's tail joins the caller's stream
   for (int i = 0; i < n && e == hipSuccess; i++) ok(hipStreamWaitEvent(s, y[i]->tail_done, 0));
   return e;
