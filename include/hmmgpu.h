@@ -364,9 +364,8 @@ int hmm_probe_pk16(hmm_stream stream, double *ops_per_s, float *ms);
  * chunks run back to back on the search stream while the Viterbi, rescore
  * and Forward of each finished chunk run on the handle's own streams beside
  * them.  Results do not depend on it.  chunks = 0 changes nothing;
- * *current (if non-NULL) receives the count in force.  The default is 4 for
- * databases of at least 512 Mi residues, 2 from 128 Mi residues, else 1
- * (plain sequential stages, which is what per-stage timing needs).
+ * *current (if non-NULL) receives the count in force.  The default is 1
+ * (plain sequential stages, which is also what per-stage timing needs).
  * Errors: HMM_EINVAL (NULL db, chunks outside 0..8). */
 int hmm_db_pipeline(hmm_db *db, int32_t chunks, int32_t *current);
 

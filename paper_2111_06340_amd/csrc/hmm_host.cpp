@@ -678,15 +678,14 @@ int hmm_db_upload(const uint8_t *residues, const int64_t *offsets, int64_t n, hm
   db->n_res = n_res;
   db->max_len = max_len;
   memcpy(db->chunk_at, chunk_at, sizeof chunk_at);
-  // Pipelining pays once a chunk's MSV outlasts the tail it hides.  Two
-  // chunks measured best on a 348M-residue database (M = 734): each MSV
-  // kernel fills every CU's LDS, so a chunk's Viterbi runs mostly after the
-  // next MSV and more chunks only add MSV launches.  On a 707M-residue one
-  // (M = 2500) four chunks beat two by 2.5 %: its long targets' rescore and
-  // Forward run with one workgroup per target and leave room beside MSV.
-  // Below about 128 Mi residues one chunk is better (69M residues, M = 256:
-  // 2.55 against 2.63 ms): the MSV kernels are too short to hide a tail.
-  db->chunks = n_res >= ((int64_t)512 << 20) ? 4 : n_res >= ((int64_t)128 << 20) ? 2 : 1;
+  // One chunk: each MSV kernel fills every CU's LDS, so a chunk's Viterbi
+  // runs mostly after the next MSV anyway, and every chunk adds an MSV
+  // launch and its drain.  Since the MSV waves take their targets from a
+  // work counter (no wave is left with a slow share), the sequential search
+  // is the fastest measured: 348M residues, M = 734: 14.34 ms against 14.64
+  // for two chunks and 15.17 for three; 707M residues, M = 2500: 111.0 ms
+  // against 111.8 for two, 112.9 for three and 113.3 for four.
+  db->chunks = 1;
   db->data = new (std::nothrow) hmm_db_data();
   if (!db->data) {
     delete db;
