@@ -290,8 +290,28 @@ __device__ __forceinline__ bool drive_pairs(const uint8_t *x, int L, int r0, int
   }
 }
 
-// Targets per run an MSV wave takes from its launch's work counter.
+// Runs of consecutive (sorted) targets for the MSV waves, taken from the
+// launch's work counter, so that waves slowed by other kernels on their CU,
+// or by longer targets, take fewer.  A run is 8 targets, or fewer where the
+// waves would otherwise get fewer than 4 runs each.  When there are no more
+// runs than waves (a small database), wave w takes run w and no counter is
+// used: the atomics alone would outlast the work (5,000 targets at M = 77:
+// 0.23 against 0.13 ms).  Measured and not kept: a first run by wave index
+// before the counter's (C2 MSV 1.51 against 1.30 ms), and a plain read of
+// the counter before each bump, to leave without an atomic once the runs
+// are gone (1.65 ms).
 constexpr int kMsvRun = 8;
+struct MsvRuns {
+  int32_t *work;
+  int n, run, nw, nruns;
+  __device__ MsvRuns(int32_t *w, int n_) : work(w), n(n_) {
+    nw = uni((int)gridDim.x * (int)(blockDim.x >> 6));
+    run = max(1, min(kMsvRun, n / (4 * nw)));
+    nruns = (n + run - 1) / run;
+  }
+  __device__ int first() const { return nruns <= nw ? wave_id() : wave_fetch_add(work, 1); }
+  __device__ int next() const { return nruns <= nw ? nruns : wave_fetch_add(work, 1); }
+};
 
 struct MsvResult {
   int raw;
@@ -514,13 +534,13 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
   for (int q = 0; q < Q; q++) da[q] = dbuf[q] = 0;
   // packed fp16 pair (v, v) as a wave-uniform dword
   auto splat = [](int v) -> uint32_t { return (uint32_t)uni((int)as_u(h2_splat(v))); };
-  // Targets come in runs of consecutive (sorted) targets from the launch's
-  // work counter, so that waves slowed by other kernels on their CU take
-  // fewer.  The next target's length and start are read during the current
-  // target's epilogue, so a target starts with one round trip (its length
-  // parameters and first residue chunks, in parallel) instead of three.
-  int t = wave_fetch_add(&db.counters[CNT_WORK_MSV], 1) * kMsvRun;
-  int tend = min(t + kMsvRun, n);
+  // Targets in runs (MsvRuns).  The next target's length and start are read
+  // during the current target's epilogue, so a target starts with one round
+  // trip (its length parameters and first residue chunks, in parallel)
+  // instead of three.
+  const MsvRuns runs(&db.counters[CNT_WORK_MSV], n);
+  int t = runs.first() * runs.run;
+  int tend = min(t + runs.run, n);
   int Lnext = 0;
   int64_t snext = 0;
   if (t < n) {
@@ -627,8 +647,8 @@ __global__ void __launch_bounds__(1024) msv_kernel(DevProfile P, DevDb db, DevOu
     const int raw = res.raw;
     int tn = t + 1;
     if (tn >= tend) {
-      tn = wave_fetch_add(&db.counters[CNT_WORK_MSV], 1) * kMsvRun;
-      tend = min(tn + kMsvRun, n);
+      tn = runs.next() * runs.run;
+      tend = min(tn + runs.run, n);
     }
     if (tn < n) {
       Lnext = uni(db.len[tn]);
@@ -702,11 +722,11 @@ msv_group_kernel(MsvGroup<G> A) {
   uint32_t ca[G * Q], cb[G * Q];
 #pragma unroll
   for (int i = 0; i < G * Q; i++) ca[i] = cb[i] = 0;
-  // runs of consecutive targets from the launch's work counter (the first
-  // profile's), as in the single-profile kernel
-  int32_t *work = &D0.counters[CNT_WORK_MSV];
-  int t = wave_fetch_add(work, 1) * kMsvRun;
-  int tend = min(t + kMsvRun, n);
+  // targets in runs, as in the single-profile kernel (the work counter is
+  // the first profile's)
+  const MsvRuns runs(&D0.counters[CNT_WORK_MSV], n);
+  int t = runs.first() * runs.run;
+  int tend = min(t + runs.run, n);
   int Lnext = 0;
   int64_t snext = 0;
   if (t < n) {
@@ -901,8 +921,8 @@ msv_group_kernel(MsvGroup<G> A) {
     }
     int tn = t + 1;
     if (tn >= tend) {
-      tn = wave_fetch_add(work, 1) * kMsvRun;
-      tend = min(tn + kMsvRun, n);
+      tn = runs.next() * runs.run;
+      tend = min(tn + runs.run, n);
     }
     if (tn < n) {
       Lnext = uni(D0.len[tn]);
@@ -1068,7 +1088,10 @@ __device__ __forceinline__ VitResult vit16_target(const uint32_t *__restrict__ e
     // A chain can cross into the next slot only from a slot whose last
     // delete value is above the floor (sat(tau + DD) <= tau <= D): when every
     // slot's last value is at the floor, nothing is left to propagate.
-    if (any_lane(D[Q - 1] != tau2)) {
+    // (and nothing moves unless some slot's first cell improves: one test
+    // rules that out in the common case)
+    if (any_lane(D[Q - 1] != tau2) &&
+        any_lane(i16_max(D[0], i16_adds(slot_up16(D[Q - 1]), tr[TR_DDIN][0])) != D[0])) {
       for (int it = 0; it < 2 * kWave; it++) {
         dc = slot_up16(D[Q - 1]);
         bool moved = true;
@@ -1212,19 +1235,23 @@ __device__ __forceinline__ int vit32_target(const int *emit, const int (&tr)[TR_
       D[q] = max(max(sadd32(q ? M[q - 1] : din, TR(TR_MDIN, q)), sadd32(dc, TR(TR_DDIN, q))), tau);
       dc = D[q];
     }
-    for (int it = 0; it < kWave; it++) {
-      dc = lane_up_i(D[Q - 1]);
-      bool moved = true;
+    // Chains crossing into the next lane: nothing moves unless some lane's
+    // first cell improves, which this one test rules out in the common case.
+    if (any_lane(lane_up_i(D[Q - 1]) + TR(TR_DDIN, 0) > D[0])) {
+      for (int it = 0; it < kWave; it++) {
+        dc = lane_up_i(D[Q - 1]);
+        bool moved = true;
 #pragma unroll
-      for (int q = 0; q < Q; q++) {
-        if (moved) {
-          const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= tau >= -2^30 already
-          moved = any_lane(nd != D[q]);
-          D[q] = nd;
-          dc = nd;
+        for (int q = 0; q < Q; q++) {
+          if (moved) {
+            const int nd = max(D[q], dc + TR(TR_DDIN, q));   // D[q] >= tau >= -2^30 already
+            moved = any_lane(nd != D[q]);
+            D[q] = nd;
+            dc = nd;
+          }
         }
+        if (!moved) break;
       }
-      if (!moved) break;
     }
     if (any_lane(accM >= T)) {
       const int m = wave_max_i32(accM);
