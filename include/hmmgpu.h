@@ -342,7 +342,8 @@ int hmm_db_stage_timing(hmm_db *db, int32_t capacity);
  * the database, forked from and joined back into the search stream): both
  * are timed from the end of the int16 Viterbi stage, the rescore to its own
  * end and Forward to the end of both, so Forward's figure is the time the
- * two together add to the search.  At most `cap` searches are returned,
+ * two together add to the search.  When the three stages after MSV run as
+ * one kernel (hmm_db_fused_tail), the Viterbi figure holds all three.  At most `cap` searches are returned,
  * their number in *n.  Waits for the recorded searches to finish and
  * clears the record.  Errors: HMM_EINVAL, HMM_EDEVICE. */
 int hmm_db_stage_times(hmm_db *db, float *out_ms, int32_t cap, int32_t *n);
