@@ -38,6 +38,9 @@ def test_stage_roofline_arithmetic():
     # pipelined: only MSV's fraction is meaningful
     piped = bench.stage_roofline([100], 10**9, ran, [10.0, 1.0, 1.0, 2.0], chunks=2)
     assert set(piped) == {"msv", "note"}
+    # fused tail: one time for Viterbi, rescore and Forward (the Viterbi stage's)
+    fused = bench.stage_roofline([100], 10**9, ran, [10.0, 3.0, 0.01, 0.02], chunks=1, fused=True)
+    assert set(fused) == {"msv", "tail"} and fused["tail"]["ms"] == pytest.approx(3.0)
 
 
 @pytest.mark.parametrize("name", ["msv_traffic_C3.json", "decode_traffic_C3.json"])
