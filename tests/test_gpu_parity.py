@@ -395,6 +395,24 @@ def test_fused_and_staged_tails_agree(M):
                 assert np.array_equal(got[1][k], got[2][k]), k
             assert np.array_equal(got[1]["fwd"].view(np.uint32), got[2]["fwd"].view(np.uint32))
             announce(f"tails M={M} F={F} agree {st}")
+    # with the composition-bias filter between MSV and Viterbi (its own
+    # parity test covers the oracle side): the two tails agree bit for bit
+    got = {}
+    for mode in (1, 2):
+        P = hg.Profile(peaked, -8.0, -9.0, -4.0)
+        D = hg.Database(res, off)
+        hg.hmm_db_fused_tail(D.handle, mode)
+        out = hg.alloc_results(D.n)
+        hg.search(P, D, (0.5, 1.0, 1.0), out, bias_filter=True)
+        torch.cuda.synchronize()
+        got[mode] = {k: v.cpu().numpy() for k, v in out.items()}
+        P.close()
+        D.close()
+    for k in ("msv", "vit", "flags", "counts"):
+        assert np.array_equal(got[1][k], got[2][k]), f"bias filter: {k}"
+    assert np.array_equal(got[1]["fwd"].view(np.uint32), got[2]["fwd"].view(np.uint32))
+    assert np.array_equal(got[1]["bias"].view(np.uint32), got[2]["bias"].view(np.uint32))
+    assert np.any((got[2]["flags"] & hg.HMM_FWD_RAN) != 0)
 
 
 @pytest.mark.parametrize("M", [700, 900, 1500, 2600])
