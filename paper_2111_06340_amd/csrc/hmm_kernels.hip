@@ -1460,8 +1460,9 @@ __global__ void __launch_bounds__(kThreads32) fwd_kernel(DevProfile P, DevDb db,
 // for the longest target of the stage before them; here a target's stages
 // follow each other without waiting for any other target, and a launch ends
 // when its last wave's chain of stages does.  The three emission tables sit
-// in LDS side by side (10 KB per int16 vector, 20 KB per 32-bit vector,
-// twice); transitions are read per target and stage, so that no stage's
+// in LDS side by side (10 KB per vector of each: the int16 Viterbi's per
+// int16 vector, the rescore's and Forward's per 32-bit vector);
+// transitions are read per target and stage, so that no stage's
 // registers stay live through the others.  Results, flags and counts are
 // the staged kernels' (the survivor lists between the stages are not
 // written).
